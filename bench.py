@@ -1,0 +1,364 @@
+#!/usr/bin/env python3
+"""Throughput of the Grouped Cross Attention hot path on one MI355X.
+
+One step = the whole path over one batch of the 64K-context training workload
+(B=2, H=16, d=64, L=65,536, S=64, 1,024 chunks, top-8, bf16): landmark scores,
+top-k, grouped cross attention forward, and its backward into q, k, v, the
+retrieval scores and both landmark tensors.  Inputs are seeded synthetic
+N(0,1) tensors already resident in HBM when the timed region starts.
+
+Prints ONE JSON line.  Besides the headline tokens/s it carries:
+  roofline     - the dominant kernel's achieved rate against its roofline peak,
+                 from HIP events recorded after every kernel on the stream the
+                 kernels run on, over the timed region;
+  cpu_baseline - the CPU oracle timed on a bounded sample of the same workload;
+  decode_scan  - the 16M-context decode retrieval (one 64-token chunk scored
+                 against 262,144 past landmark keys, top-8, attention over the
+                 8 gathered chunks) in GB/s against HBM peak.
+"""
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+S, DH = 64, 64
+
+
+# ------------------------------------------------------------ HIP events ----
+
+class Events:
+    """Raw hipEvent_t handles (the library records them on the kernels' stream)."""
+
+    def __init__(self, n):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.n = n
+        self.arr = (ctypes.c_void_p * n)()
+        for i in range(n):
+            assert self.hip.hipEventCreate(ctypes.byref(self.arr, i * ctypes.sizeof(ctypes.c_void_p))) == 0
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+
+    def record(self, i, stream):
+        assert self.hip.hipEventRecord(self.arr[i], ctypes.c_void_p(stream.cuda_stream)) == 0
+
+    def ms(self, a, b):
+        out = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(out), self.arr[a], self.arr[b]) == 0
+        return out.value
+
+    def close(self):
+        for i in range(self.n):
+            self.hip.hipEventDestroy(self.arr[i])
+
+
+def kernel_times(run_step, steps, stream, gca, per_step_capacity=32):
+    """Run `steps` steps with the per-kernel hook armed.  Returns (total ms,
+    {kernel: [durations ms]}) where each duration is the time between the event
+    after the previous kernel (or the step start) and the event after this one."""
+    import torch
+    starts = Events(steps + 1)
+    evs = Events(steps * per_step_capacity)
+    torch.cuda.synchronize()
+    gca.profile_arm(evs.arr, evs.n)
+    bounds = []
+    for s in range(steps):
+        starts.record(s, stream)
+        lo = gca.lib().gca_profile_count()
+        run_step()
+        bounds.append((lo, gca.lib().gca_profile_count()))
+    starts.record(steps, stream)
+    torch.cuda.synchronize()
+    names = gca.profile_record()
+    gca.profile_arm(None, 0)
+    per = {}
+    for s, (lo, hi) in enumerate(bounds):
+        for i in range(lo, hi):
+            d = evs.ms(i - 1, i) if i > lo else _ms_between(starts, s, evs, i)
+            per.setdefault(names[i], []).append(d)
+    total = starts.ms(0, steps)
+    starts.close()
+    evs.close()
+    return total, per
+
+
+def _ms_between(ev_a, ia, ev_b, ib):
+    out = ctypes.c_float()
+    assert ev_a.hip.hipEventElapsedTime(ctypes.byref(out), ev_a.arr[ia], ev_b.arr[ib]) == 0
+    return out.value
+
+
+# ------------------------------------------------------------ workloads ----
+
+def upload(w, a, dev):
+    import numpy as np
+    import torch
+    a = np.ascontiguousarray(a)
+    if w.dtype == "bf16":
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+    return torch.from_numpy(a).to(dev)
+
+
+def landmarks(w):
+    """Seeded landmark inputs from the shared generator (throughput does not need the
+    parity tests' top-k margin check)."""
+    from gen import inputs as gi
+    return gi.draw_landmarks(w)
+
+
+def valid_units(idx_host, w):
+    """Valid (batch, head, query chunk, slot) tuples the attention kernels process."""
+    import numpy as np
+    valid = (idx_host >= 0)
+    if w.mode == "causal":
+        per_row = valid[:, :, :-1, :].sum()      # row t feeds chunk t+1
+    else:
+        per_row = valid.sum()
+    heads_per_rhead = w.H // w.Hr
+    return int(per_row) * heads_per_rhead
+
+
+def flops_per_unit():
+    # per valid (query token, slot, head): one S x d product is 2*S*d flops
+    return {"xattn_fwd_kernel": 2 * (2 * S * DH),     # S = QK^T and PV
+            "bwd_dq_kernel": 3 * (2 * S * DH),        # S recompute, dP = dO V^T, dQ = dS K
+            "bwd_dkdv_kernel": 2 * (2 * S * DH)}      # dV = P^T dO, dK = dS^T Q (its own S/dP recompute not counted)
+
+
+def bench_train(args, dev, gca):
+    import numpy as np
+    import torch
+    from gen import get_workload, inputs as gi
+
+    w = get_workload("fwdbwd_64k_bf16")
+    lq, lk = landmarks(w)
+    t = {"lmk_q": upload(w, lq, dev), "lmk_k": upload(w, lk, dev)}
+    t.update(gi.device_tensors(w, ("q", "k", "v", "dout"), dev))
+    p = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode)
+    sh = gca.shapes(p)
+    fo = {"out": torch.empty(sh.q, dtype=torch.bfloat16, device=dev),
+          "idx": torch.empty(sh.rows, dtype=torch.int32, device=dev),
+          "sel": torch.empty(sh.rows, dtype=torch.float32, device=dev),
+          "lse": torch.empty(sh.lse, dtype=torch.float32, device=dev),
+          "w": torch.empty(sh.rows, dtype=torch.float32, device=dev)}
+    grads = {"dq": torch.empty(sh.q, dtype=torch.bfloat16, device=dev),
+             "dk": torch.empty(sh.kv, dtype=torch.bfloat16, device=dev),
+             "dv": torch.empty(sh.kv, dtype=torch.bfloat16, device=dev),
+             "dsel": torch.empty(sh.rows, dtype=torch.float32, device=dev),
+             "dlmk_q": torch.empty(sh.lmk_q, dtype=torch.float32, device=dev),
+             "dlmk_k": torch.empty(sh.lmk_k, dtype=torch.float32, device=dev)}
+    wsf, _ = gca.workspace(p, gca.OP_FORWARD, dev)
+    wsb, _ = gca.workspace(p, gca.OP_BACKWARD, dev)
+
+    def step():
+        gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"], out=fo["out"], idx=fo["idx"],
+                    sel=fo["sel"], lse=fo["lse"], w=fo["w"], ws=wsf)
+        gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], fo["idx"], fo["sel"], fo["lse"], t["dout"],
+                              t["lmk_q"], t["lmk_k"], ws=wsb, grads=grads)
+
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    # timed region: K steps, bracketed by synchronisation, per-kernel events armed
+    t0 = time.perf_counter()
+    total_ms, per = kernel_times(step, args.steps, stream, gca)
+    wall = time.perf_counter() - t0
+    ms_step = total_ms / args.steps
+    tokens = w.B * w.Lq
+    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step (wall {wall:.2f}s)", file=sys.stderr,
+          flush=True)
+
+    idx_host = fo["idx"].cpu().numpy()
+    units = valid_units(idx_host, w)
+    fpu = flops_per_unit()
+    kern = {}
+    for name, ds in per.items():
+        avg = sum(ds) / len(ds)
+        kern[name] = {"avg_ms": avg, "launches_per_step": len(ds) / args.steps,
+                      "ms_per_step": sum(ds) / args.steps}
+        if name in fpu:
+            fl = units * S * fpu[name]
+            kern[name]["tflops"] = fl / (avg * 1e-3) / 1e12
+    dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
+    if dom in fpu:
+        ach = kern[dom]["tflops"]
+        roof = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": ach / BF16_PEAK_TFLOPS, "traffic": None,
+                "algorithmic_flops_per_launch": units * S * fpu[dom], "avg_launch_ms": kern[dom]["avg_ms"]}
+    else:
+        roof = {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
+                "traffic": None}
+    algo_fl = units * S * (fpu["xattn_fwd_kernel"] + 5 * 2 * S * DH)
+    return {
+        "w": w, "t": t, "tokens": tokens, "ms_step": ms_step, "kernels": kern, "roofline": roof,
+        "units": units, "path_tflops": algo_fl / (ms_step * 1e-3) / 1e12,
+    }
+
+
+def cpu_baseline(w, t, heads=2):
+    """The oracle (as it stands) on a bounded sample: batch 0's scores and top-k over
+    all 1,024 landmark rows, then attention forward and backward for `heads` heads of
+    batch 0 over every chunk.  Extrapolated to the whole batch in tokens/s."""
+    import numpy as np
+    from gen import inputs as gi
+    from oracle import gca as og
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = 1
+
+    def host(x):
+        return x.float().cpu().double().numpy()
+
+    lq = host(t["lmk_q"][:1])
+    lk = host(t["lmk_k"][:1])
+    t0 = time.perf_counter()
+    r = og.scores(lq, lk, w.score_scale, w.mode)
+    idx, sel = og.topk(r, w.topk)
+    wt = og.fusion_weights(sel)
+    t_sel = time.perf_counter() - t0
+    q = host(t["q"][:1, :heads])
+    k = host(t["k"][:1, :heads])
+    v = host(t["v"][:1, :heads])
+    do = host(t["dout"][:1, :heads])
+    t1 = time.perf_counter()
+    og.xattn_fwd(q, k, v, idx, wt, w.S, w.attn_scale, w.mode)
+    og.xattn_bwd(q, k, v, idx, wt, do, w.S, w.attn_scale, w.mode)
+    t_attn = time.perf_counter() - t1
+    full = w.B * t_sel + (w.B * w.H / heads) * t_attn
+    return {"value": w.B * w.Lq / full, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"batch 0: scores+top-k over all {w.n_chunks} landmark rows ({t_sel:.2f}s), then "
+                      f"attention fwd+bwd for {heads} of {w.H} heads over all chunks ({t_attn:.2f}s); "
+                      f"extrapolated to B={w.B}, H={w.H}",
+            "sample_seconds": t_sel + t_attn}
+
+
+def bench_decode(args, dev, gca):
+    """16M-context decode retrieval: GB/s of algorithmic bytes against HBM peak."""
+    import numpy as np
+    import torch
+    from gen import get_workload, inputs as gi
+
+    w = get_workload("decode_16m_bf16")
+    lq, lk = landmarks(w)
+    lmk_q = upload(w, lq, dev)
+    keys = [upload(w, lk, dev)]
+    keys.append(keys[0].clone())                   # 2 x 268 MB: rotation defeats the 256 MB MALL
+    kv = gi.device_kv(w, dev)
+    q = gi.device_tensors(w, ("q",), dev)["q"]
+    p = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode)
+    sh = gca.shapes(p)
+    out = torch.empty(sh.q, dtype=torch.bfloat16, device=dev)
+    idx = torch.empty(sh.rows, dtype=torch.int32, device=dev)
+    sel = torch.empty(sh.rows, dtype=torch.float32, device=dev)
+    lse = torch.empty(sh.lse, dtype=torch.float32, device=dev)
+    wts = torch.empty(sh.rows, dtype=torch.float32, device=dev)
+    ws, _ = gca.workspace(p, gca.OP_FORWARD, dev)
+    it = [0]
+
+    def call():
+        gca.forward(p, lmk_q, keys[it[0] % 2], q, kv["k"], kv["v"], out=out, idx=idx, sel=sel, lse=lse, w=wts,
+                    ws=ws)
+        it[0] += 1
+
+    for _ in range(5):
+        call()
+    torch.cuda.synchronize()
+    steps = args.decode_steps
+    total_ms, per = kernel_times(call, steps, torch.cuda.current_stream(), gca)
+    ms_call = total_ms / steps
+    planted = int(gi.plant_positions(w)[0])
+    found = planted in idx.cpu().numpy().ravel().tolist()
+    key_bytes = w.n_chunks * w.Dl * 2
+    kv_bytes = 2 * w.topk * w.H * S * DH * 2
+    io_bytes = 2 * w.H * S * DH * 2 + w.Dl * 2
+    total_bytes = key_bytes + kv_bytes + io_bytes
+    scan_ms = sum(per["decode_scan_kernel"]) / len(per["decode_scan_kernel"])
+    kern = {k: {"avg_ms": sum(v) / len(v)} for k, v in per.items()}
+    scan_gbs = key_bytes / (scan_ms * 1e-3) / 1e9
+    del kv, keys
+    torch.cuda.empty_cache()
+    return {
+        "metric": "retrieval-scan GB/s at 16M-ctx decode", "unit": "GB/s",
+        "value": total_bytes / (ms_call * 1e-3) / 1e9, "ms_per_call": ms_call, "calls": steps,
+        "bytes_per_call": total_bytes, "frac_of_hbm_peak": total_bytes / (ms_call * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "planted_retrieved": found,
+        "config": {"workload": "decode_16m_bf16: B=1 H=8 d=64, 16,777,216 past tokens (262,144 chunks), "
+                               "S=64, top-8, D=512, bf16"},
+        "roofline": {"kernel": "decode_scan_kernel", "bound": "hbm", "achieved": scan_gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": scan_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": key_bytes, "avg_launch_ms": scan_ms},
+        "kernels": kern,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--decode-steps", type=int, default=50)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the GCA path here runs on a single MI355X with no "
+              "collectives, so --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    from paper_2410_01651_amd import build as _b
+    if not os.path.exists(_b.OUT):
+        _b.build()
+    from paper_2410_01651_amd import gca
+    dev = torch.device("cuda:0")
+
+    tr = bench_train(args, dev, gca)
+    w = tr["w"]
+    line = {
+        "metric": "GCA fwd+bwd tokens/s at 64K ctx; retrieval-scan GB/s at 16M-ctx decode",
+        "value": tr["tokens"] / (tr["ms_step"] * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": tr["ms_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "fwdbwd_64k_bf16: B=2 H=16 d=64 L=65,536 S=64 (1,024 chunks) top-8 D=1,024, "
+                               "bf16 in / fp32 accumulate; forward (scores, top-k, grouped cross attention) + "
+                               "backward (dq, dk, dv, dsel, dlmk_q, dlmk_k)",
+                   "global_batch": w.B, "seq_len": w.Lq, "parallelism": "none (1 GPU)"},
+        "roofline": tr["roofline"],
+        "path_algorithmic_tflops": tr["path_tflops"],
+        "kernels": tr["kernels"],
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle sample)", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(w, tr["t"])
+    del tr
+    torch.cuda.empty_cache()
+    if not args.no_decode:
+        print("[bench] decode scan at 16M context", file=sys.stderr, flush=True)
+        line["decode_scan"] = bench_decode(args, dev, gca)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -145,19 +145,21 @@ def draw_inputs(w: Workload, attempt: int = 0, tokens: bool = True):
     return inp
 
 
-def device_kv(w: Workload, device, torch_mod=None):
-    """K/V cache drawn on the device for workloads too large for the host.
+def device_tensors(w: Workload, names, device, torch_mod=None):
+    """Per-token tensors drawn on the device, for workloads too large for the host.
 
-    Each (b, h) slice of k and v is i.i.d. N(0,1) from a torch device
-    generator seeded with ``seed * 1_000_003 + tensor_id * 10_007 + b * 131 + h``
-    and stored as bf16.  Tests read back only the chunks they need.
+    Each (b, h) slice of each named tensor (q and dout are [B,H,Lq,d], k and v
+    [B,H,Lkv,d]) is i.i.d. N(0,1) from a torch device generator seeded with
+    ``seed * 1_000_003 + tensor_id * 10_007 + b * 131 + h`` and stored in the
+    workload dtype.  Tests read back only the slices they need.
     """
     import torch as _t
     torch = torch_mod or _t
     dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     out = {}
-    for name in ("k", "v"):
-        t = torch.empty((w.B, w.H, w.Lkv, w.d), dtype=dt, device=device)
+    for name in names:
+        rows = w.Lq if name in ("q", "dout") else w.Lkv
+        t = torch.empty((w.B, w.H, rows, w.d), dtype=dt, device=device)
         for b in range(w.B):
             for h in range(w.H):
                 g = torch.Generator(device=device)
@@ -165,3 +167,8 @@ def device_kv(w: Workload, device, torch_mod=None):
                 t[b, h].normal_(generator=g)
         out[name] = t
     return out
+
+
+def device_kv(w: Workload, device, torch_mod=None):
+    """The K/V cache of a workload drawn on the device (see device_tensors)."""
+    return device_tensors(w, ("k", "v"), device, torch_mod)

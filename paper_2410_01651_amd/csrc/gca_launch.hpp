@@ -1,0 +1,59 @@
+// Host-side launchers shared between the C ABI (api.cpp) and the kernel files.
+// Every launcher enqueues on `stream` and returns the hipError_t of its last
+// launch; shapes have been validated by the caller.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace gca {
+
+struct Shape {
+  int B, H, Hr, D, topk;
+  int64_t nQ;      // landmark query rows (query chunks)
+  int64_t nKV;     // key/value chunks (score columns)
+  int causal;      // 1: row t feeds chunk t+1 and sees chunks [0,t); 0: decode
+  int bf16;        // element type of tensors: 1 bf16, 0 fp32
+  int off_by_one;
+  float score_scale, attn_scale;
+};
+
+// Eq. 1 scores, written as a [B,Hr,nQ,nKV] fp32 matrix.
+hipError_t launch_chunk_scores(const Shape& s, const void* lmk_q, const void* lmk_k, float* scores,
+                               hipStream_t stream);
+// Eq. 1 top-k over a score matrix.
+hipError_t launch_topk(const Shape& s, const float* scores, int32_t* idx, float* sel,
+                       hipStream_t stream);
+// Decode: split scan of all past landmark keys, then merge into idx/sel.
+size_t decode_workspace(const Shape& s);
+hipError_t launch_decode_select(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx,
+                                float* sel, void* ws, hipStream_t stream);
+// Causal: scores and top-k in one pass, no score matrix.
+size_t fused_workspace(const Shape& s);
+hipError_t launch_fused_select(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx,
+                               float* sel, void* ws, hipStream_t stream);
+
+// Eq. 2-3 forward.
+hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const void* v,
+                            const int32_t* idx, const float* sel, void* out, float* lse, float* w,
+                            hipStream_t stream);
+
+// Backward (Algorithm 2 and the score/landmark chain rule).
+size_t bwd_workspace(const Shape& s);
+hipError_t launch_xattn_bwd(const Shape& s, const void* q, const void* k, const void* v,
+                            const int32_t* idx, const float* sel, const float* lse, const void* dout,
+                            void* dq, void* dk, void* dv, float* dsel, const void* lmk_q,
+                            const void* lmk_k, float* dlmk_q, float* dlmk_k, void* ws,
+                            hipStream_t stream);
+
+// Called right after every kernel launch: keeps the launch's error (the first
+// one of a sequence) and records the armed profiling event, if any.
+void note_launch(const char* kernel, hipStream_t stream);
+// The first launch error since the last call (hipSuccess if none); clears it.
+hipError_t take_launch_error();
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline int64_t round8(int64_t n) { return (n + 7) & ~int64_t(7); }
+
+}  // namespace gca

@@ -1,0 +1,142 @@
+"""The C ABI on the host: the library loads, exports every entry point that
+include/gca.h declares, sizes workspaces, and rejects malformed calls before
+launching anything (so these run without a GPU: no call here reaches a kernel)."""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from _helpers import ROOT, ensure_built
+
+HEADER = os.path.join(ROOT, "include", "gca.h")
+
+
+@pytest.fixture(scope="module")
+def gca():
+    ensure_built()
+    from paper_2410_01651_amd import gca as g
+    g.lib()
+    return g
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gca_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(gca):
+    names = _declared()
+    assert set(names) == set(gca.EXPORTS)
+    L = gca.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_problem_struct_layout(gca):
+    assert ctypes.sizeof(gca.Problem) == 64
+    assert gca.Problem.n_chunks.offset == 16
+    assert gca.Problem.flags.offset == 56
+
+
+def test_status_strings(gca):
+    L = gca.lib()
+    for s in range(5):
+        assert L.gca_status_string(s).decode().startswith("GCA_")
+    assert b"unknown" in L.gca_status_string(99)
+
+
+def test_workspace_sizes(gca):
+    r = lambda n: (n + 255) // 256 * 256
+    p = gca.problem(2, 16, 1024, 8)                     # materialised scores
+    assert gca.workspace_size(p, gca.OP_FORWARD) == r(4 * 2 * 1024 * 1024)
+    big = gca.problem(1, 8, 16384, 8)                   # 1 GiB matrix -> single-pass select
+    assert gca.workspace_size(big, gca.OP_FORWARD) == 0
+    forced = gca.problem(1, 8, 16384, 8, flags=gca.FLAG_MATERIALIZE)
+    assert gca.workspace_size(forced, gca.OP_FORWARD) == r(4 * 16384 * 16384)
+    dec = gca.problem(1, 8, 262144, 8, mode="decode")
+    assert 0 < gca.workspace_size(dec, gca.OP_FORWARD) < 1 << 20
+    bwd = gca.workspace_size(p, gca.OP_BACKWARD)
+    assert bwd >= 4 * 2 * 16 * 1024 * 64 * 8            # D per (token, slot) at least
+    bad = gca.problem(1, 1, 16, 2, d=32)
+    assert gca.workspace_size(bad, gca.OP_FORWARD) == 0
+    assert gca.workspace_size(p, 7) == 0
+
+
+FAKE = ctypes.c_void_p(1 << 20)   # aligned, never dereferenced: validation fails first
+
+
+def _fwd_call(gca, p, **override):
+    args = dict(lmk_q=FAKE, lmk_k=FAKE, q=FAKE, k=FAKE, v=FAKE, out=FAKE, idx=FAKE, sel=FAKE,
+                lse=None, w=None, ws=None, nbytes=0)
+    args.update(override)
+    L = gca.lib()
+    st = L.gca_forward(ctypes.byref(p), args["lmk_q"], args["lmk_k"], args["q"], args["k"], args["v"],
+                       args["out"], args["idx"], args["sel"], args["lse"], args["w"], args["ws"],
+                       ctypes.c_size_t(args["nbytes"]), None)
+    return st, L.gca_last_error().decode()
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("d", 32, "UNSUPPORTED"), ("S", 128, "UNSUPPORTED"), ("topk", 0, "INVALID"),
+    ("topk", 33, "UNSUPPORTED"), ("Hr", 3, "INVALID"), ("D", 96, "UNSUPPORTED"), ("D", 0, "INVALID"),
+    ("n_chunks", 0, "INVALID"), ("B", 0, "INVALID"), ("dtype", 5, "INVALID"), ("mode", 2, "INVALID"),
+    ("off_by_one", 2, "INVALID"), ("flags", 3, "INVALID"), ("flags", 8, "INVALID"),
+    ("attn_scale", math.inf, "INVALID"),
+])
+def test_invalid_problem_rejected(gca, field, value, status):
+    p = gca.problem(1, 4, 64, 8)
+    setattr(p, field, value)
+    st, msg = _fwd_call(gca, p)
+    assert st == getattr(gca, "GCA_ERR_" + status), msg
+    assert msg
+
+
+@pytest.mark.parametrize("arg", ["lmk_q", "lmk_k", "q", "k", "v", "out", "idx", "sel"])
+def test_null_required_pointer(gca, arg):
+    p = gca.problem(1, 4, 64, 8)
+    n = gca.workspace_size(p, gca.OP_FORWARD)
+    st, msg = _fwd_call(gca, p, ws=FAKE, nbytes=n, **{arg: None})
+    assert st == gca.GCA_ERR_INVALID and arg in msg
+
+
+def test_misaligned_pointer(gca):
+    p = gca.problem(1, 4, 64, 8)
+    st, msg = _fwd_call(gca, p, q=ctypes.c_void_p((1 << 20) + 8))
+    assert st == gca.GCA_ERR_INVALID and "aligned" in msg
+
+
+def test_workspace_checks(gca):
+    p = gca.problem(1, 4, 64, 8)
+    n = gca.workspace_size(p, gca.OP_FORWARD)
+    st, msg = _fwd_call(gca, p, ws=None, nbytes=0)
+    assert st == gca.GCA_ERR_WORKSPACE
+    st, msg = _fwd_call(gca, p, ws=FAKE, nbytes=n - 1)
+    assert st == gca.GCA_ERR_WORKSPACE and "too small" in msg
+    st, msg = _fwd_call(gca, p, ws=ctypes.c_void_p((1 << 20) + 16), nbytes=n)
+    assert st == gca.GCA_ERR_WORKSPACE and "aligned" in msg
+
+
+def test_backward_argument_rules(gca):
+    L = gca.lib()
+    p = gca.problem(1, 4, 64, 8)
+    n = gca.workspace_size(p, gca.OP_BACKWARD)
+
+    def call(lmk_q, lmk_k, dlq, dlk, ws=FAKE, nbytes=n):
+        return L.gca_grouped_xattn_bwd(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                       FAKE, FAKE, lmk_q, lmk_k, dlq, dlk, ws, ctypes.c_size_t(nbytes), None)
+    assert call(FAKE, None, FAKE, None) == gca.GCA_ERR_INVALID          # dlmk_q without lmk_k
+    assert call(None, FAKE, None, FAKE) == gca.GCA_ERR_INVALID          # dlmk_k without lmk_q
+    assert call(None, None, None, None, ws=FAKE, nbytes=n - 256) == gca.GCA_ERR_WORKSPACE
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """The binding raises when libgca is absent instead of computing anything itself."""
+    from paper_2410_01651_amd import gca as g
+    monkeypatch.setattr(g, "LIB_PATH", str(tmp_path / "nope.so"))
+    monkeypatch.setattr(g, "_lib", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        g.lib()

@@ -1,0 +1,246 @@
+"""GPU parity of every libgca entry point against the CPU oracle.
+
+Inputs are seeded and margin-checked (the k-th and (k+1)-th landmark scores of
+every row differ by >= 1e-3), so top-k indices must match bit-exactly; floating
+outputs must match within max-abs-rel 1e-4 (fp32) or 2e-2 (bf16).  Shapes here
+are small enough for the oracle to run in seconds while spanning several tiles
+and ragged tails; the full workload sizes are in test_gpu_workloads.py.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+from _helpers import TOL, decode_all, ensure_built, host64, max_abs_rel, oracle_params, problem_for, upload
+from gen import get_workload, inputs as gi
+from oracle import gca as og, margins
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ensure_built()
+    return torch.device("cuda:0")
+
+
+def _case(name, **kw):
+    w = get_workload(name, **kw)
+    inp, _ = margins.checked_inputs(w)
+    return w, inp
+
+
+def _check_forward(w, inp, f, off_by_one=False, tol=None):
+    tol = tol or TOL[w.dtype]
+    x = decode_all(w, inp)
+    ref = og.forward(oracle_params(w, off_by_one), x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"])
+    np.testing.assert_array_equal(f["idx"].cpu().numpy(), ref["idx"])
+    assert max_abs_rel(host64(f["sel"]), ref["sel"]) <= tol
+    if f.get("w") is not None:
+        assert max_abs_rel(host64(f["w"]), ref["w"]) <= tol
+    assert max_abs_rel(host64(f["out"]), ref["out"]) <= tol
+    if f.get("lse") is not None:
+        assert max_abs_rel(host64(f["lse"]), ref["lse"]) <= tol
+    return ref
+
+
+def test_tiny_fp32_forward(dev):
+    """1,024 tokens, 16 chunks, top-2, fp32: the whole forward against the oracle."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case("tiny_fp32_1k")
+    t = upload(w, inp, dev)
+    f = gca.forward(problem_for(w), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    ref = _check_forward(w, inp, f)
+    out = f["out"].cpu().numpy()
+    assert np.all(out[:, :, :2 * w.S] == 0.0)          # chunks 0 and 1 retrieve nothing
+    assert np.all(ref["idx"][0, 0, 0] == -1)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_stepwise_equals_forward(dev, dtype):
+    """gca_chunk_scores -> gca_topk -> gca_grouped_xattn_fwd gives what gca_forward gives."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case("train_16k_bf16", B=2, H=3, n_chunks=70, topk=5, dtype=dtype)
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    sc = gca.chunk_scores(p, t["lmk_q"], t["lmk_k"])
+    idx, sel = gca.topk(p, sc)
+    out, lse, wt = gca.grouped_xattn_fwd(p, t["q"], t["k"], t["v"], idx, sel)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    assert np.array_equal(idx.cpu().numpy(), f["idx"].cpu().numpy())
+    assert np.array_equal(sel.cpu().numpy(), f["sel"].cpu().numpy())
+    assert np.array_equal(host64(out), host64(f["out"]))
+    assert np.array_equal(lse.cpu().numpy(), f["lse"].cpu().numpy())
+    _check_forward(w, inp, dict(f, w=wt))
+    x = decode_all(w, inp)
+    rs = og.scores(x["lmk_q"], x["lmk_k"], w.score_scale)
+    assert max_abs_rel(host64(sc), rs) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_topk_ties_to_lower_chunk(dev, dtype):
+    """Score rows full of exact ties: the chosen set is decided by (score desc, chunk asc)."""
+    import torch
+    from paper_2410_01651_amd import gca
+    rng = np.random.default_rng(5)
+    for nC, k in ((16, 2), (100, 8), (300, 32), (1000, 17)):
+        p = gca.problem(2, 1, nC, k, D=64, dtype=dtype)
+        r = rng.integers(-4, 5, size=(2, 1, nC, nC)).astype(np.float32)
+        r = np.where(np.arange(nC)[None, :] < np.arange(nC)[:, None], r, -np.inf).astype(np.float32)
+        idx, sel = gca.topk(p, torch.from_numpy(r).to(dev))
+        ri, rs = og.topk(r.astype(np.float64), k)
+        np.testing.assert_array_equal(idx.cpu().numpy(), ri)
+        np.testing.assert_array_equal(sel.cpu().numpy(), rs.astype(np.float32))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_fused_select_equals_oracle(dev, dtype):
+    """The single-pass causal select (no score matrix) against the oracle and the
+    materialised path."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case("planted_1m_bf16", H=2, n_chunks=300, dtype=dtype)
+    t = upload(w, inp, dev)
+    fa = gca.forward(problem_for(w, flags=gca.FLAG_FUSED_TOPK), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    fb = gca.forward(problem_for(w, flags=gca.FLAG_MATERIALIZE), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    assert np.array_equal(fa["idx"].cpu().numpy(), fb["idx"].cpu().numpy())
+    ref = _check_forward(w, inp, fa)
+    assert list(ref["idx"][0, 0, -1]) == list(gi.plant_positions(w))
+
+
+SWEEP = [
+    # name, overrides, off_by_one
+    ("train_16k_bf16", dict(B=1, H=2, n_chunks=1, topk=4), False),       # single chunk: all empty
+    ("train_16k_bf16", dict(B=2, H=2, n_chunks=3, topk=8), False),       # k > history
+    ("train_16k_bf16", dict(B=1, H=4, n_chunks=9, topk=1), False),       # k = 1
+    ("train_16k_bf16", dict(B=1, H=4, Hr=4, D=64, n_chunks=33, topk=3), False),   # per-head retrieval
+    ("train_16k_bf16", dict(B=2, H=2, n_chunks=65, topk=32), True),      # off-by-one, k = 32
+    ("tiny_fp32_1k", dict(B=2, H=3, n_chunks=37, topk=6, whole_reseed=False), True),
+    ("tiny_fp32_1k", dict(B=1, H=2, Hr=2, D=128, n_chunks=20, topk=9, whole_reseed=False), False),
+    ("decode_16m_bf16", dict(H=4, n_chunks=3000, device_kv=False), False),
+    ("decode_16m_bf16", dict(H=2, n_chunks=500, topk=32, dtype="fp32", device_kv=False), True),
+    ("decode_16m_bf16", dict(H=2, Hr=2, D=64, n_chunks=5, topk=8, device_kv=False), False),
+]
+
+
+@pytest.mark.parametrize("name,kw,obo", SWEEP)
+def test_forward_sweep(dev, name, kw, obo):
+    from paper_2410_01651_amd import gca
+    w, inp = _case(name, **kw)
+    t = upload(w, inp, dev)
+    f = gca.forward(problem_for(w, off_by_one=obo), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    _check_forward(w, inp, f, off_by_one=obo)
+
+
+BWD = [
+    ("tiny_fp32_1k", dict(B=1, H=2, n_chunks=16, topk=2), False),
+    ("tiny_fp32_1k", dict(B=2, H=2, n_chunks=21, topk=4, whole_reseed=False), True),
+    ("tiny_fp32_1k", dict(B=1, H=3, Hr=3, D=64, n_chunks=12, topk=3, whole_reseed=False), False),
+    ("fwdbwd_64k_bf16", dict(B=2, H=3, n_chunks=40, topk=8), False),
+    ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=70, topk=20), True),
+    ("fwdbwd_64k_bf16", dict(B=1, H=2, Hr=2, D=128, n_chunks=33, topk=5), False),
+    ("decode_16m_bf16", dict(H=2, n_chunks=300, planted=0, backward=True, device_kv=False), False),
+    ("decode_16m_bf16", dict(H=2, n_chunks=100, topk=4, planted=0, dtype="fp32", backward=True,
+                             device_kv=False), False),
+]
+
+
+@pytest.mark.parametrize("name,kw,obo", BWD)
+def test_backward(dev, name, kw, obo):
+    """dq, dk, dv, dsel and both landmark gradients against the oracle's chain rule."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case(name, **kw)
+    if "dout" not in inp:
+        inp["dout"] = gi.draw_slices(w, "dout", (w.B, w.H, w.Lq, w.d))
+    t = upload(w, inp, dev)
+    p = problem_for(w, off_by_one=obo)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                              t["lmk_q"], t["lmk_k"])
+    x = decode_all(w, inp)
+    pp = oracle_params(w, obo)
+    rf = og.forward(pp, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"])
+    np.testing.assert_array_equal(f["idx"].cpu().numpy(), rf["idx"])
+    rb = og.backward(pp, rf, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"], x["dout"])
+    tol = TOL[w.dtype]
+    for key in ("dq", "dk", "dv", "dsel", "dlmk_q", "dlmk_k"):
+        e = max_abs_rel(host64(g[key]), rb[key])
+        assert e <= tol, (key, e)
+    # the score gradient sums to zero over each row's slots
+    assert np.abs(host64(g["dsel"]).sum(-1)).max() <= 1e-5 * max(1.0, np.abs(rb["dsel"]).max())
+
+
+def test_backward_saturated_weights(dev):
+    """A planted chunk takes weight 1 - O(e^-85): the score gradient vanishes (in absolute
+    terms) and the token gradients equal single-chunk attention's."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case("decode_16m_bf16", H=2, n_chunks=300, backward=True, device_kv=False)
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                              t["lmk_q"], t["lmk_k"])
+    x = decode_all(w, inp)
+    pp = oracle_params(w)
+    rf = og.forward(pp, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"])
+    np.testing.assert_array_equal(f["idx"].cpu().numpy(), rf["idx"])
+    assert int(gi.plant_positions(w)[0]) in list(rf["idx"][0, 0, 0])
+    rb = og.backward(pp, rf, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"], x["dout"])
+    assert np.abs(rb["dsel"]).max() < 1e-30
+    assert np.abs(host64(g["dsel"])).max() <= 1e-6
+    for key in ("dq", "dk", "dv"):
+        assert max_abs_rel(host64(g[key]), rb[key]) <= TOL[w.dtype], key
+
+
+def test_backward_deterministic(dev):
+    """No floating-point atomics: two backward passes are bit-identical."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case("fwdbwd_64k_bf16", B=1, H=4, n_chunks=96, topk=8)
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    g1 = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                               t["lmk_q"], t["lmk_k"])
+    g2 = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                               t["lmk_q"], t["lmk_k"])
+    for key in g1:
+        assert np.array_equal(host64(g1[key]), host64(g2[key])), key
+
+
+def test_xattn_only_entry_points(dev):
+    """gca_grouped_xattn_fwd / _bwd driven with an index set chosen by the caller,
+    including pad slots in the middle and an out-of-range index (treated as a pad)."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w = get_workload("tiny_fp32_1k", B=1, H=2, n_chunks=10, topk=4, whole_reseed=False)
+    inp = gi.draw_tokens(w, with_dout=True)
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    nC, k = w.n_chunks, w.topk
+    idx = np.full((1, 1, nC, k), -1, np.int32)
+    sel = np.full((1, 1, nC, k), -np.inf, np.float32)
+    rng = np.random.default_rng(3)
+    for r in range(1, nC):
+        js = sorted(rng.choice(r, size=min(r, 3), replace=False))
+        slots = [0, 2, 3][:len(js)]
+        for s, j in zip(slots, js):
+            idx[0, 0, r, s] = j
+            sel[0, 0, r, s] = rng.standard_normal()
+    idx[0, 0, 5, 1] = 10_000          # out of range -> pad
+    ti, ts = torch.from_numpy(idx).to(dev), torch.from_numpy(sel).to(dev)
+    out, lse, wt = gca.grouped_xattn_fwd(p, t["q"], t["k"], t["v"], ti, ts)
+    x = decode_all(w, inp)
+    idx_ref = np.where(idx >= nC, -1, idx)
+    sel_ref = np.where(idx >= nC, -np.inf, sel).astype(np.float64)
+    w_ref = og.fusion_weights(sel_ref)
+    o_ref, l_ref = og.xattn_fwd(x["q"], x["k"], x["v"], idx_ref, w_ref, w.S, w.attn_scale)
+    assert max_abs_rel(host64(out), o_ref) <= 1e-4
+    assert max_abs_rel(host64(lse), l_ref) <= 1e-4
+    assert max_abs_rel(host64(wt), w_ref) <= 1e-5
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], ti, ts, lse, t["dout"], landmark_grads=False)
+    dq, dk, dv, dw = og.xattn_bwd(x["q"], x["k"], x["v"], idx_ref, w_ref, x["dout"], w.S, w.attn_scale)
+    for key, ref in (("dq", dq), ("dk", dk), ("dv", dv), ("dsel", og.dsel_from_dw(w_ref, dw))):
+        assert max_abs_rel(host64(g[key]), ref) <= 1e-4, key
