@@ -189,8 +189,9 @@ def test_backward_saturated_weights(dev):
     np.testing.assert_array_equal(f["idx"].cpu().numpy(), rf["idx"])
     assert int(gi.plant_positions(w)[0]) in list(rf["idx"][0, 0, 0])
     rb = og.backward(pp, rf, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"], x["dout"])
-    assert np.abs(rb["dsel"]).max() < 1e-30
-    assert np.abs(host64(g["dsel"])).max() <= 1e-6
+    dw = max(1.0, np.abs(rb["dw"]).max())
+    assert np.abs(rb["dsel"]).max() <= 1e-12 * dw          # w = 1 - O(e^-85): only rounding left
+    assert np.abs(host64(g["dsel"])).max() <= 1e-5 * dw
     for key in ("dq", "dk", "dv"):
         assert max_abs_rel(host64(g[key]), rb[key]) <= TOL[w.dtype], key
 

@@ -1,0 +1,192 @@
+"""Parity at the full workload sizes, in the launch configuration bench.py times.
+
+The GPU runs the whole workload; the oracle checks what it can compute one by
+one: top-k indices (exact) on every row or on a seeded sample of rows, and the
+attention outputs / gradients on sampled query chunks, heads or (batch, head)
+slices.  Per-token tensors of the large workloads are drawn on the device by the
+shared seeded generator and only the sampled slices are copied back.
+"""
+
+import numpy as np
+import pytest
+
+from _helpers import TOL, ensure_built, host64, max_abs_rel, oracle_params, problem_for, to_dev
+from gen import get_workload, inputs as gi
+from oracle import gca as og, margins
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ensure_built()
+    return torch.device("cuda:0")
+
+
+def _setup(name, dev, **kw):
+    w = get_workload(name, **kw)
+    inp, _ = margins.checked_inputs(w, tokens=False)
+    t = {"lmk_q": to_dev(w.dtype, inp["lmk_q"], dev), "lmk_k": to_dev(w.dtype, inp["lmk_k"], dev)}
+    names = ("q", "k", "v", "dout") if w.backward else ("q", "k", "v")
+    t.update(gi.device_tensors(w, names, dev))
+    return w, inp, t
+
+
+def _oracle_rows(w, inp, rows, b=0, hr=0):
+    """Oracle scores -> top-k -> weights for the listed landmark rows of (b, hr)."""
+    lq = gi.decode(w, inp["lmk_q"][b:b + 1, hr:hr + 1])
+    lk = gi.decode(w, inp["lmk_k"][b:b + 1, hr:hr + 1])
+    r = og.scores(lq, lk, w.score_scale, w.mode, rows=rows)
+    idx, sel = og.topk(r, w.topk)
+    return idx[0, 0], sel[0, 0], og.fusion_weights(sel)[0, 0]
+
+
+def _oracle_chunk(w, t, b, c, idx_row, sel_row, heads=None):
+    """Oracle output and lse of query chunk c of batch b (all heads or `heads`) from its
+    retrieved chunks, as a one-chunk grouped cross attention problem."""
+    heads = list(range(w.H)) if heads is None else heads
+    js = [int(j) for j in idx_row if j >= 0]
+    S = w.S
+    q = host64(t["q"][b, heads, c * S:(c + 1) * S])[None]
+    k = np.concatenate([host64(t["k"][b, heads, j * S:(j + 1) * S]) for j in js], axis=1)[None]
+    v = np.concatenate([host64(t["v"][b, heads, j * S:(j + 1) * S]) for j in js], axis=1)[None]
+    kk = w.topk
+    idx = np.full((1, 1, 1, kk), -1, np.int32)
+    sel = np.full((1, 1, 1, kk), -np.inf)
+    valid = [s for s in range(kk) if idx_row[s] >= 0]
+    for n, s in enumerate(valid):
+        idx[0, 0, 0, s] = n
+        sel[0, 0, 0, s] = sel_row[s]
+    wt = og.fusion_weights(sel)
+    out, lse = og.xattn_fwd(q, k, v, idx, wt, S, w.attn_scale, mode="decode")
+    return out[0], lse[0]
+
+
+def _check_rows_and_chunks(w, inp, t, f, rows, chunks):
+    """Exact indices on `rows` (every batch); outputs on `chunks` = [(b, c)]."""
+    tol = TOL[w.dtype]
+    gi_idx = f["idx"].cpu().numpy()
+    gs = f["sel"].cpu().numpy()
+    ref_rows = {}
+    for b in range(w.B):
+        ri, rs, rw = _oracle_rows(w, inp, rows, b=b)
+        np.testing.assert_array_equal(gi_idx[b, 0, rows], ri)
+        assert max_abs_rel(gs[b, 0, rows].astype(np.float64), rs) <= tol
+        ref_rows[b] = {int(r): (ri[n], rs[n]) for n, r in enumerate(rows)}
+    out = f["out"]
+    lse = f["lse"]
+    for b, c in chunks:
+        t_row = c - 1 if w.mode == "causal" else 0
+        if t_row < 0 or t_row not in ref_rows[b]:
+            ri, rs, _ = _oracle_rows(w, inp, [t_row], b=b) if t_row >= 0 else (None, None, None)
+            if t_row < 0:
+                assert np.all(host64(out[b, :, c * w.S:(c + 1) * w.S]) == 0.0)
+                continue
+            idx_row, sel_row = ri[0], rs[0]
+        else:
+            idx_row, sel_row = ref_rows[b][t_row]
+        if not np.any(idx_row >= 0):
+            assert np.all(host64(out[b, :, c * w.S:(c + 1) * w.S]) == 0.0)
+            continue
+        o_ref, l_ref = _oracle_chunk(w, t, b, c, idx_row, sel_row)
+        assert max_abs_rel(host64(out[b, :, c * w.S:(c + 1) * w.S]), o_ref) <= tol, (b, c)
+        assert max_abs_rel(host64(lse[b, :, c * w.S:(c + 1) * w.S]), l_ref) <= tol, (b, c)
+
+
+def test_train_16k_forward(dev):
+    """16,384 tokens x batch 8, 12 heads, width 768, top-8: every row's indices; sampled outputs."""
+    from paper_2410_01651_amd import gca
+    w, inp, t = _setup("train_16k_bf16", dev)
+    f = gca.forward(problem_for(w), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    rows = list(range(w.n_chunks))
+    rng = np.random.default_rng(20)
+    chunks = [(0, 0), (0, 1), (0, 2), (w.B - 1, w.n_chunks - 1)]
+    chunks += [(int(rng.integers(w.B)), int(rng.integers(2, w.n_chunks))) for _ in range(12)]
+    _check_rows_and_chunks(w, inp, t, f, rows, chunks)
+
+
+def test_fwdbwd_64k(dev):
+    """65,536 tokens x batch 2, 16 heads, top-8, forward + backward.  Indices on every
+    row; outputs on sampled chunks; dq/dk/dv on two whole (batch, head) slices; dsel
+    and the landmark gradients for batch 0 (which sum over all 16 heads)."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w, inp, t = _setup("fwdbwd_64k_bf16", dev)
+    p = problem_for(w)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                              t["lmk_q"], t["lmk_k"])
+    torch.cuda.synchronize()
+    rows = list(range(w.n_chunks))
+    rng = np.random.default_rng(30)
+    chunks = [(0, 1), (1, 2), (1, w.n_chunks - 1)]
+    chunks += [(int(rng.integers(w.B)), int(rng.integers(2, w.n_chunks))) for _ in range(8)]
+    _check_rows_and_chunks(w, inp, t, f, rows, chunks)
+
+    tol = TOL[w.dtype]
+    b = 0
+    ri, rs, rw = _oracle_rows(w, inp, rows, b=b)
+    idx = ri[None, None]
+    wt = rw[None, None]
+    # dq/dk/dv on two whole slices
+    for h in (0, w.H - 1):
+        sl = lambda name: host64(t[name][b:b + 1, h:h + 1])
+        dq, dk, dv, _ = og.xattn_bwd(sl("q"), sl("k"), sl("v"), idx, wt, sl("dout"), w.S, w.attn_scale)
+        for key, ref in (("dq", dq), ("dk", dk), ("dv", dv)):
+            e = max_abs_rel(host64(g[key][b:b + 1, h:h + 1]), ref)
+            assert e <= tol, (key, h, e)
+    # score and landmark gradients of batch 0: dw sums over all heads
+    full = lambda name: host64(t[name][b:b + 1])
+    _, _, _, dw = og.xattn_bwd(full("q"), full("k"), full("v"), idx, wt, full("dout"), w.S, w.attn_scale)
+    dsel = og.dsel_from_dw(wt, dw)
+    dlq, dlk = og.landmark_grads(dsel, idx, gi.decode(w, inp["lmk_q"][b:b + 1]),
+                                 gi.decode(w, inp["lmk_k"][b:b + 1]), w.score_scale)
+    assert max_abs_rel(host64(g["dsel"][b:b + 1]), dsel) <= tol
+    assert max_abs_rel(host64(g["dlmk_q"][b:b + 1]), dlq) <= tol
+    assert max_abs_rel(host64(g["dlmk_k"][b:b + 1]), dlk) <= tol
+
+
+def test_planted_1m_forward(dev):
+    """1,048,576 tokens, 16,384 chunks (single-pass select, no score matrix): the last
+    row's top-8 is exactly the eight planted chunks with weight 1/8 each; sampled rows'
+    indices are exact and sampled chunks' outputs match."""
+    from paper_2410_01651_amd import gca
+    w, inp, t = _setup("planted_1m_bf16", dev)
+    p = problem_for(w)
+    assert gca.workspace_size(p, gca.OP_FORWARD) == 0          # the fused path is chosen
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    last = w.n_chunks - 1
+    pos = gi.plant_positions(w)
+    assert list(f["idx"][0, 0, last].cpu().numpy()) == list(pos)
+    np.testing.assert_allclose(f["w"][0, 0, last].cpu().numpy(), np.full(8, 1 / 8), rtol=1e-6)
+    rng = np.random.default_rng(40)
+    rows = sorted(set([0, 1, 2, 7, 8, 9, 63, 64, 65, last] + [int(x) for x in rng.integers(0, w.n_chunks, 300)]))
+    chunks = [(0, 1), (0, last)] + [(0, int(c)) for c in rng.integers(2, w.n_chunks, 10)]
+    _check_rows_and_chunks(w, inp, t, f, rows, chunks)
+
+
+def test_decode_16m(dev):
+    """One new chunk against 16,777,216 cached tokens: the planted chunk is retrieved,
+    indices are exact, and the output matches the oracle over the gathered chunks."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w = get_workload("decode_16m_bf16")
+    inp, _ = margins.checked_inputs(w, tokens=False)
+    t = {"lmk_q": to_dev(w.dtype, inp["lmk_q"], dev), "lmk_k": to_dev(w.dtype, inp["lmk_k"], dev)}
+    t.update(gi.device_kv(w, dev))
+    t.update(gi.device_tensors(w, ("q",), dev))
+    p = problem_for(w)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    torch.cuda.synchronize()
+    ri, rs, _ = _oracle_rows(w, inp, [0])
+    np.testing.assert_array_equal(f["idx"][0, 0].cpu().numpy(), ri)
+    assert int(gi.plant_positions(w)[0]) in list(ri[0])
+    assert max_abs_rel(host64(f["sel"][0, 0]), rs) <= TOL[w.dtype]
+    o_ref, l_ref = _oracle_chunk(w, t, 0, 0, ri[0], rs[0])
+    assert max_abs_rel(host64(f["out"][0]), o_ref) <= TOL[w.dtype]
+    assert max_abs_rel(host64(f["lse"][0]), l_ref) <= TOL[w.dtype]
+    del t
+    torch.cuda.empty_cache()
