@@ -314,6 +314,8 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--only", choices=["train", "decode"], default=None,
+                    help="run one leg only (for profiling); the JSON line then carries that leg")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -331,6 +333,12 @@ def main():
     from paper_2410_01651_amd import gca
     dev = torch.device("cuda:0")
 
+    if args.only == "decode":
+        print(json.dumps({"decode_scan": bench_decode(args, dev, gca)}), flush=True)
+        return
+    if args.only == "train":
+        args.no_decode = True
+        args.no_cpu_baseline = True
     tr = bench_train(args, dev, gca)
     w = tr["w"]
     line = {

@@ -19,6 +19,13 @@ OUT = os.path.join(HERE, "libgca.so")
 OBJ_DIR = os.path.join(HERE, "_build")
 
 SOURCES = ["api.cpp", "scores.hip", "xattn_fwd.hip", "xattn_bwd.hip"]
+# The attention kernels never rely on NaN semantics: without IEEE mode the
+# softmax max needs no operand canonicalisation, and MFMA accumulators in
+# ordinary VGPRs need no copies out of the accumulation registers.
+PER_SOURCE = {
+    "xattn_fwd.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "xattn_bwd.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
 ARCH = "gfx950"
 
 COMMON = [
@@ -45,7 +52,7 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
     for src in SOURCES:
         obj = os.path.join(OBJ_DIR, os.path.splitext(src)[0] + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else []
-        cmd = [cc, *COMMON, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [cc, *COMMON, *PER_SOURCE.get(src, []), *lang, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))

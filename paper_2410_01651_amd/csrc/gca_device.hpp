@@ -181,6 +181,125 @@ struct Tile64 {
   }
 };
 
+// ------------------------------------------- asynchronous tile staging ----
+//
+// Chunk tiles (64 tokens x 64 dims, row-major in HBM) are copied straight into
+// LDS with global_load_lds_dwordx4: each lane supplies a global address and the
+// 64 lanes of one instruction fill 1 KB of consecutive LDS.  The LDS copy is
+// XOR-swizzled at 16-byte granularity: LDS chunk c' of row r holds the row's
+// global chunk c' ^ (r mod chunks-per-row), so that reading one 16-byte chunk
+// per row from 32 consecutive rows, or the 8-byte transposed reads, spread over
+// the banks instead of hitting the same ones.
+//
+// The copies are asynchronous: a wave's own copies are complete once its
+// vector-memory counter has dropped to the number issued after them
+// (wait_vmem), and the other waves' copies once all waves have passed the next
+// barrier (block_barrier).  block_barrier deliberately does not drain the
+// counter, so copies for later slots stay in flight across it; no global store
+// or load into registers may be issued between a copy and the wait for it.
+
+template <typename T>
+struct Swz {
+  static constexpr int kVec = 16 / sizeof(T);  // elements per 16-byte chunk
+  static constexpr int kCPR = kD / kVec;       // chunks per row (8 bf16, 16 fp32)
+  __device__ static __forceinline__ int off(int r, int col) {
+    return r * kD + ((((col / kVec) ^ (r & (kCPR - 1)))) * kVec) + (col % kVec);
+  }
+};
+
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Wait until at most m * L of this wave's vector-memory operations are pending.
+template <int L>
+__device__ __forceinline__ void wait_slots(int m) {
+  if (m >= 3) wait_vmem<3 * L>();
+  else if (m == 2) wait_vmem<2 * L>();
+  else if (m == 1) wait_vmem<L>();
+  else wait_vmem<0>();
+}
+
+__device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// One direct-to-LDS copy: every lane moves `Bytes` (16 or 4) from its global
+// address to LDS at lds_base + lane * Bytes.  Issued as inline assembly so that
+// the compiler neither drains the vector-memory counter for it nor orders LDS
+// reads behind it: completion is tracked only by the explicit wait_vmem /
+// wait_slots calls and the barrier that follows them.  The statement is volatile
+// (kept in order with the barrier) but does not clobber memory: the LDS it
+// writes is never touched between the issuing barrier and the next wait, and
+// leaving other memory unclobbered lets uniform global reads stay scalar.
+template <int Bytes>
+__device__ __forceinline__ void dma_copy(const void* g, const void* lds_base) {
+  const uint32_t base = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)lds_base));
+  if constexpr (Bytes == 16) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(base) : "m0");
+  } else {
+    static_assert(Bytes == 4, "copy size");
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(base) : "m0");
+  }
+}
+
+// Copy one 64x64 tile into swizzled LDS using NW waves (each issues kCPR/NW copies).
+template <typename T, int NW>
+__device__ __forceinline__ void dma_tile(const T* __restrict__ g, T* lds, int wave, int lane) {
+  constexpr int kVec = Swz<T>::kVec, kCPR = Swz<T>::kCPR;
+#pragma unroll
+  for (int ii = 0; ii < kCPR / NW; ++ii) {
+    const int i = ii * NW + wave;
+    const int pch = i * 64 + lane;
+    const int r = pch / kCPR;
+    const int c = (pch % kCPR) ^ (r & (kCPR - 1));
+    dma_copy<16>(g + r * kD + c * kVec, lds + i * 64 * kVec);
+  }
+}
+
+// Copy 64 floats spaced `stride` apart into 64 consecutive LDS floats (one wave).
+__device__ __forceinline__ void dma_column(const float* __restrict__ g, int64_t stride, float* lds, int lane) {
+  dma_copy<4>(g + lane * stride, lds);
+}
+
+// Fragments from a swizzled tile: 8 consecutive elements of row r from column col
+// (a multiple of 8) ...
+__device__ __forceinline__ bf16x8 lds_frag(const __bf16* tile, int r, int col) {
+  return *reinterpret_cast<const bf16x8*>(tile + Swz<__bf16>::off(r, col));
+}
+__device__ __forceinline__ f32x8 lds_frag(const float* tile, int r, int col) {
+  f32x8 f;
+  f.lo = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off(r, col));
+  f.hi = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off(r, col + 4));
+  return f;
+}
+
+// ... and down a column (see load_frag_t): lane gets rows r0..r0+3 then r1..r1+3 of
+// column cbase + lane%16.
+__device__ __forceinline__ bf16x8 lds_frag_t(const __bf16* tile, int r0, int r1, int cbase) {
+  const int s = threadIdx.x & 15;
+  typedef __attribute__((address_space(3))) bf16x4_tr lds_v4;
+  const __bf16* p0 = tile + Swz<__bf16>::off(r0 + (s >> 2), cbase + 4 * (s & 3));
+  const __bf16* p1 = tile + Swz<__bf16>::off(r1 + (s >> 2), cbase + 4 * (s & 3));
+  bf16x4_tr a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p0));
+  bf16x4_tr b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p1));
+  bf16x8 f;
+  f[0] = a[0]; f[1] = a[1]; f[2] = a[2]; f[3] = a[3];
+  f[4] = b[0]; f[5] = b[1]; f[6] = b[2]; f[7] = b[3];
+  return f;
+}
+__device__ __forceinline__ f32x8 lds_frag_t(const float* tile, int r0, int r1, int cbase) {
+  const int col = cbase + (threadIdx.x & 15);
+  using Z = Swz<float>;
+  f32x8 f;
+  f.lo = f32x4{tile[Z::off(r0, col)], tile[Z::off(r0 + 1, col)], tile[Z::off(r0 + 2, col)],
+               tile[Z::off(r0 + 3, col)]};
+  f.hi = f32x4{tile[Z::off(r1, col)], tile[Z::off(r1 + 1, col)], tile[Z::off(r1 + 2, col)],
+               tile[Z::off(r1 + 3, col)]};
+  return f;
+}
+
 // ------------------------------------------------------ cross-lane ops ----
 
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
@@ -272,6 +391,32 @@ __device__ __forceinline__ int rank_by_chunk(int my_j, int count) {
     rank += (oj < my_j) ? 1 : 0;
   }
   return rank;
+}
+
+// Fusion weights (Eq. 2) of one retrieval row computed by one wave: lane s < K
+// loads slot s; returns w (0 on pads) and the chunk (-1 on pads) in that lane,
+// and whether the row has any valid slot.  Valid slots are 0 <= idx < nKV.
+__device__ __forceinline__ bool wave_row_weight(const int32_t* __restrict__ idx, const float* __restrict__ sel,
+                                                int64_t row_off, int K, int64_t nKV, float& w, int& j) {
+  const int lane = threadIdx.x & 63;
+  int jj = -1;
+  float sv = -INFINITY;
+  if (lane < K) {
+    jj = idx[row_off + lane];
+    sv = sel[row_off + lane];
+  }
+  const bool valid = lane < K && jj >= 0 && jj < nKV;
+  float m = valid ? sv : -INFINITY;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  const bool any = __ballot(valid) != 0;
+  const float e = valid ? expf(sv - m) : 0.f;
+  float sum = e;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+  w = valid ? e / sum : 0.f;
+  j = valid ? jj : -1;
+  return any;
 }
 
 // Fusion weight (Eq. 2) of slot s of one retrieval row: softmax over the valid

@@ -20,6 +20,7 @@
 #include "gca_launch.hpp"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace gca {
 namespace {
@@ -198,13 +199,51 @@ __global__ __launch_bounds__(256) void csr_sort_kernel(const int* __restrict__ o
   }
 }
 
+// LDS ring depth (retrieved chunks / retrievers in flight per workgroup).
+template <typename T> struct RingDepth;
+template <> struct RingDepth<__bf16> { static constexpr int v = 4; };
+template <> struct RingDepth<float> { static constexpr int v = 2; };
+
+#define GCA_RING_DECL(T, NB, SIZE)                                       \
+  __shared__ __attribute__((aligned(16))) T ring0[SIZE];                 \
+  __shared__ __attribute__((aligned(16))) T ring1[SIZE];                 \
+  __shared__ __attribute__((aligned(16))) T ring2[(NB) > 2 ? (SIZE) : 8]; \
+  __shared__ __attribute__((aligned(16))) T ring3[(NB) > 3 ? (SIZE) : 8]; \
+  auto slot_buf = [&](auto B) __device__ -> T* {                         \
+    constexpr int b_ = decltype(B)::value;                               \
+    if constexpr (b_ == 0) return ring0;                                 \
+    else if constexpr (b_ == 1) return ring1;                            \
+    else if constexpr (b_ == 2) return ring2;                            \
+    else return ring3;                                                   \
+  };
+
+template <int V>
+using ic = std::integral_constant<int, V>;
+
+// Runs step(ic<b>, u) for u = 0..n-1 with ring buffer b = u % NB known at compile
+// time, after issuing the copies for the first NB - 1 items.
+template <int NB, typename Issue, typename Step>
+__device__ __forceinline__ void ring_loop(int n, Issue&& issue, Step&& step) {
+  issue(ic<0>{}, 0);
+  if (NB > 2 && n > 1) issue(ic<1>{}, 1);
+  if (NB > 3 && n > 2) issue(ic<(NB > 3 ? 2 : 0)>{}, 2);
+  for (int u0 = 0; u0 < n; u0 += NB) {
+    step(ic<0>{}, u0);
+    if (u0 + 1 < n) step(ic<1>{}, u0 + 1);
+    if (NB > 2 && u0 + 2 < n) step(ic<(NB > 2 ? 2 : 0)>{}, u0 + 2);
+    if (NB > 3 && u0 + 3 < n) step(ic<(NB > 3 ? 3 : 0)>{}, u0 + 3);
+  }
+}
+
 // ------------------------------------------------- query-stationary dQ ----
 
 template <typename T>
 __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t nwork) {
-  constexpr int LD = LdsLd<T>::v;
-  __shared__ __attribute__((aligned(16))) T sK[kS * LD];
-  __shared__ __attribute__((aligned(16))) T sV[kS * LD];
+  constexpr int NB = RingDepth<T>::v;
+  constexpr int TILE = kS * kD;
+  constexpr int L = Swz<T>::kCPR;  // copies per wave per slot (K and V tiles over 2 waves)
+  GCA_RING_DECL(T, NB, 2 * TILE)
+  __shared__ float sL[32 * kS];  // [slot][query]: lse on entry, D_s on exit
   __shared__ float sW[32];
   __shared__ int sJ[32];
   __shared__ int sSlot[32];
@@ -222,6 +261,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
   const int64_t t = p.causal ? c - 1 : 0;
   const int K = p.K;
   const int64_t row_base = (b * p.Hr + hr) * p.nQ;
+  const int64_t tok0 = ((b * p.H + h) * p.nQ + c) * kS;
 
   if (tid < 32) {
     float wv = 0.f;
@@ -238,6 +278,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     sPart[0][tid] = 0.f;
     sPart[1][tid] = 0.f;
   }
+  if (t >= 0)
+    for (int e = tid; e < kS * K; e += kThreads) sL[(e % K) * kS + e / K] = p.lse[tok0 * K + e];
   __syncthreads();
   if (tid == 0) {
     int n = 0;
@@ -248,7 +290,6 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
   __syncthreads();
   const int n = sN;
 
-  const int64_t tok0 = ((b * p.H + h) * p.nQ + c) * kS;
   T* dq = reinterpret_cast<T*>(p.dq) + tok0 * kD;
   if (n == 0) {
     for (int e = tid; e < kS * kD / 4; e += kThreads) store4(dq + 4 * e, 0.f, 0.f, 0.f, 0.f);
@@ -265,57 +306,49 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     qf[kb] = load_frag(qrow + 16 * kb + 8 * hh);
     df[kb] = load_frag(dorow + 16 * kb + 8 * hh);
   }
-  const float* lse_row = p.lse + (tok0 + qi) * K;
-  float* D_row = p.ws.Dbuf + (tok0 + qi) * K;
+  wait_vmem<0>();
 
-  const int64_t kv0 = (b * p.H + h) * p.nKV * (kS * kD);
+  const int64_t kv0 = (b * p.H + h) * p.nKV * TILE;
   const T* kbase = reinterpret_cast<const T*>(p.k) + kv0;
   const T* vbase = reinterpret_cast<const T*>(p.v) + kv0;
-  Tile64<T, kThreads> tk, tv;
-  {
-    const int64_t j0 = sJ[sSlot[0]];
-    tk.load_cached(kbase + j0 * (kS * kD), tid);
-    tv.load_cached(vbase + j0 * (kS * kD), tid);
-  }
   f32x16 g0 = zero16(), g1 = zero16();  // dQ^T, d rows 0-31 / 32-63
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
 
-  for (int u = 0; u < n; ++u) {
+  auto issue = [&](auto B, int u) __device__ {
+    const int64_t j = sJ[sSlot[u]];
+    T* dst = slot_buf(B);
+    dma_tile<T, 2>(kbase + j * TILE, dst, wave, lane);
+    dma_tile<T, 2>(vbase + j * TILE, dst + TILE, wave, lane);
+  };
+  auto step = [&](auto B, int u) __device__ {
+    constexpr int bb = decltype(B)::value;
     const int s = sSlot[u];
-    __syncthreads();
-    tk.store(sK, LD, tid);
-    tv.store(sV, LD, tid);
-    __syncthreads();
-    if (u + 1 < n) {
-      const int64_t jn = sJ[sSlot[u + 1]];
-      tk.load_cached(kbase + jn * (kS * kD), tid);
-      tv.load_cached(vbase + jn * (kS * kD), tid);
-    }
-    const float lse2 = lse_row[s] * kLog2e;
+    wait_slots<L>(min(NB - 2, n - 1 - u));
+    block_barrier();
+    if (u + NB - 1 < n) issue(ic<(bb + NB - 1) % NB>{}, u + NB - 1);
+    const T* sK = slot_buf(B);
+    const T* sV = sK + TILE;
+    const float lse2 = sL[s * kS + qi] * kLog2e;
 
     f32x16 s0 = zero16(), s1 = zero16(), p0 = zero16(), p1 = zero16();
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const Frag<T> ka = load_frag(sK + (lane & 31) * LD + 16 * kb + 8 * hh);
-      const Frag<T> kb2 = load_frag(sK + (32 + (lane & 31)) * LD + 16 * kb + 8 * hh);
-      mma32(s0, ka, qf[kb]);
-      mma32(s1, kb2, qf[kb]);
-      const Frag<T> va = load_frag(sV + (lane & 31) * LD + 16 * kb + 8 * hh);
-      const Frag<T> vb = load_frag(sV + (32 + (lane & 31)) * LD + 16 * kb + 8 * hh);
-      mma32(p0, va, df[kb]);
-      mma32(p1, vb, df[kb]);
+      mma32(s0, lds_frag(sK, lane & 31, 16 * kb + 8 * hh), qf[kb]);
+      mma32(s1, lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh), qf[kb]);
+      mma32(p0, lds_frag(sV, lane & 31, 16 * kb + 8 * hh), df[kb]);
+      mma32(p1, lds_frag(sV, 32 + (lane & 31), 16 * kb + 8 * hh), df[kb]);
     }
     // P^T and D = rowsum(P o dP) for this lane's query
     float Dq = 0.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      s0[i] = __builtin_amdgcn_exp2f(s0[i] * sc - lse2);
-      s1[i] = __builtin_amdgcn_exp2f(s1[i] * sc - lse2);
+      s0[i] = __builtin_amdgcn_exp2f(fmaf(s0[i], sc, -lse2));
+      s1[i] = __builtin_amdgcn_exp2f(fmaf(s1[i], sc, -lse2));
       Dq += s0[i] * p0[i] + s1[i] * p1[i];
     }
     Dq += xor32(Dq);
-    if (hh == 0) D_row[s] = Dq;
+    if (hh == 0) sL[s * kS + qi] = Dq;  // this lane alone read the lse it replaces
     const float ws = sW[s];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -329,17 +362,16 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     frag_from_acc(f[3], s1, 1, 1.f);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const Frag<T> a0 = load_frag_t(sK, LD, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
-      const Frag<T> a1 = load_frag_t(sK, LD, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
-      mma32(g0, a0, f[kb]);
-      mma32(g1, a1, f[kb]);
+      mma32(g0, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), f[kb]);
+      mma32(g1, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), f[kb]);
     }
     // this wave's share of dw[t, s]: sum of D over its 32 queries
     float dsum = Dq;
 #pragma unroll
     for (int o = 16; o >= 1; o >>= 1) dsum += __shfl_xor(dsum, o);
     if (lane == 0) sPart[wave][s] = dsum;
-  }
+  };
+  ring_loop<NB>(n, issue, step);
 
   const float as = p.attn_scale;
   T* drow = dq + qi * kD;
@@ -351,18 +383,23 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
   }
   __syncthreads();
   if (tid < K) p.ws.dwp[(bh * p.nQ + t) * K + tid] = sPart[0][tid] + sPart[1][tid];
+  float* Dout = p.ws.Dbuf + tok0 * K;
+  for (int e = tid; e < kS * K; e += kThreads) {
+    const int q = e / K, s = e % K;
+    Dout[e] = sJ[s] >= 0 ? sL[s * kS + q] : 0.f;
+  }
 }
 
 // ---------------------------------------------- key-stationary dK, dV ----
 
 template <typename T>
 __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t nwork) {
-  constexpr int LD = LdsLd<T>::v;
-  __shared__ __attribute__((aligned(16))) T sQ[kS * LD];
-  __shared__ __attribute__((aligned(16))) T sO[kS * LD];
-  __shared__ __attribute__((aligned(16))) float sL[kS];
-  __shared__ __attribute__((aligned(16))) float sD[kS];
-  __shared__ float sWt;
+  constexpr int NB = RingDepth<T>::v;
+  constexpr int TILE = kS * kD;
+  constexpr int L = Swz<T>::kCPR + 1;  // per wave per retriever: Q/dO tile copies + one column
+  // ring entry: Q_c tile, dO_c tile, lse column, D column
+  constexpr int ENTRY = 2 * TILE + 2 * kS * (int)(sizeof(float) / sizeof(T));
+  GCA_RING_DECL(T, NB, ENTRY)
 
   const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
   if (wid >= nwork) return;
@@ -376,12 +413,16 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t
   const int64_t bhr = b * p.Hr + hr;
   const int* off = p.ws.offs + bhr * (p.nKV + 1);
   const int lo = off[j], hi = off[j + 1];
-  const int* list = p.ws.sorted + bhr * p.nQ * K;
+  const int* list_g = p.ws.sorted + bhr * p.nQ * K + lo;
+  const int n = hi - lo;
+  constexpr int NE = 256;  // retrievers staged in LDS per batch
+  __shared__ int sE[NE];
+  __shared__ float sWt[NE];
 
   const int64_t key0 = (bh * p.nKV + j) * kS;  // first key token of chunk j
   T* dk = reinterpret_cast<T*>(p.dk) + key0 * kD;
   T* dv = reinterpret_cast<T*>(p.dv) + key0 * kD;
-  if (lo == hi) {
+  if (n == 0) {
     for (int e = tid; e < kS * kD / 4; e += kThreads) {
       store4(dk + 4 * e, 0.f, 0.f, 0.f, 0.f);
       store4(dv + 4 * e, 0.f, 0.f, 0.f, 0.f);
@@ -399,57 +440,50 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t
     kf[kb] = load_frag(krow + 16 * kb + 8 * hh);
     vf[kb] = load_frag(vrow + 16 * kb + 8 * hh);
   }
+  wait_vmem<0>();
 
   const T* qb = reinterpret_cast<const T*>(p.q) + bh * p.nQ * kS * kD;
   const T* ob = reinterpret_cast<const T*>(p.dout) + bh * p.nQ * kS * kD;
   const float* lseb = p.lse + bh * p.nQ * kS * K;
   const float* Db = p.ws.Dbuf + bh * p.nQ * kS * K;
+  const float* wrow = p.ws.w + bhr * p.nQ * K;
 
-  Tile64<T, kThreads> tq, to;
-  float lv = 0.f, dv_ = 0.f;
-  auto fetch = [&](int e) {
-    const int64_t t = e / K;
+  auto issue = [&](auto B, int u) __device__ {
+    const int e = sE[u];
+    const int64_t c = e / K + p.causal;
     const int s = e % K;
-    const int64_t c = t + p.causal;
-    tq.load_cached(qb + c * (kS * kD), tid);
-    to.load_cached(ob + c * (kS * kD), tid);
-    if (tid < kS) {
-      lv = lseb[(c * kS + tid) * K + s];
-      dv_ = Db[(c * kS + tid) * K + s];
-    }
+    T* dst = slot_buf(B);
+    dma_tile<T, 2>(qb + c * TILE, dst, wave, lane);
+    dma_tile<T, 2>(ob + c * TILE, dst + TILE, wave, lane);
+    float* cols = reinterpret_cast<float*>(dst + 2 * TILE);
+    if (wave == 0) dma_column(lseb + c * kS * K + s, K, cols, lane);
+    else dma_column(Db + c * kS * K + s, K, cols + kS, lane);
   };
-  fetch(list[lo]);
 
   f32x16 dv0 = zero16(), dv1 = zero16(), dk0 = zero16(), dk1 = zero16();
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
+  int nb = 0;  // retrievers in the current batch
 
-  for (int u = lo; u < hi; ++u) {
-    const int e = list[u];
-    __syncthreads();
-    tq.store(sQ, LD, tid);
-    to.store(sO, LD, tid);
-    if (tid < kS) {
-      sL[tid] = lv * kLog2e;
-      sD[tid] = dv_;
-    }
-    if (tid == 0) sWt = p.ws.w[(bhr * p.nQ + e / K) * K + e % K];
-    __syncthreads();
-    if (u + 1 < hi) fetch(list[u + 1]);
-    const float wt = sWt;
+  auto step = [&](auto B, int u) __device__ {
+    constexpr int bb = decltype(B)::value;
+    const float wt = sWt[u];
+    wait_slots<L>(min(NB - 2, nb - 1 - u));
+    block_barrier();
+    if (u + NB - 1 < nb) issue(ic<(bb + NB - 1) % NB>{}, u + NB - 1);
+    const T* sQ = slot_buf(B);
+    const T* sO = sQ + TILE;
+    const float* sL = reinterpret_cast<const float*>(sQ + 2 * TILE);
+    const float* sD = sL + kS;
 
     // S = Q K^T and dP = dO V^T for this wave's keys; queries 0-31 / 32-63
     f32x16 s0 = zero16(), s1 = zero16(), p0 = zero16(), p1 = zero16();
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const Frag<T> qa = load_frag(sQ + (lane & 31) * LD + 16 * kb + 8 * hh);
-      const Frag<T> qb2 = load_frag(sQ + (32 + (lane & 31)) * LD + 16 * kb + 8 * hh);
-      mma32(s0, qa, kf[kb]);
-      mma32(s1, qb2, kf[kb]);
-      const Frag<T> oa = load_frag(sO + (lane & 31) * LD + 16 * kb + 8 * hh);
-      const Frag<T> ob2 = load_frag(sO + (32 + (lane & 31)) * LD + 16 * kb + 8 * hh);
-      mma32(p0, oa, vf[kb]);
-      mma32(p1, ob2, vf[kb]);
+      mma32(s0, lds_frag(sQ, lane & 31, 16 * kb + 8 * hh), kf[kb]);
+      mma32(s1, lds_frag(sQ, 32 + (lane & 31), 16 * kb + 8 * hh), kf[kb]);
+      mma32(p0, lds_frag(sO, lane & 31, 16 * kb + 8 * hh), vf[kb]);
+      mma32(p1, lds_frag(sO, 32 + (lane & 31), 16 * kb + 8 * hh), vf[kb]);
     }
     // accumulator row i holds query 32*qt + 8*(i/4) + 4*hh + i%4
     Frag<T> wp[4], ds[4];
@@ -461,8 +495,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t
       const f32x4 d1 = *reinterpret_cast<const f32x4*>(sD + 32 + 8 * g + 4 * hh);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float pa = wt * __builtin_amdgcn_exp2f(s0[4 * g + r] * sc - l0[r]);
-        const float pb = wt * __builtin_amdgcn_exp2f(s1[4 * g + r] * sc - l1[r]);
+        const float pa = wt * __builtin_amdgcn_exp2f(fmaf(s0[4 * g + r], sc, -l0[r] * kLog2e));
+        const float pb = wt * __builtin_amdgcn_exp2f(fmaf(s1[4 * g + r], sc, -l1[r] * kLog2e));
         s0[4 * g + r] = pa;
         s1[4 * g + r] = pb;
         p0[4 * g + r] = pa * (p0[4 * g + r] - d0[r]);
@@ -480,15 +514,24 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t
     // dV^T += dO^T (wP), dK^T += Q^T dS  (contraction over the 64 queries)
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const Frag<T> oa = load_frag_t(sO, LD, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
-      const Frag<T> ob2 = load_frag_t(sO, LD, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
-      mma32(dv0, oa, wp[kb]);
-      mma32(dv1, ob2, wp[kb]);
-      const Frag<T> qa = load_frag_t(sQ, LD, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
-      const Frag<T> qb2 = load_frag_t(sQ, LD, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
-      mma32(dk0, qa, ds[kb]);
-      mma32(dk1, qb2, ds[kb]);
+      mma32(dv0, lds_frag_t(sO, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), wp[kb]);
+      mma32(dv1, lds_frag_t(sO, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), wp[kb]);
+      mma32(dk0, lds_frag_t(sQ, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), ds[kb]);
+      mma32(dk1, lds_frag_t(sQ, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), ds[kb]);
     }
+  };
+  // the retriever list is staged through LDS in batches; each batch runs its
+  // own ring of copies, drained at the batch's end
+  for (int b0 = 0; b0 < n; b0 += NE) {
+    nb = min(NE, n - b0);
+    __syncthreads();
+    for (int i = tid; i < nb; i += kThreads) {
+      const int e = list_g[b0 + i];
+      sE[i] = e;
+      sWt[i] = wrow[e];
+    }
+    __syncthreads();
+    ring_loop<NB>(nb, issue, step);
   }
 
   // accumulators are transposed: lane holds key kr, d = 32*dt + 8*g + 4*hh + 0..3

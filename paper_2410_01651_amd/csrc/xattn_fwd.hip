@@ -3,8 +3,10 @@
 //
 // One workgroup of two waves per (batch, head, query chunk).  Each wave owns 32
 // of the chunk's 64 query tokens and keeps their Q fragments in registers for
-// the whole kernel.  For every retrieved chunk (slot) the workgroup gathers
-// that chunk's 64 keys and values into LDS, computes S^T = K Q^T on the
+// the whole kernel.  The retrieved chunks' keys and values stream through a
+// ring of LDS slots filled by asynchronous direct-to-LDS copies, several
+// chunks ahead of the one being computed.  For every slot the workgroup
+// computes S^T = K Q^T on the
 // matrix cores, takes each query's softmax over the 64 keys (one retrieved
 // chunk is exactly one tile, so no running rescale is needed), folds the
 // fusion weight w_s / l_s into P, and accumulates O^T += V^T (w_s P_s)^T into a
@@ -17,6 +19,8 @@
 // fragments come from the row-major V tile through LDS transpose reads.
 #include "gca_device.hpp"
 #include "gca_launch.hpp"
+
+#include <type_traits>
 
 namespace gca {
 namespace {
@@ -42,11 +46,23 @@ struct FwdParams {
   float attn_scale;
 };
 
+// LDS ring depth (retrieved chunks in flight per workgroup).
+template <typename T> struct RingDepth;
+template <> struct RingDepth<__bf16> { static constexpr int v = 4; };  // 4 x 16 KB
+template <> struct RingDepth<float> { static constexpr int v = 2; };   // 2 x 32 KB
+
 template <typename T, bool OBO>
 __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
-  constexpr int LD = LdsLd<T>::v;
-  __shared__ __attribute__((aligned(16))) T sK[kS * LD];
-  __shared__ __attribute__((aligned(16))) T sV[kS * LD];
+  constexpr int NB = RingDepth<T>::v;
+  constexpr int TILE = kS * kD;
+  constexpr int L = Swz<T>::kCPR;  // copies per wave per slot: 2 tiles x kCPR / 2 waves
+  // one LDS variable per ring slot: with the slot known at compile time in the
+  // unrolled loop below, the compiler waits only for that slot's copies
+  __shared__ __attribute__((aligned(16))) T ring0[2 * TILE];
+  __shared__ __attribute__((aligned(16))) T ring1[2 * TILE];
+  __shared__ __attribute__((aligned(16))) T ring2[NB > 2 ? 2 * TILE : 8];
+  __shared__ __attribute__((aligned(16))) T ring3[NB > 3 ? 2 * TILE : 8];
+  __shared__ float sLse[32 * kS];  // [slot][query]
   __shared__ float sW[32];
   __shared__ int sJ[32];
   __shared__ int sSlot[32];
@@ -64,29 +80,27 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
   const int K = p.topk;
   const int64_t row_base = (b * p.Hr + hr) * p.nQ;  // retrieval rows of (b, hr)
 
-  if (tid < 32) {
+  // The retrieval row's slots (Eq. 2 weights, compacted list of valid slots) by
+  // wave 0 with one load per slot; wave 1 writes the weights of the causal last
+  // row, which feeds no chunk and is owned by chunk 0.
+  if (wave == 0 || (p.w && p.causal && c == 0 && (p.Hr != 1 || h == 0))) {
+    const int64_t row = wave == 0 ? t : p.nQ - 1;
     float wv = 0.f;
     int jv = -1;
-    if (t >= 0 && tid < K)
-      row_weight(p.idx + (row_base + t) * K, p.sel + (row_base + t) * K, K, p.nKV, tid, wv, jv);
-    sW[tid] = wv;
-    sJ[tid] = jv;
-    // every row's weights are written once: by the query chunk it feeds, and
-    // the causal last row (which feeds no chunk) by chunk 0
-    if (p.w && tid < K && (p.Hr != 1 || h == 0)) {
-      const int64_t wt = p.causal ? (c == 0 ? p.nQ - 1 : c - 1) : 0;
-      float ww;
-      int jj;
-      row_weight(p.idx + (row_base + wt) * K, p.sel + (row_base + wt) * K, K, p.nKV, tid, ww, jj);
-      p.w[(row_base + wt) * K + tid] = ww;
+    const bool any = row >= 0 && wave_row_weight(p.idx, p.sel, (row_base + row) * K, K, p.nKV, wv, jv);
+    if (wave == 0) {
+      const uint64_t mask = __ballot(jv >= 0 && lane < K);
+      if (lane < 32) {
+        sW[lane] = wv;
+        sJ[lane] = jv;
+      }
+      if (jv >= 0 && lane < K) sSlot[__popcll(mask & ((1ull << lane) - 1))] = lane;
+      if (lane == 0) sN = any ? __popcll(mask) : 0;
+      // this row's weights go out with the chunk it feeds
+      if (p.w && row >= 0 && lane < K && (p.Hr != 1 || h == 0)) p.w[(row_base + row) * K + lane] = wv;
+    } else if (lane < K) {
+      p.w[(row_base + row) * K + lane] = wv;
     }
-  }
-  __syncthreads();
-  if (tid == 0) {
-    int n = 0;
-    for (int s = 0; s < K; ++s)
-      if (sJ[s] >= 0) sSlot[n++] = s;
-    sN = n;
   }
   __syncthreads();
   const int n = sN;
@@ -107,39 +121,48 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
   Frag<T> qf[4];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qrow + 16 * kb + 8 * hh);
+  wait_vmem<0>();  // nothing but the chunk copies may be pending inside the slot loop
 
-  const int64_t kv0 = (b * p.H + h) * p.nKV * (kS * kD);
+  const int64_t kv0 = (b * p.H + h) * p.nKV * TILE;
   const T* kbase = reinterpret_cast<const T*>(p.k) + kv0;
   const T* vbase = reinterpret_cast<const T*>(p.v) + kv0;
+  auto slot_buf = [&](auto B) __device__ -> T* {
+    constexpr int b = decltype(B)::value;
+    if constexpr (b == 0) return ring0;
+    else if constexpr (b == 1) return ring1;
+    else if constexpr (b == 2) return ring2;
+    else return ring3;
+  };
+  auto issue = [&](auto B, int u) __device__ {
+    const int64_t j = sJ[sSlot[u]];
+    T* dst = slot_buf(B);
+    dma_tile<T, 2>(kbase + j * TILE, dst, wave, lane);
+    dma_tile<T, 2>(vbase + j * TILE, dst + TILE, wave, lane);
+  };
+  issue(std::integral_constant<int, 0>{}, 0);
+  if (NB > 2 && n > 1) issue(std::integral_constant<int, 1>{}, 1);
+  if (NB > 3 && n > 2) issue(std::integral_constant<int, (NB > 3 ? 2 : 0)>{}, 2);
 
-  Tile64<T, kThreads> tk, tv;
-  {
-    const int64_t j0 = sJ[sSlot[0]];
-    tk.load_cached(kbase + j0 * (kS * kD), tid);
-    tv.load_cached(vbase + j0 * (kS * kD), tid);
-  }
   f32x16 o0 = zero16(), o1 = zero16();
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
 
-  for (int u = 0; u < n; ++u) {
+  // one slot of work on ring buffer B; the copy for slot u + NB - 1 goes to the
+  // buffer slot u - 1 used, which every wave has finished reading at the barrier
+  auto step = [&](auto B, int u) __device__ {
+    constexpr int b = decltype(B)::value;
     const int s = sSlot[u];
-    __syncthreads();
-    tk.store(sK, LD, tid);
-    tv.store(sV, LD, tid);
-    __syncthreads();
-    if (u + 1 < n) {
-      const int64_t jn = sJ[sSlot[u + 1]];
-      tk.load_cached(kbase + jn * (kS * kD), tid);
-      tv.load_cached(vbase + jn * (kS * kD), tid);
-    }
-
+    wait_slots<L>(min(NB - 2, n - 1 - u));
+    block_barrier();
+    if (u + NB - 1 < n) issue(std::integral_constant<int, (b + NB - 1) % NB>{}, u + NB - 1);
+    const T* sK = slot_buf(B);
+    const T* sV = sK + TILE;
     // S^T (keys x queries): rows 0-31 in st0, 32-63 in st1
     f32x16 st0 = zero16(), st1 = zero16();
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const Frag<T> a0 = load_frag(sK + (lane & 31) * LD + 16 * kb + 8 * hh);
-      const Frag<T> a1 = load_frag(sK + (32 + (lane & 31)) * LD + 16 * kb + 8 * hh);
+      const Frag<T> a0 = lds_frag(sK, lane & 31, 16 * kb + 8 * hh);
+      const Frag<T> a1 = lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh);
       mma32(st0, a0, qf[kb]);
       mma32(st1, a1, qf[kb]);
     }
@@ -147,23 +170,19 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
     // softmax of this lane's query over the chunk's 64 keys (base-2 domain)
     float mx = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      st0[i] *= sc;
-      st1[i] *= sc;
-      mx = fmaxf(mx, fmaxf(st0[i], st1[i]));
-    }
-    mx = fmaxf(mx, xor32(mx));
+    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(st0[i], st1[i]));
+    mx = fmaxf(mx, xor32(mx)) * sc;
     if (OBO) mx = fmaxf(mx, 0.f);
     float sum = 0.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      st0[i] = __builtin_amdgcn_exp2f(st0[i] - mx);
-      st1[i] = __builtin_amdgcn_exp2f(st1[i] - mx);
+      st0[i] = __builtin_amdgcn_exp2f(fmaf(st0[i], sc, -mx));
+      st1[i] = __builtin_amdgcn_exp2f(fmaf(st1[i], sc, -mx));
       sum += st0[i] + st1[i];
     }
     sum += xor32(sum);
     if (OBO) sum += __builtin_amdgcn_exp2f(-mx);
-    if (lse && hh == 0) lse[qi * K + s] = (mx + __builtin_amdgcn_logf(sum)) * kLn2;
+    if (hh == 0) sLse[s * kS + qi] = (mx + __builtin_amdgcn_logf(sum)) * kLn2;
 
     // fuse w_s / l_s into P and accumulate O^T += V^T P^T
     const float coef = sW[s] / sum;
@@ -174,11 +193,17 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
     frag_from_acc(pf[3], st1, 1, coef);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const Frag<T> a0 = load_frag_t(sV, LD, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
-      const Frag<T> a1 = load_frag_t(sV, LD, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
+      const Frag<T> a0 = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
+      const Frag<T> a1 = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
       mma32(o0, a0, pf[kb]);
       mma32(o1, a1, pf[kb]);
     }
+  };
+  for (int u0 = 0; u0 < n; u0 += NB) {
+    step(std::integral_constant<int, 0>{}, u0);
+    if (u0 + 1 < n) step(std::integral_constant<int, 1>{}, u0 + 1);
+    if (NB > 2 && u0 + 2 < n) step(std::integral_constant<int, (NB > 2 ? 2 : 0)>{}, u0 + 2);
+    if (NB > 3 && u0 + 3 < n) step(std::integral_constant<int, (NB > 3 ? 3 : 0)>{}, u0 + 3);
   }
 
   // O^T accumulator: lane holds query qi, d = 32*dt + 8*g + 4*hh + 0..3
@@ -188,9 +213,13 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
     store4(orow + 8 * g + 4 * hh, o0[4 * g], o0[4 * g + 1], o0[4 * g + 2], o0[4 * g + 3]);
     store4(orow + 32 + 8 * g + 4 * hh, o1[4 * g], o1[4 * g + 1], o1[4 * g + 2], o1[4 * g + 3]);
   }
-  if (lse)
-    for (int e = tid; e < kS * K; e += kThreads)
-      if (sJ[e % K] < 0) lse[e] = -INFINITY;
+  if (lse) {
+    __syncthreads();
+    for (int e = tid; e < kS * K; e += kThreads) {
+      const int q = e / K, s = e % K;
+      lse[e] = sJ[s] >= 0 ? sLse[s * kS + q] : -INFINITY;
+    }
+  }
 }
 
 }  // namespace
