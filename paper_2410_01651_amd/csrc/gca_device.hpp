@@ -16,6 +16,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace gca {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
@@ -130,6 +132,10 @@ __device__ __forceinline__ void frag_from_acc(f32x8& f, const f32x16& acc, int h
   f.lo = f32x4{acc[8 * half + 0], acc[8 * half + 1], acc[8 * half + 2], acc[8 * half + 3]} * scale;
   f.hi = f32x4{acc[8 * half + 4], acc[8 * half + 5], acc[8 * half + 6], acc[8 * half + 7]} * scale;
 }
+
+// Entry m of a fragment as fp32.
+__device__ __forceinline__ float frag_elem(const bf16x8& f, int m) { return (float)f[m]; }
+__device__ __forceinline__ float frag_elem(const f32x8& f, int m) { return m < 4 ? f.lo[m] : f.hi[m - 4]; }
 
 // ------------------------------------------------------- element stores ----
 
@@ -261,6 +267,75 @@ __device__ __forceinline__ void dma_tile(const T* __restrict__ g, T* lds, int wa
 // Copy 64 floats spaced `stride` apart into 64 consecutive LDS floats (one wave).
 __device__ __forceinline__ void dma_column(const float* __restrict__ g, int64_t stride, float* lds, int lane) {
   dma_copy<4>(g + lane * stride, lds);
+}
+
+// Four LDS ring slots as separate variables (so each access names its slot at
+// compile time) and slot_buf(ic<b>) returning slot b.
+template <int V>
+using ic = std::integral_constant<int, V>;
+
+#define GCA_RING4(T, SIZE)                                \
+  __shared__ __attribute__((aligned(16))) T ring0[SIZE];  \
+  __shared__ __attribute__((aligned(16))) T ring1[SIZE];  \
+  __shared__ __attribute__((aligned(16))) T ring2[SIZE];  \
+  __shared__ __attribute__((aligned(16))) T ring3[SIZE];  \
+  auto slot_buf = [&](auto B) __device__ -> T* {          \
+    constexpr int b_ = decltype(B)::value;                \
+    if constexpr (b_ == 0) return ring0;                  \
+    else if constexpr (b_ == 1) return ring1;             \
+    else if constexpr (b_ == 2) return ring2;             \
+    else return ring3;                                    \
+  };
+
+// The same loop over one ring array with runtime slot indices (no per-slot code
+// copies, so the compiler keeps one set of lane address offsets).
+template <typename Issue, typename Run>
+__device__ __forceinline__ void pair_ring_dyn(int n, int pair, Issue&& issue, Run&& run) {
+  issue(0, 0);
+  if (n > 1) issue(1, 1);
+  for (int v = 0; 2 * v < n; ++v) {
+    wait_vmem<0>();
+    block_barrier();
+    const int base = 2 * (v & 1);
+    if (2 * v + 2 < n) issue(2 - base, 2 * v + 2);
+    if (2 * v + 3 < n) issue(3 - base, 2 * v + 3);
+    const int u = 2 * v + pair;
+    if (u < n) run(base + pair, u);
+  }
+}
+
+// Work loop of a 4-wave workgroup whose two wave pairs take alternate items of
+// a list of n items streamed through the 4-slot ring: round v computes items
+// 2v (pair 0) and 2v+1 (pair 1) from slots 2(v%2) and 2(v%2)+1 while the copies
+// for round v+1 fill the other two slots.  issue(ic<slot>, item) starts an
+// item's copies (all waves take part); run(ic<slot>, item) computes one item on
+// the calling pair.  Before each round every wave waits for all of its copies
+// (only the current round's are outstanding) and the barrier makes everyone's
+// copies visible and frees the slots of the previous round.
+template <typename Issue, typename Run>
+__device__ __forceinline__ void pair_ring(int n, int pair, Issue&& issue, Run&& run) {
+  issue(ic<0>{}, 0);
+  if (n > 1) issue(ic<1>{}, 1);
+  for (int v = 0; 2 * v < n; ++v) {
+    wait_vmem<0>();
+    block_barrier();
+    const int u = 2 * v + pair;
+    if ((v & 1) == 0) {
+      if (2 * v + 2 < n) issue(ic<2>{}, 2 * v + 2);
+      if (2 * v + 3 < n) issue(ic<3>{}, 2 * v + 3);
+      if (u < n) {
+        if (pair == 0) run(ic<0>{}, u);
+        else run(ic<1>{}, u);
+      }
+    } else {
+      if (2 * v + 2 < n) issue(ic<0>{}, 2 * v + 2);
+      if (2 * v + 3 < n) issue(ic<1>{}, 2 * v + 3);
+      if (u < n) {
+        if (pair == 0) run(ic<2>{}, u);
+        else run(ic<3>{}, u);
+      }
+    }
+  }
 }
 
 // Fragments from a swizzled tile: 8 consecutive elements of row r from column col

@@ -107,6 +107,20 @@ struct ScanPlan {
   int64_t slices;  // slices per retrieval row
 };
 
+// 8-element dot product accumulated in fp32 (bf16 products are exact in fp32).
+__device__ __forceinline__ float dot8(const bf16x8& a, const bf16x8& b, float acc) {
+#pragma unroll
+  for (int m = 0; m < 8; ++m) acc = fmaf((float)a[m], (float)b[m], acc);
+  return acc;
+}
+__device__ __forceinline__ float dot8(const f32x8& a, const f32x8& b, float acc) {
+  acc = fmaf(a.lo[0], b.lo[0], acc); acc = fmaf(a.lo[1], b.lo[1], acc);
+  acc = fmaf(a.lo[2], b.lo[2], acc); acc = fmaf(a.lo[3], b.lo[3], acc);
+  acc = fmaf(a.hi[0], b.hi[0], acc); acc = fmaf(a.hi[1], b.hi[1], acc);
+  acc = fmaf(a.hi[2], b.hi[2], acc); acc = fmaf(a.hi[3], b.hi[3], acc);
+  return acc;
+}
+
 ScanPlan scan_plan(int64_t nC) {
   int64_t per = (nC + kMaxScanSlices - 1) / kMaxScanSlices;
   if (per < 256) per = 256;
@@ -117,9 +131,10 @@ ScanPlan scan_plan(int64_t nC) {
   return p;
 }
 
-// Wave-level merge, then merge of the workgroup's 4 wave results by wave 0.
+// Wave-level merge, then merge of the workgroup's NW wave results by wave 0.
 // Leaves the workgroup's best (<= K) in lanes of wave 0: (ms, mj), cnt.
-template <int KM>
+// sS/sJ hold NW * 32 entries, sCnt NW.
+template <int KM, int NW>
 __device__ __forceinline__ void block_merge(TopList<KM>& L, int K, float* sS, int* sJ, int* sCnt, float& ms,
                                             int& mj, int& cnt) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -133,8 +148,10 @@ __device__ __forceinline__ void block_merge(TopList<KM>& L, int K, float* sS, in
   if (wave == 0) {
     L.init();
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
-      if (lane < sCnt[w]) L.insert(sS[w * 32 + lane], sJ[w * 32 + lane]);
+    for (int w0 = 0; w0 < NW; w0 += 2) {
+      const int w = w0 + (lane >> 5);  // lanes 0-31 take wave w0, lanes 32-63 wave w0 + 1
+      if (w < NW && (lane & 31) < sCnt[w]) L.insert(sS[w * 32 + (lane & 31)], sJ[w * 32 + (lane & 31)]);
+    }
     wave_merge(L, K, ms, mj, cnt);
   }
 }
@@ -147,9 +164,9 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
                                                                    int64_t slices) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   T* sq = reinterpret_cast<T*>(smem);
-  __shared__ float sS[128];
-  __shared__ int sJ[128];
-  __shared__ int sCnt[4];
+  __shared__ float sS[kScanThreads / 64 * 32];
+  __shared__ int sJ[kScanThreads / 64 * 32];
+  __shared__ int sCnt[kScanThreads / 64];
 
   const int64_t g = blockIdx.x % slices;
   const int64_t bhr = blockIdx.x / slices;
@@ -163,38 +180,42 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
   const int64_t hi = lo + per < nC ? lo + per : nC;
   TopList<KM> L;
   L.init();
+  // a wave scores two groups of 8 keys per round (lane: key lane/8, 16-byte
+  // column block lane%8 of every 128 bytes), so 2 * D/64 loads are in flight
+  constexpr int kWaves = kScanThreads / 64;
   int it = 0;
-  for (int64_t base = lo + wave * 8; base < hi; base += 32, ++it) {
-    const int64_t key = base + (lane >> 3);
-    float acc = 0.f;
-    if (key < hi) {
-      const T* kr = lk + (bhr * nC + key) * D;
-      for (int x = sub * 8; x < D; x += 64) {
-        const Frag<T> a = load_frag(kr + x);
-        const Frag<T> b = load_frag(sq + x);
-        if constexpr (sizeof(T) == 2) {
-#pragma unroll
-          for (int m = 0; m < 8; ++m) acc = fmaf((float)a[m], (float)b[m], acc);
-        } else {
-          acc = fmaf(a.lo[0], b.lo[0], acc); acc = fmaf(a.lo[1], b.lo[1], acc);
-          acc = fmaf(a.lo[2], b.lo[2], acc); acc = fmaf(a.lo[3], b.lo[3], acc);
-          acc = fmaf(a.hi[0], b.hi[0], acc); acc = fmaf(a.hi[1], b.hi[1], acc);
-          acc = fmaf(a.hi[2], b.hi[2], acc); acc = fmaf(a.hi[3], b.hi[3], acc);
-        }
-      }
+  for (int64_t base = lo + wave * 16; base < hi; base += 16 * kWaves, it += 2) {
+    const int64_t key0 = base + (lane >> 3), key1 = key0 + 8;
+    const T* kr0 = lk + (bhr * nC + (key0 < hi ? key0 : lo)) * D;
+    const T* kr1 = lk + (bhr * nC + (key1 < hi ? key1 : lo)) * D;
+    float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll 4
+    for (int x = sub * 8; x < D; x += 64) {
+      const Frag<T> a0 = load_frag(kr0 + x);
+      const Frag<T> a1 = load_frag(kr1 + x);
+      const Frag<T> b = load_frag(sq + x);
+      acc0 = dot8(a0, b, acc0);
+      acc1 = dot8(a1, b, acc1);
     }
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
-    acc += __shfl_xor(acc, 4);
+    acc0 += __shfl_xor(acc0, 1);
+    acc1 += __shfl_xor(acc1, 1);
+    acc0 += __shfl_xor(acc0, 2);
+    acc1 += __shfl_xor(acc1, 2);
+    acc0 += __shfl_xor(acc0, 4);
+    acc1 += __shfl_xor(acc1, 4);
     // spread the insertions of one key group over its 8 lanes
-    if (key < hi && sub == (it & 7)) {
-      const float v = acc * scale;
-      if (__builtin_isfinite(v)) L.insert(v, (int)key);
+    if (key0 < hi && sub == (it & 7)) {
+      const float v = acc0 * scale;
+      if (__builtin_isfinite(v)) L.insert(v, (int)key0);
+    }
+    if (key1 < hi && sub == ((it + 1) & 7)) {
+      const float v = acc1 * scale;
+      if (__builtin_isfinite(v)) L.insert(v, (int)key1);
     }
   }
   float ms;
   int mj, cnt;
-  block_merge(L, K, sS, sJ, sCnt, ms, mj, cnt);
+  block_merge<KM, kScanThreads / 64>(L, K, sS, sJ, sCnt, ms, mj, cnt);
   if (wave == 0 && lane < K) {
     const int64_t o = (bhr * slices + g) * K + lane;
     cs[o] = lane < cnt ? ms : -INFINITY;
@@ -202,24 +223,41 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
   }
 }
 
+constexpr int kMergeThreads = 1024;
+
 template <int KM>
-__global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restrict__ cs, const int* __restrict__ cj,
-                                                           int32_t* __restrict__ idx, float* __restrict__ sel,
-                                                           int K, int64_t slices) {
-  __shared__ float sS[128];
-  __shared__ int sJ[128];
-  __shared__ int sCnt[4];
+__global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(const float* __restrict__ cs,
+                                                                     const int* __restrict__ cj,
+                                                                     int32_t* __restrict__ idx,
+                                                                     float* __restrict__ sel, int K,
+                                                                     int64_t slices) {
+  constexpr int NW = kMergeThreads / 64;
+  __shared__ float sS[NW * 32];
+  __shared__ int sJ[NW * 32];
+  __shared__ int sCnt[NW];
   const int64_t bhr = blockIdx.x;
   const int64_t n = slices * K;
+  const float* c_s = cs + bhr * n;
+  const int* c_j = cj + bhr * n;
   TopList<KM> L;
   L.init();
-  for (int64_t e = threadIdx.x; e < n; e += 256) {
-    const int j = cj[bhr * n + e];
-    if (j >= 0) L.insert(cs[bhr * n + e], j);
+  // eight independent loads in flight per thread per round
+  for (int64_t base = threadIdx.x; base < n; base += 8 * kMergeThreads) {
+    float v[8];
+    int jv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int64_t e = base + q * kMergeThreads;
+      jv[q] = e < n ? c_j[e] : -1;
+      v[q] = e < n ? c_s[e] : -INFINITY;
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      if (jv[q] >= 0) L.insert(v[q], jv[q]);
   }
   float ms;
   int mj, cnt;
-  block_merge(L, K, sS, sJ, sCnt, ms, mj, cnt);
+  block_merge<KM, NW>(L, K, sS, sJ, sCnt, ms, mj, cnt);
   if ((threadIdx.x >> 6) == 0) write_sorted<KM>(idx + bhr * K, sel + bhr * K, K, ms, mj, cnt);
 }
 
@@ -364,7 +402,7 @@ hipError_t launch_decode_k(const Shape& s, const void* lq, const void* lk, int32
   note_launch("decode_scan_kernel", st);
   const hipError_t e = take_launch_error();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(decode_merge_kernel<KM>, dim3((unsigned)rows), dim3(256), 0, st, cs, cj, idx, sel, s.topk,
+  hipLaunchKernelGGL(decode_merge_kernel<KM>, dim3((unsigned)rows), dim3(kMergeThreads), 0, st, cs, cj, idx, sel, s.topk,
                      plan.slices);
   note_launch("decode_merge_kernel", st);
   return take_launch_error();

@@ -25,7 +25,7 @@
 namespace gca {
 namespace {
 
-constexpr int kThreads = 128;
+constexpr int kThreads = 256;  // two pairs of waves
 
 template <typename T> struct LdsLd;
 template <> struct LdsLd<__bf16> { static constexpr int v = 72; };
@@ -199,60 +199,26 @@ __global__ __launch_bounds__(256) void csr_sort_kernel(const int* __restrict__ o
   }
 }
 
-// LDS ring depth (retrieved chunks / retrievers in flight per workgroup).
-template <typename T> struct RingDepth;
-template <> struct RingDepth<__bf16> { static constexpr int v = 4; };
-template <> struct RingDepth<float> { static constexpr int v = 2; };
-
-#define GCA_RING_DECL(T, NB, SIZE)                                       \
-  __shared__ __attribute__((aligned(16))) T ring0[SIZE];                 \
-  __shared__ __attribute__((aligned(16))) T ring1[SIZE];                 \
-  __shared__ __attribute__((aligned(16))) T ring2[(NB) > 2 ? (SIZE) : 8]; \
-  __shared__ __attribute__((aligned(16))) T ring3[(NB) > 3 ? (SIZE) : 8]; \
-  auto slot_buf = [&](auto B) __device__ -> T* {                         \
-    constexpr int b_ = decltype(B)::value;                               \
-    if constexpr (b_ == 0) return ring0;                                 \
-    else if constexpr (b_ == 1) return ring1;                            \
-    else if constexpr (b_ == 2) return ring2;                            \
-    else return ring3;                                                   \
-  };
-
-template <int V>
-using ic = std::integral_constant<int, V>;
-
-// Runs step(ic<b>, u) for u = 0..n-1 with ring buffer b = u % NB known at compile
-// time, after issuing the copies for the first NB - 1 items.
-template <int NB, typename Issue, typename Step>
-__device__ __forceinline__ void ring_loop(int n, Issue&& issue, Step&& step) {
-  issue(ic<0>{}, 0);
-  if (NB > 2 && n > 1) issue(ic<1>{}, 1);
-  if (NB > 3 && n > 2) issue(ic<(NB > 3 ? 2 : 0)>{}, 2);
-  for (int u0 = 0; u0 < n; u0 += NB) {
-    step(ic<0>{}, u0);
-    if (u0 + 1 < n) step(ic<1>{}, u0 + 1);
-    if (NB > 2 && u0 + 2 < n) step(ic<(NB > 2 ? 2 : 0)>{}, u0 + 2);
-    if (NB > 3 && u0 + 3 < n) step(ic<(NB > 3 ? 3 : 0)>{}, u0 + 3);
-  }
-}
-
 // ------------------------------------------------- query-stationary dQ ----
 
+// One workgroup of four waves per (batch, head, query chunk); the two wave pairs
+// take alternate retrieved chunks from a four-slot LDS ring (K_j and V_j tiles),
+// each wave owning 32 query tokens.  dQ partials of the pairs are summed at the end.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t nwork) {
-  constexpr int NB = RingDepth<T>::v;
   constexpr int TILE = kS * kD;
-  constexpr int L = Swz<T>::kCPR;  // copies per wave per slot (K and V tiles over 2 waves)
-  GCA_RING_DECL(T, NB, 2 * TILE)
+  GCA_RING4(T, 2 * TILE)
   __shared__ float sL[32 * kS];  // [slot][query]: lse on entry, D_s on exit
   __shared__ float sW[32];
   __shared__ int sJ[32];
   __shared__ int sSlot[32];
   __shared__ int sN;
-  __shared__ float sPart[2][32];
+  __shared__ float sPart[4][32];
 
   const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
   if (wid >= nwork) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
+  const int pair = wave >> 1, half = wave & 1;
   const int64_t c = wid % p.nQ;
   const int64_t bh = wid / p.nQ;
   const int h = (int)(bh % p.H);
@@ -263,30 +229,27 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
   const int64_t row_base = (b * p.Hr + hr) * p.nQ;
   const int64_t tok0 = ((b * p.H + h) * p.nQ + c) * kS;
 
-  if (tid < 32) {
-    float wv = 0.f;
+  if (wave == 0) {
     int jv = -1;
-    if (t >= 0 && tid < K) {
-      const int j = p.idx[(row_base + t) * K + tid];
+    float wv = 0.f;
+    if (t >= 0 && lane < K) {
+      const int j = p.idx[(row_base + t) * K + lane];
       if (j >= 0 && j < p.nKV) {
         jv = j;
-        wv = p.ws.w[(row_base + t) * K + tid];
+        wv = p.ws.w[(row_base + t) * K + lane];
       }
     }
-    sW[tid] = wv;
-    sJ[tid] = jv;
-    sPart[0][tid] = 0.f;
-    sPart[1][tid] = 0.f;
+    const uint64_t mask = __ballot(jv >= 0);
+    if (lane < 32) {
+      sW[lane] = wv;
+      sJ[lane] = jv;
+    }
+    if (jv >= 0) sSlot[__popcll(mask & ((1ull << lane) - 1))] = lane;
+    if (lane == 0) sN = __popcll(mask);
   }
+  if (tid < 128) sPart[tid >> 5][tid & 31] = 0.f;
   if (t >= 0)
     for (int e = tid; e < kS * K; e += kThreads) sL[(e % K) * kS + e / K] = p.lse[tok0 * K + e];
-  __syncthreads();
-  if (tid == 0) {
-    int n = 0;
-    for (int s = 0; s < K; ++s)
-      if (sJ[s] >= 0) sSlot[n++] = s;
-    sN = n;
-  }
   __syncthreads();
   const int n = sN;
 
@@ -297,7 +260,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     return;
   }
 
-  const int qi = 32 * wave + (lane & 31);
+  const int qi = 32 * half + (lane & 31);
   const T* qrow = reinterpret_cast<const T*>(p.q) + (tok0 + qi) * kD;
   const T* dorow = reinterpret_cast<const T*>(p.dout) + (tok0 + qi) * kD;
   Frag<T> qf[4], df[4];
@@ -318,19 +281,14 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
   auto issue = [&](auto B, int u) __device__ {
     const int64_t j = sJ[sSlot[u]];
     T* dst = slot_buf(B);
-    dma_tile<T, 2>(kbase + j * TILE, dst, wave, lane);
-    dma_tile<T, 2>(vbase + j * TILE, dst + TILE, wave, lane);
+    dma_tile<T, 4>(kbase + j * TILE, dst, wave, lane);
+    dma_tile<T, 4>(vbase + j * TILE, dst + TILE, wave, lane);
   };
-  auto step = [&](auto B, int u) __device__ {
-    constexpr int bb = decltype(B)::value;
+  auto run = [&](auto B, int u) __device__ {
     const int s = sSlot[u];
-    wait_slots<L>(min(NB - 2, n - 1 - u));
-    block_barrier();
-    if (u + NB - 1 < n) issue(ic<(bb + NB - 1) % NB>{}, u + NB - 1);
     const T* sK = slot_buf(B);
     const T* sV = sK + TILE;
     const float lse2 = sL[s * kS + qi] * kLog2e;
-
     f32x16 s0 = zero16(), s1 = zero16(), p0 = zero16(), p1 = zero16();
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
@@ -348,7 +306,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
       Dq += s0[i] * p0[i] + s1[i] * p1[i];
     }
     Dq += xor32(Dq);
-    if (hh == 0) sL[s * kS + qi] = Dq;  // this lane alone read the lse it replaces
+    if (hh == 0) sL[s * kS + qi] = Dq;  // this lane's pair alone reads the lse it replaces
     const float ws = sW[s];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -371,18 +329,35 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     for (int o = 16; o >= 1; o >>= 1) dsum += __shfl_xor(dsum, o);
     if (lane == 0) sPart[wave][s] = dsum;
   };
-  ring_loop<NB>(n, issue, step);
+  pair_ring(n, pair, issue, run);
 
-  const float as = p.attn_scale;
-  T* drow = dq + qi * kD;
+  // pair 1 hands its dQ^T partial to pair 0 through LDS
+  float* part = reinterpret_cast<float*>(ring0);
+  __syncthreads();
+  if (pair == 1) {
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    store4(drow + 8 * g + 4 * hh, as * g0[4 * g], as * g0[4 * g + 1], as * g0[4 * g + 2], as * g0[4 * g + 3]);
-    store4(drow + 32 + 8 * g + 4 * hh, as * g1[4 * g], as * g1[4 * g + 1], as * g1[4 * g + 2],
-           as * g1[4 * g + 3]);
+    for (int g = 0; g < 4; ++g) {
+      *reinterpret_cast<f32x4*>(part + qi * kD + 8 * g + 4 * hh) =
+          f32x4{g0[4 * g], g0[4 * g + 1], g0[4 * g + 2], g0[4 * g + 3]};
+      *reinterpret_cast<f32x4*>(part + qi * kD + 32 + 8 * g + 4 * hh) =
+          f32x4{g1[4 * g], g1[4 * g + 1], g1[4 * g + 2], g1[4 * g + 3]};
+    }
   }
   __syncthreads();
-  if (tid < K) p.ws.dwp[(bh * p.nQ + t) * K + tid] = sPart[0][tid] + sPart[1][tid];
+  if (pair == 0) {
+    const float as = p.attn_scale;
+    T* drow = dq + qi * kD;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(part + qi * kD + 8 * g + 4 * hh);
+      const f32x4 x1 = *reinterpret_cast<const f32x4*>(part + qi * kD + 32 + 8 * g + 4 * hh);
+      store4(drow + 8 * g + 4 * hh, as * (g0[4 * g] + x0[0]), as * (g0[4 * g + 1] + x0[1]),
+             as * (g0[4 * g + 2] + x0[2]), as * (g0[4 * g + 3] + x0[3]));
+      store4(drow + 32 + 8 * g + 4 * hh, as * (g1[4 * g] + x1[0]), as * (g1[4 * g + 1] + x1[1]),
+             as * (g1[4 * g + 2] + x1[2]), as * (g1[4 * g + 3] + x1[3]));
+    }
+  }
+  if (tid < K) p.ws.dwp[(bh * p.nQ + t) * K + tid] = sPart[0][tid] + sPart[1][tid] + sPart[2][tid] + sPart[3][tid];
   float* Dout = p.ws.Dbuf + tok0 * K;
   for (int e = tid; e < kS * K; e += kThreads) {
     const int q = e / K, s = e % K;
@@ -392,18 +367,24 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
 
 // ---------------------------------------------- key-stationary dK, dV ----
 
+// One workgroup of four waves per (batch, head, key chunk j); the two wave pairs
+// take alternate retrievers (row t, slot s) of chunk j from a four-slot LDS ring
+// (Q_c and dO_c tiles plus the lse and D columns of slot s), each wave owning 32
+// of chunk j's keys.  dK/dV partials of the pairs are summed at the end.
 template <typename T>
-__global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t nwork) {
-  constexpr int NB = RingDepth<T>::v;
+__global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int64_t nwork) {
   constexpr int TILE = kS * kD;
-  constexpr int L = Swz<T>::kCPR + 1;  // per wave per retriever: Q/dO tile copies + one column
-  // ring entry: Q_c tile, dO_c tile, lse column, D column
+  // ring slot: Q_c tile, dO_c tile, lse column, D column
   constexpr int ENTRY = 2 * TILE + 2 * kS * (int)(sizeof(float) / sizeof(T));
-  GCA_RING_DECL(T, NB, ENTRY)
+  __shared__ __attribute__((aligned(16))) T ring[4 * ENTRY];
+  constexpr int NE = 256;  // retrievers staged in LDS per batch
+  __shared__ int sE[NE];
+  __shared__ float sWt[NE];
 
   const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
   if (wid >= nwork) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
+  const int pair = wave >> 1, half = wave & 1;
   const int64_t j = wid % p.nKV;
   const int64_t bh = wid / p.nKV;
   const int h = (int)(bh % p.H);
@@ -415,9 +396,6 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t
   const int lo = off[j], hi = off[j + 1];
   const int* list_g = p.ws.sorted + bhr * p.nQ * K + lo;
   const int n = hi - lo;
-  constexpr int NE = 256;  // retrievers staged in LDS per batch
-  __shared__ int sE[NE];
-  __shared__ float sWt[NE];
 
   const int64_t key0 = (bh * p.nKV + j) * kS;  // first key token of chunk j
   T* dk = reinterpret_cast<T*>(p.dk) + key0 * kD;
@@ -431,7 +409,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t
   }
 
   // this wave's 32 keys of chunk j as B operands (K^T, V^T columns)
-  const int kr = 32 * wave + (lane & 31);
+  const int kr = 32 * half + (lane & 31);
   const T* krow = reinterpret_cast<const T*>(p.k) + (key0 + kr) * kD;
   const T* vrow = reinterpret_cast<const T*>(p.v) + (key0 + kr) * kD;
   Frag<T> kf[4], vf[4];
@@ -448,82 +426,96 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t
   const float* Db = p.ws.Dbuf + bh * p.nQ * kS * K;
   const float* wrow = p.ws.w + bhr * p.nQ * K;
 
-  auto issue = [&](auto B, int u) __device__ {
+  auto issue = [&](int slot, int u) __device__ {
     const int e = sE[u];
     const int64_t c = e / K + p.causal;
     const int s = e % K;
-    T* dst = slot_buf(B);
-    dma_tile<T, 2>(qb + c * TILE, dst, wave, lane);
-    dma_tile<T, 2>(ob + c * TILE, dst + TILE, wave, lane);
+    T* dst = ring + slot * ENTRY;
+    dma_tile<T, 4>(qb + c * TILE, dst, wave, lane);
+    dma_tile<T, 4>(ob + c * TILE, dst + TILE, wave, lane);
     float* cols = reinterpret_cast<float*>(dst + 2 * TILE);
     if (wave == 0) dma_column(lseb + c * kS * K + s, K, cols, lane);
-    else dma_column(Db + c * kS * K + s, K, cols + kS, lane);
+    else if (wave == 1) dma_column(Db + c * kS * K + s, K, cols + kS, lane);
   };
 
   f32x16 dv0 = zero16(), dv1 = zero16(), dk0 = zero16(), dk1 = zero16();
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
-  int nb = 0;  // retrievers in the current batch
 
-  auto step = [&](auto B, int u) __device__ {
-    constexpr int bb = decltype(B)::value;
+  auto run = [&](int slot, int u) __device__ {
     const float wt = sWt[u];
-    wait_slots<L>(min(NB - 2, nb - 1 - u));
-    block_barrier();
-    if (u + NB - 1 < nb) issue(ic<(bb + NB - 1) % NB>{}, u + NB - 1);
-    const T* sQ = slot_buf(B);
+    const T* sQ = ring + slot * ENTRY;
     const T* sO = sQ + TILE;
     const float* sL = reinterpret_cast<const float*>(sQ + 2 * TILE);
     const float* sD = sL + kS;
-
-    // S = Q K^T and dP = dO V^T for this wave's keys; queries 0-31 / 32-63
-    f32x16 s0 = zero16(), s1 = zero16(), p0 = zero16(), p1 = zero16();
+    // S = Q K^T for this wave's keys; queries 0-31 in s0, 32-63 in s1
+    Frag<T> wp[4];
+    {
+      f32x16 s0 = zero16(), s1 = zero16();
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      mma32(s0, lds_frag(sQ, lane & 31, 16 * kb + 8 * hh), kf[kb]);
-      mma32(s1, lds_frag(sQ, 32 + (lane & 31), 16 * kb + 8 * hh), kf[kb]);
-      mma32(p0, lds_frag(sO, lane & 31, 16 * kb + 8 * hh), vf[kb]);
-      mma32(p1, lds_frag(sO, 32 + (lane & 31), 16 * kb + 8 * hh), vf[kb]);
-    }
-    // accumulator row i holds query 32*qt + 8*(i/4) + 4*hh + i%4
-    Frag<T> wp[4], ds[4];
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 l0 = *reinterpret_cast<const f32x4*>(sL + 8 * g + 4 * hh);
-      const f32x4 l1 = *reinterpret_cast<const f32x4*>(sL + 32 + 8 * g + 4 * hh);
-      const f32x4 d0 = *reinterpret_cast<const f32x4*>(sD + 8 * g + 4 * hh);
-      const f32x4 d1 = *reinterpret_cast<const f32x4*>(sD + 32 + 8 * g + 4 * hh);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float pa = wt * __builtin_amdgcn_exp2f(fmaf(s0[4 * g + r], sc, -l0[r] * kLog2e));
-        const float pb = wt * __builtin_amdgcn_exp2f(fmaf(s1[4 * g + r], sc, -l1[r] * kLog2e));
-        s0[4 * g + r] = pa;
-        s1[4 * g + r] = pb;
-        p0[4 * g + r] = pa * (p0[4 * g + r] - d0[r]);
-        p1[4 * g + r] = pb * (p1[4 * g + r] - d1[r]);
+      for (int kb = 0; kb < 4; ++kb) {
+        mma32(s0, lds_frag(sQ, lane & 31, 16 * kb + 8 * hh), kf[kb]);
+        mma32(s1, lds_frag(sQ, 32 + (lane & 31), 16 * kb + 8 * hh), kf[kb]);
       }
+      // w P; accumulator row i holds query 32*qt + 8*(i/4) + 4*hh + i%4
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 l0 = *reinterpret_cast<const f32x4*>(sL + 8 * g + 4 * hh);
+        const f32x4 l1 = *reinterpret_cast<const f32x4*>(sL + 32 + 8 * g + 4 * hh);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          s0[4 * g + r] = wt * __builtin_amdgcn_exp2f(fmaf(s0[4 * g + r], sc, -l0[r] * kLog2e));
+          s1[4 * g + r] = wt * __builtin_amdgcn_exp2f(fmaf(s1[4 * g + r], sc, -l1[r] * kLog2e));
+        }
+      }
+      frag_from_acc(wp[0], s0, 0, 1.f);
+      frag_from_acc(wp[1], s0, 1, 1.f);
+      frag_from_acc(wp[2], s1, 0, 1.f);
+      frag_from_acc(wp[3], s1, 1, 1.f);
     }
-    frag_from_acc(wp[0], s0, 0, 1.f);
-    frag_from_acc(wp[1], s0, 1, 1.f);
-    frag_from_acc(wp[2], s1, 0, 1.f);
-    frag_from_acc(wp[3], s1, 1, 1.f);
-    frag_from_acc(ds[0], p0, 0, 1.f);
-    frag_from_acc(ds[1], p0, 1, 1.f);
-    frag_from_acc(ds[2], p1, 0, 1.f);
-    frag_from_acc(ds[3], p1, 1, 1.f);
-    // dV^T += dO^T (wP), dK^T += Q^T dS  (contraction over the 64 queries)
+    // dV^T += dO^T (w P)  (contraction over the 64 queries)
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       mma32(dv0, lds_frag_t(sO, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), wp[kb]);
       mma32(dv1, lds_frag_t(sO, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), wp[kb]);
+    }
+    // dP = dO V^T, then dS = w P o (dP - D) from the w P fragments
+    Frag<T> ds[4];
+    {
+      f32x16 p0 = zero16(), p1 = zero16();
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        mma32(p0, lds_frag(sO, lane & 31, 16 * kb + 8 * hh), vf[kb]);
+        mma32(p1, lds_frag(sO, 32 + (lane & 31), 16 * kb + 8 * hh), vf[kb]);
+      }
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 d0 = *reinterpret_cast<const f32x4*>(sD + 8 * g + 4 * hh);
+        const f32x4 d1 = *reinterpret_cast<const f32x4*>(sD + 32 + 8 * g + 4 * hh);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = 4 * g + r;  // register i of tile qt lives in wp[2*qt + i/8] entry i%8
+          p0[i] = frag_elem(wp[i >> 3], i & 7) * (p0[i] - d0[r]);
+          p1[i] = frag_elem(wp[2 + (i >> 3)], i & 7) * (p1[i] - d1[r]);
+        }
+      }
+      frag_from_acc(ds[0], p0, 0, 1.f);
+      frag_from_acc(ds[1], p0, 1, 1.f);
+      frag_from_acc(ds[2], p1, 0, 1.f);
+      frag_from_acc(ds[3], p1, 1, 1.f);
+    }
+    // dK^T += Q^T dS
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
       mma32(dk0, lds_frag_t(sQ, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), ds[kb]);
       mma32(dk1, lds_frag_t(sQ, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), ds[kb]);
     }
   };
-  // the retriever list is staged through LDS in batches; each batch runs its
-  // own ring of copies, drained at the batch's end
+
+  // the retriever list is staged through LDS in batches, each streamed through
+  // the ring and drained at its end
   for (int b0 = 0; b0 < n; b0 += NE) {
-    nb = min(NE, n - b0);
+    const int nb = min(NE, n - b0);
     __syncthreads();
     for (int i = tid; i < nb; i += kThreads) {
       const int e = list_g[b0 + i];
@@ -531,20 +523,48 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(BwdParams p, int64_t
       sWt[i] = wrow[e];
     }
     __syncthreads();
-    ring_loop<NB>(nb, issue, step);
+    pair_ring_dyn(nb, pair, issue, run);
   }
 
-  // accumulators are transposed: lane holds key kr, d = 32*dt + 8*g + 4*hh + 0..3
-  const float as = p.attn_scale;
-  T* dkr = dk + kr * kD;
-  T* dvr = dv + kr * kD;
+  // pair 1 hands its dK^T/dV^T partials to pair 0 through LDS: dV in ring0,
+  // dK in ring1, each [half][tile][register][lane] fp32 (16 KB)
+  float* partv = reinterpret_cast<float*>(ring);
+  float* partk = reinterpret_cast<float*>(ring + ENTRY);
+  __syncthreads();
+  auto slot = [&](int which, int i) {
+    return (which < 2 ? partv : partk) + ((half * 2 + (which & 1)) * 16 + i) * 64 + lane;
+  };
+  if (pair == 1) {
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    store4(dvr + 8 * g + 4 * hh, dv0[4 * g], dv0[4 * g + 1], dv0[4 * g + 2], dv0[4 * g + 3]);
-    store4(dvr + 32 + 8 * g + 4 * hh, dv1[4 * g], dv1[4 * g + 1], dv1[4 * g + 2], dv1[4 * g + 3]);
-    store4(dkr + 8 * g + 4 * hh, as * dk0[4 * g], as * dk0[4 * g + 1], as * dk0[4 * g + 2], as * dk0[4 * g + 3]);
-    store4(dkr + 32 + 8 * g + 4 * hh, as * dk1[4 * g], as * dk1[4 * g + 1], as * dk1[4 * g + 2],
-           as * dk1[4 * g + 3]);
+    for (int i = 0; i < 16; ++i) {
+      *slot(0, i) = dv0[i];
+      *slot(1, i) = dv1[i];
+      *slot(2, i) = dk0[i];
+      *slot(3, i) = dk1[i];
+    }
+  }
+  __syncthreads();
+  if (pair == 0) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      dv0[i] += *slot(0, i);
+      dv1[i] += *slot(1, i);
+      dk0[i] += *slot(2, i);
+      dk1[i] += *slot(3, i);
+    }
+    // accumulators are transposed: lane holds key kr, d = 32*dt + 8*g + 4*hh + 0..3
+    const float as = p.attn_scale;
+    T* dkr = dk + kr * kD;
+    T* dvr = dv + kr * kD;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      store4(dvr + 8 * g + 4 * hh, dv0[4 * g], dv0[4 * g + 1], dv0[4 * g + 2], dv0[4 * g + 3]);
+      store4(dvr + 32 + 8 * g + 4 * hh, dv1[4 * g], dv1[4 * g + 1], dv1[4 * g + 2], dv1[4 * g + 3]);
+      store4(dkr + 8 * g + 4 * hh, as * dk0[4 * g], as * dk0[4 * g + 1], as * dk0[4 * g + 2],
+             as * dk0[4 * g + 3]);
+      store4(dkr + 32 + 8 * g + 4 * hh, as * dk1[4 * g], as * dk1[4 * g + 1], as * dk1[4 * g + 2],
+             as * dk1[4 * g + 3]);
+    }
   }
 }
 

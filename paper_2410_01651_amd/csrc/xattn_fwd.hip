@@ -1,16 +1,17 @@
 // Grouped cross attention forward (Eq. 2-3 of the method; Algorithm 1 in the
 // appendix is its tiled form).
 //
-// One workgroup of two waves per (batch, head, query chunk).  Each wave owns 32
-// of the chunk's 64 query tokens and keeps their Q fragments in registers for
-// the whole kernel.  The retrieved chunks' keys and values stream through a
-// ring of LDS slots filled by asynchronous direct-to-LDS copies, several
-// chunks ahead of the one being computed.  For every slot the workgroup
-// computes S^T = K Q^T on the
+// One workgroup of four waves per (batch, head, query chunk): two pairs of
+// waves take alternate retrieved chunks, and within a pair each wave owns 32 of
+// the chunk's 64 query tokens and keeps their Q fragments in registers.  The
+// retrieved chunks' keys and values stream through a four-slot LDS ring filled
+// by asynchronous direct-to-LDS copies one round ahead of the compute (two
+// waves per SIMD hide each other's MFMA, LDS and cross-lane latencies).  For
+// every retrieved chunk (slot) a pair computes S^T = K Q^T on the
 // matrix cores, takes each query's softmax over the 64 keys (one retrieved
 // chunk is exactly one tile, so no running rescale is needed), folds the
-// fusion weight w_s / l_s into P, and accumulates O^T += V^T (w_s P_s)^T into a
-// single fp32 accumulator shared by all slots.  The per-chunk outputs O'_s of
+// fusion weight w_s / l_s into P, and accumulates O^T += V^T (w_s P_s)^T into one
+// fp32 accumulator per pair; the two pairs' accumulators are summed at the end.  The per-chunk outputs O'_s of
 // Algorithm 1 are never written; the log-sum-exp of every (row, slot) is.
 //
 // Computing the transposed products keeps every query's statistics inside one
@@ -25,7 +26,7 @@
 namespace gca {
 namespace {
 
-constexpr int kThreads = 128;
+constexpr int kThreads = 256;  // two pairs of waves
 
 template <typename T> struct LdsLd;
 template <> struct LdsLd<__bf16> { static constexpr int v = 72; };  // 144-byte rows
@@ -46,22 +47,10 @@ struct FwdParams {
   float attn_scale;
 };
 
-// LDS ring depth (retrieved chunks in flight per workgroup).
-template <typename T> struct RingDepth;
-template <> struct RingDepth<__bf16> { static constexpr int v = 4; };  // 4 x 16 KB
-template <> struct RingDepth<float> { static constexpr int v = 2; };   // 2 x 32 KB
-
 template <typename T, bool OBO>
 __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
-  constexpr int NB = RingDepth<T>::v;
   constexpr int TILE = kS * kD;
-  constexpr int L = Swz<T>::kCPR;  // copies per wave per slot: 2 tiles x kCPR / 2 waves
-  // one LDS variable per ring slot: with the slot known at compile time in the
-  // unrolled loop below, the compiler waits only for that slot's copies
-  __shared__ __attribute__((aligned(16))) T ring0[2 * TILE];
-  __shared__ __attribute__((aligned(16))) T ring1[2 * TILE];
-  __shared__ __attribute__((aligned(16))) T ring2[NB > 2 ? 2 * TILE : 8];
-  __shared__ __attribute__((aligned(16))) T ring3[NB > 3 ? 2 * TILE : 8];
+  GCA_RING4(T, 2 * TILE)           // each slot: one retrieved chunk's K and V tiles
   __shared__ float sLse[32 * kS];  // [slot][query]
   __shared__ float sW[32];
   __shared__ int sJ[32];
@@ -71,6 +60,7 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
   const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
   if (wid >= p.nwork) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
+  const int pair = wave >> 1, half = wave & 1;
   const int64_t c = wid % p.nQ;
   const int64_t bh = wid / p.nQ;
   const int h = (int)(bh % p.H);
@@ -83,7 +73,7 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
   // The retrieval row's slots (Eq. 2 weights, compacted list of valid slots) by
   // wave 0 with one load per slot; wave 1 writes the weights of the causal last
   // row, which feeds no chunk and is owned by chunk 0.
-  if (wave == 0 || (p.w && p.causal && c == 0 && (p.Hr != 1 || h == 0))) {
+  if (wave == 0 || (wave == 1 && p.w && p.causal && c == 0 && (p.Hr != 1 || h == 0))) {
     const int64_t row = wave == 0 ? t : p.nQ - 1;
     float wv = 0.f;
     int jv = -1;
@@ -116,7 +106,7 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
     return;
   }
 
-  const int qi = 32 * wave + (lane & 31);  // this lane's query token within the chunk
+  const int qi = 32 * half + (lane & 31);  // this lane's query token within the chunk
   const T* qrow = reinterpret_cast<const T*>(p.q) + (tok0 + qi) * kD;
   Frag<T> qf[4];
 #pragma unroll
@@ -126,47 +116,28 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
   const int64_t kv0 = (b * p.H + h) * p.nKV * TILE;
   const T* kbase = reinterpret_cast<const T*>(p.k) + kv0;
   const T* vbase = reinterpret_cast<const T*>(p.v) + kv0;
-  auto slot_buf = [&](auto B) __device__ -> T* {
-    constexpr int b = decltype(B)::value;
-    if constexpr (b == 0) return ring0;
-    else if constexpr (b == 1) return ring1;
-    else if constexpr (b == 2) return ring2;
-    else return ring3;
-  };
   auto issue = [&](auto B, int u) __device__ {
     const int64_t j = sJ[sSlot[u]];
     T* dst = slot_buf(B);
-    dma_tile<T, 2>(kbase + j * TILE, dst, wave, lane);
-    dma_tile<T, 2>(vbase + j * TILE, dst + TILE, wave, lane);
+    dma_tile<T, 4>(kbase + j * TILE, dst, wave, lane);
+    dma_tile<T, 4>(vbase + j * TILE, dst + TILE, wave, lane);
   };
-  issue(std::integral_constant<int, 0>{}, 0);
-  if (NB > 2 && n > 1) issue(std::integral_constant<int, 1>{}, 1);
-  if (NB > 3 && n > 2) issue(std::integral_constant<int, (NB > 3 ? 2 : 0)>{}, 2);
 
   f32x16 o0 = zero16(), o1 = zero16();
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
 
-  // one slot of work on ring buffer B; the copy for slot u + NB - 1 goes to the
-  // buffer slot u - 1 used, which every wave has finished reading at the barrier
-  auto step = [&](auto B, int u) __device__ {
-    constexpr int b = decltype(B)::value;
+  auto run = [&](auto B, int u) __device__ {
     const int s = sSlot[u];
-    wait_slots<L>(min(NB - 2, n - 1 - u));
-    block_barrier();
-    if (u + NB - 1 < n) issue(std::integral_constant<int, (b + NB - 1) % NB>{}, u + NB - 1);
     const T* sK = slot_buf(B);
     const T* sV = sK + TILE;
     // S^T (keys x queries): rows 0-31 in st0, 32-63 in st1
     f32x16 st0 = zero16(), st1 = zero16();
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const Frag<T> a0 = lds_frag(sK, lane & 31, 16 * kb + 8 * hh);
-      const Frag<T> a1 = lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh);
-      mma32(st0, a0, qf[kb]);
-      mma32(st1, a1, qf[kb]);
+      mma32(st0, lds_frag(sK, lane & 31, 16 * kb + 8 * hh), qf[kb]);
+      mma32(st1, lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh), qf[kb]);
     }
-
     // softmax of this lane's query over the chunk's 64 keys (base-2 domain)
     float mx = -INFINITY;
 #pragma unroll
@@ -183,7 +154,6 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
     sum += xor32(sum);
     if (OBO) sum += __builtin_amdgcn_exp2f(-mx);
     if (hh == 0) sLse[s * kS + qi] = (mx + __builtin_amdgcn_logf(sum)) * kLn2;
-
     // fuse w_s / l_s into P and accumulate O^T += V^T P^T
     const float coef = sW[s] / sum;
     Frag<T> pf[4];
@@ -193,28 +163,39 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
     frag_from_acc(pf[3], st1, 1, coef);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const Frag<T> a0 = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
-      const Frag<T> a1 = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
-      mma32(o0, a0, pf[kb]);
-      mma32(o1, a1, pf[kb]);
+      mma32(o0, lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), pf[kb]);
+      mma32(o1, lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), pf[kb]);
     }
   };
-  for (int u0 = 0; u0 < n; u0 += NB) {
-    step(std::integral_constant<int, 0>{}, u0);
-    if (u0 + 1 < n) step(std::integral_constant<int, 1>{}, u0 + 1);
-    if (NB > 2 && u0 + 2 < n) step(std::integral_constant<int, (NB > 2 ? 2 : 0)>{}, u0 + 2);
-    if (NB > 3 && u0 + 3 < n) step(std::integral_constant<int, (NB > 3 ? 3 : 0)>{}, u0 + 3);
-  }
+  pair_ring(n, pair, issue, run);
 
-  // O^T accumulator: lane holds query qi, d = 32*dt + 8*g + 4*hh + 0..3
-  T* orow = out + qi * kD;
+  // pair 1 hands its partial O^T to pair 0 through LDS (the ring is free now)
+  float* part = reinterpret_cast<float*>(ring0);  // [query][d] fp32, 16 KB
+  __syncthreads();
+  if (pair == 1) {
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    store4(orow + 8 * g + 4 * hh, o0[4 * g], o0[4 * g + 1], o0[4 * g + 2], o0[4 * g + 3]);
-    store4(orow + 32 + 8 * g + 4 * hh, o1[4 * g], o1[4 * g + 1], o1[4 * g + 2], o1[4 * g + 3]);
+    for (int g = 0; g < 4; ++g) {
+      *reinterpret_cast<f32x4*>(part + qi * kD + 8 * g + 4 * hh) =
+          f32x4{o0[4 * g], o0[4 * g + 1], o0[4 * g + 2], o0[4 * g + 3]};
+      *reinterpret_cast<f32x4*>(part + qi * kD + 32 + 8 * g + 4 * hh) =
+          f32x4{o1[4 * g], o1[4 * g + 1], o1[4 * g + 2], o1[4 * g + 3]};
+    }
+  }
+  __syncthreads();
+  if (pair == 0) {
+    // O^T accumulator: lane holds query qi, d = 32*dt + 8*g + 4*hh + 0..3
+    T* orow = out + qi * kD;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 a = *reinterpret_cast<const f32x4*>(part + qi * kD + 8 * g + 4 * hh);
+      const f32x4 bq = *reinterpret_cast<const f32x4*>(part + qi * kD + 32 + 8 * g + 4 * hh);
+      store4(orow + 8 * g + 4 * hh, o0[4 * g] + a[0], o0[4 * g + 1] + a[1], o0[4 * g + 2] + a[2],
+             o0[4 * g + 3] + a[3]);
+      store4(orow + 32 + 8 * g + 4 * hh, o1[4 * g] + bq[0], o1[4 * g + 1] + bq[1], o1[4 * g + 2] + bq[2],
+             o1[4 * g + 3] + bq[3]);
+    }
   }
   if (lse) {
-    __syncthreads();
     for (int e = tid; e < kS * K; e += kThreads) {
       const int q = e / K, s = e % K;
       lse[e] = sJ[s] >= 0 ? sLse[s * kS + q] : -INFINITY;
