@@ -379,6 +379,17 @@ __device__ __forceinline__ f32x8 lds_frag_t(const float* tile, int r0, int r1, i
 
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
 
+// x[l] op x[l ^ 32] in every lane with one v_permlane32_swap (no LDS round
+// trip): swapping the wave's halves hands each lane the pair {x[l], x[l ^ 32]}.
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // Map a 1-D block id to a logical work id so that each of the 8 XCDs (which
 // receive blocks round-robin) works on one contiguous range of logical ids and
 // its private L2 sees a coherent working set.  The grid must be a multiple of 8

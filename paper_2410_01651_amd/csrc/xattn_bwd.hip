@@ -213,7 +213,6 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
   __shared__ int sJ[32];
   __shared__ int sSlot[32];
   __shared__ int sN;
-  __shared__ float sPart[4][32];
 
   const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
   if (wid >= nwork) return;
@@ -247,7 +246,6 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     if (jv >= 0) sSlot[__popcll(mask & ((1ull << lane) - 1))] = lane;
     if (lane == 0) sN = __popcll(mask);
   }
-  if (tid < 128) sPart[tid >> 5][tid & 31] = 0.f;
   if (t >= 0)
     for (int e = tid; e < kS * K; e += kThreads) sL[(e % K) * kS + e / K] = p.lse[tok0 * K + e];
   __syncthreads();
@@ -305,7 +303,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
       s1[i] = __builtin_amdgcn_exp2f(fmaf(s1[i], sc, -lse2));
       Dq += s0[i] * p0[i] + s1[i] * p1[i];
     }
-    Dq += xor32(Dq);
+    Dq = sum_xor32(Dq);
     if (hh == 0) sL[s * kS + qi] = Dq;  // this lane's pair alone reads the lse it replaces
     const float ws = sW[s];
 #pragma unroll
@@ -323,11 +321,6 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
       mma32(g0, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), f[kb]);
       mma32(g1, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), f[kb]);
     }
-    // this wave's share of dw[t, s]: sum of D over its 32 queries
-    float dsum = Dq;
-#pragma unroll
-    for (int o = 16; o >= 1; o >>= 1) dsum += __shfl_xor(dsum, o);
-    if (lane == 0) sPart[wave][s] = dsum;
   };
   pair_ring(n, pair, issue, run);
 
@@ -357,7 +350,17 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
              as * (g1[4 * g + 2] + x1[2]), as * (g1[4 * g + 3] + x1[3]));
     }
   }
-  if (tid < K) p.ws.dwp[(bh * p.nQ + t) * K + tid] = sPart[0][tid] + sPart[1][tid] + sPart[2][tid] + sPart[3][tid];
+  // dw[t, s] = sum over the chunk's 64 queries of D_s (staged in sL): 8 threads per slot
+  {
+    const int s = tid >> 3, part8 = tid & 7;
+    float acc = 0.f;
+    if (s < K && sJ[s] >= 0)
+      for (int q = part8; q < kS; q += 8) acc += sL[s * kS + q];
+    acc += __shfl_xor(acc, 1);
+    acc += __shfl_xor(acc, 2);
+    acc += __shfl_xor(acc, 4);
+    if (s < K && part8 == 0) p.ws.dwp[(bh * p.nQ + t) * K + s] = acc;
+  }
   float* Dout = p.ws.Dbuf + tok0 * K;
   for (int e = tid; e < kS * K; e += kThreads) {
     const int q = e / K, s = e % K;

@@ -43,106 +43,135 @@ struct FwdParams {
   float* w;
   int H, Hr, topk;
   int64_t nQ, nKV, nwork;
+  int64_t per;  // chunks per workgroup
   int causal;
   float attn_scale;
 };
 
+// Per-lane retrieval metadata of one landmark row: lane s < K holds slot s's
+// chunk index and raw score (chunk -1 for lanes >= K or rows that do not exist).
+struct RowMeta {
+  int j;
+  float sv;
+};
+
+__device__ __forceinline__ RowMeta load_row_meta(const FwdParams& p, int64_t row_off, bool exists) {
+  const int lane = threadIdx.x & 63;
+  RowMeta m{-1, -INFINITY};
+  if (exists && lane < p.topk) {
+    m.j = p.idx[row_off + lane];
+    m.sv = p.sel[row_off + lane];
+  }
+  return m;
+}
+
 template <typename T, bool OBO>
-__global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
+__global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   constexpr int TILE = kS * kD;
   GCA_RING4(T, 2 * TILE)           // each slot: one retrieved chunk's K and V tiles
-  __shared__ float sLse[32 * kS];  // [slot][query]
-  __shared__ float sW[32];
-  __shared__ int sJ[32];
-  __shared__ int sSlot[32];
-  __shared__ int sN;
+  __shared__ float sLse[32 * kS];  // current chunk: [slot][query]
+  __shared__ float sW[2][32];      // slot lists of the current and the next chunk
+  __shared__ int sJ[2][32];
+  __shared__ int sSlot[2][32];
+  __shared__ int sN[2];
 
-  const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
-  if (wid >= p.nwork) return;
+  const int64_t g = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int64_t c_begin = g * p.per;
+  const int64_t c_end = c_begin + p.per < p.nwork ? c_begin + p.per : p.nwork;
+  if (c_begin >= c_end) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
-  const int64_t c = wid % p.nQ;
-  const int64_t bh = wid / p.nQ;
-  const int h = (int)(bh % p.H);
-  const int64_t b = bh / p.H;
-  const int hr = p.Hr == 1 ? 0 : h;
-  const int64_t t = p.causal ? c - 1 : 0;
   const int K = p.topk;
-  const int64_t row_base = (b * p.Hr + hr) * p.nQ;  // retrieval rows of (b, hr)
-
-  // The retrieval row's slots (Eq. 2 weights, compacted list of valid slots) by
-  // wave 0 with one load per slot; wave 1 writes the weights of the causal last
-  // row, which feeds no chunk and is owned by chunk 0.
-  if (wave == 0 || (wave == 1 && p.w && p.causal && c == 0 && (p.Hr != 1 || h == 0))) {
-    const int64_t row = wave == 0 ? t : p.nQ - 1;
-    float wv = 0.f;
-    int jv = -1;
-    const bool any = row >= 0 && wave_row_weight(p.idx, p.sel, (row_base + row) * K, K, p.nKV, wv, jv);
-    if (wave == 0) {
-      const uint64_t mask = __ballot(jv >= 0 && lane < K);
-      if (lane < 32) {
-        sW[lane] = wv;
-        sJ[lane] = jv;
-      }
-      if (jv >= 0 && lane < K) sSlot[__popcll(mask & ((1ull << lane) - 1))] = lane;
-      if (lane == 0) sN = any ? __popcll(mask) : 0;
-      // this row's weights go out with the chunk it feeds
-      if (p.w && row >= 0 && lane < K && (p.Hr != 1 || h == 0)) p.w[(row_base + row) * K + lane] = wv;
-    } else if (lane < K) {
-      p.w[(row_base + row) * K + lane] = wv;
-    }
-  }
-  __syncthreads();
-  const int n = sN;
-
-  const int64_t tok0 = ((b * p.H + h) * p.nQ + c) * kS;  // first query token of the chunk
-  T* out = reinterpret_cast<T*>(p.out) + tok0 * kD;
-  float* lse = p.lse ? p.lse + tok0 * K : nullptr;
-
-  if (n == 0) {
-    for (int e = tid; e < kS * kD / 4; e += kThreads) store4(out + 4 * e, 0.f, 0.f, 0.f, 0.f);
-    if (lse)
-      for (int e = tid; e < kS * K; e += kThreads) lse[e] = -INFINITY;
-    return;
-  }
-
-  const int qi = 32 * half + (lane & 31);  // this lane's query token within the chunk
-  const T* qrow = reinterpret_cast<const T*>(p.q) + (tok0 + qi) * kD;
-  Frag<T> qf[4];
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qrow + 16 * kb + 8 * hh);
-  wait_vmem<0>();  // nothing but the chunk copies may be pending inside the slot loop
-
-  const int64_t kv0 = (b * p.H + h) * p.nKV * TILE;
-  const T* kbase = reinterpret_cast<const T*>(p.k) + kv0;
-  const T* vbase = reinterpret_cast<const T*>(p.v) + kv0;
-  auto issue = [&](auto B, int u) __device__ {
-    const int64_t j = sJ[sSlot[u]];
-    T* dst = slot_buf(B);
-    dma_tile<T, 4>(kbase + j * TILE, dst, wave, lane);
-    dma_tile<T, 4>(vbase + j * TILE, dst + TILE, wave, lane);
-  };
-
-  f32x16 o0 = zero16(), o1 = zero16();
+  const int qi = 32 * half + (lane & 31);  // this lane's query token within a chunk
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
 
-  auto run = [&](auto B, int u) __device__ {
-    const int s = sSlot[u];
+  // work item w = (b, h, c): geometry helpers
+  auto row_of = [&](int64_t w, int64_t& row_off, bool& exists, bool& owner, int64_t& b_h) __device__ {
+    const int64_t c = w % p.nQ, bh = w / p.nQ;
+    const int h = (int)(bh % p.H);
+    const int64_t b = bh / p.H;
+    const int hr = p.Hr == 1 ? 0 : h;
+    const int64_t t = p.causal ? c - 1 : 0;
+    exists = t >= 0;
+    row_off = ((b * p.Hr + hr) * p.nQ + (exists ? t : 0)) * K;
+    owner = p.Hr != 1 || h == 0;  // writes the row's weights
+    b_h = bh;
+  };
+  // wave 0: turn a row's metadata into the compacted slot list of buffer par
+  auto make_slots = [&](const RowMeta& m, int64_t w, int par) __device__ {
+    int64_t row_off, bh;
+    bool exists, owner;
+    row_of(w, row_off, exists, owner, bh);
+    const bool valid = lane < K && m.j >= 0 && m.j < p.nKV;
+    float mx = valid ? m.sv : -INFINITY;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    const float e = valid ? expf(m.sv - mx) : 0.f;
+    float sum = e;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+    const float wv = valid ? e / sum : 0.f;
+    const uint64_t mask = __ballot(valid);
+    if (lane < 32) {
+      sW[par][lane] = wv;
+      sJ[par][lane] = valid ? m.j : -1;
+    }
+    if (valid) sSlot[par][__popcll(mask & ((1ull << lane) - 1))] = lane;
+    if (lane == 0) sN[par] = __popcll(mask);
+    if (p.w && exists && owner && lane < K) p.w[row_off + lane] = wv;
+  };
+  auto qrow_ptr = [&](int64_t w) __device__ {
+    return reinterpret_cast<const T*>(p.q) + (w * kS + qi) * kD;
+  };
+
+  // ---- prologue: the first chunk's slot list and Q, the second chunk's metadata
+  Frag<T> qf[4], qn[4];
+  RowMeta meta{-1, -INFINITY};
+  {
+    int64_t ro, bh;
+    bool ex, ow;
+    row_of(c_begin, ro, ex, ow, bh);
+    const RowMeta m0 = load_row_meta(p, ro, ex);
+    const T* qr = qrow_ptr(c_begin);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qr + 16 * kb + 8 * hh);
+    if (wave == 0) make_slots(m0, c_begin, 0);
+    if (c_begin + 1 < c_end) {
+      row_of(c_begin + 1, ro, ex, ow, bh);
+      meta = load_row_meta(p, ro, ex);
+    }
+    wait_vmem<0>();
+    __syncthreads();
+  }
+
+  // the ring: global round counter picks the slot pair (rounds alternate slots 0,1 / 2,3)
+  int round = 0;
+  auto issue_item = [&](int64_t w, int par, int u, int slot) __device__ {
+    const int64_t kv0 = (w / p.nQ) * p.nKV * TILE;
+    const int64_t j = sJ[par][sSlot[par][u]];
+    T* dst = slot == 0 ? ring0 : slot == 1 ? ring1 : slot == 2 ? ring2 : ring3;
+    dma_tile<T, 4>(reinterpret_cast<const T*>(p.k) + kv0 + j * TILE, dst, wave, lane);
+    dma_tile<T, 4>(reinterpret_cast<const T*>(p.v) + kv0 + j * TILE, dst + TILE, wave, lane);
+  };
+  // copies of round 0 of the first chunk
+  if (sN[0] > 0) issue_item(c_begin, 0, 0, 0);
+  if (sN[0] > 1) issue_item(c_begin, 0, 1, 1);
+
+  auto compute = [&](auto B, int par, int u, f32x16& o0, f32x16& o1) __device__ {
+    const int s = sSlot[par][u];
     const T* sK = slot_buf(B);
     const T* sV = sK + TILE;
-    // S^T (keys x queries): rows 0-31 in st0, 32-63 in st1
     f32x16 st0 = zero16(), st1 = zero16();
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       mma32(st0, lds_frag(sK, lane & 31, 16 * kb + 8 * hh), qf[kb]);
       mma32(st1, lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh), qf[kb]);
     }
-    // softmax of this lane's query over the chunk's 64 keys (base-2 domain)
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(st0[i], st1[i]));
-    mx = fmaxf(mx, xor32(mx)) * sc;
+    mx = max_xor32(mx) * sc;
     if (OBO) mx = fmaxf(mx, 0.f);
     float sum = 0.f;
 #pragma unroll
@@ -151,11 +180,10 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
       st1[i] = __builtin_amdgcn_exp2f(fmaf(st1[i], sc, -mx));
       sum += st0[i] + st1[i];
     }
-    sum += xor32(sum);
+    sum = sum_xor32(sum);
     if (OBO) sum += __builtin_amdgcn_exp2f(-mx);
     if (hh == 0) sLse[s * kS + qi] = (mx + __builtin_amdgcn_logf(sum)) * kLn2;
-    // fuse w_s / l_s into P and accumulate O^T += V^T P^T
-    const float coef = sW[s] / sum;
+    const float coef = sW[par][s] * __builtin_amdgcn_rcpf(sum);
     Frag<T> pf[4];
     frag_from_acc(pf[0], st0, 0, coef);
     frag_from_acc(pf[1], st0, 1, coef);
@@ -167,38 +195,108 @@ __global__ __launch_bounds__(kThreads) void xattn_fwd_kernel(FwdParams p) {
       mma32(o1, lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), pf[kb]);
     }
   };
-  pair_ring(n, pair, issue, run);
 
-  // pair 1 hands its partial O^T to pair 0 through LDS (the ring is free now)
-  float* part = reinterpret_cast<float*>(ring0);  // [query][d] fp32, 16 KB
-  __syncthreads();
-  if (pair == 1) {
+  for (int64_t w = c_begin; w < c_end; ++w) {
+    const int par = (int)((w - c_begin) & 1);
+    const int n = sN[par];
+    const int R = n > 0 ? (n + 1) / 2 : 1;
+    const bool has_next = w + 1 < c_end;
+    f32x16 o0 = zero16(), o1 = zero16();
+    for (int r = 0; r < R; ++r) {
+      wait_vmem<0>();
+      block_barrier();
+      if (r == 0) {
+        if (w != c_begin) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      *reinterpret_cast<f32x4*>(part + qi * kD + 8 * g + 4 * hh) =
-          f32x4{o0[4 * g], o0[4 * g + 1], o0[4 * g + 2], o0[4 * g + 3]};
-      *reinterpret_cast<f32x4*>(part + qi * kD + 32 + 8 * g + 4 * hh) =
-          f32x4{o1[4 * g], o1[4 * g + 1], o1[4 * g + 2], o1[4 * g + 3]};
-    }
-  }
-  __syncthreads();
-  if (pair == 0) {
-    // O^T accumulator: lane holds query qi, d = 32*dt + 8*g + 4*hh + 0..3
-    T* orow = out + qi * kD;
+          for (int kb = 0; kb < 4; ++kb) qf[kb] = qn[kb];
+        }
+        if (has_next) {
+          const T* qr = qrow_ptr(w + 1);
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 a = *reinterpret_cast<const f32x4*>(part + qi * kD + 8 * g + 4 * hh);
-      const f32x4 bq = *reinterpret_cast<const f32x4*>(part + qi * kD + 32 + 8 * g + 4 * hh);
-      store4(orow + 8 * g + 4 * hh, o0[4 * g] + a[0], o0[4 * g + 1] + a[1], o0[4 * g + 2] + a[2],
-             o0[4 * g + 3] + a[3]);
-      store4(orow + 32 + 8 * g + 4 * hh, o1[4 * g] + bq[0], o1[4 * g + 1] + bq[1], o1[4 * g + 2] + bq[2],
-             o1[4 * g + 3] + bq[3]);
+          for (int kb = 0; kb < 4; ++kb) qn[kb] = load_frag(qr + 16 * kb + 8 * hh);
+          if (wave == 0) make_slots(meta, w + 1, par ^ 1);
+          if (w + 2 < c_end) {
+            int64_t ro, bh;
+            bool ex, ow;
+            row_of(w + 2, ro, ex, ow, bh);
+            meta = load_row_meta(p, ro, ex);
+          }
+        }
+        block_barrier();  // the next chunk's slot list is visible
+      }
+      const int cur = 2 * (round & 1), nxt = 2 - cur;
+      if (r + 1 < R) {
+        if (2 * r + 2 < n) issue_item(w, par, 2 * r + 2, nxt);
+        if (2 * r + 3 < n) issue_item(w, par, 2 * r + 3, nxt + 1);
+      } else if (has_next) {
+        const int nn = sN[par ^ 1];
+        if (nn > 0) issue_item(w + 1, par ^ 1, 0, nxt);
+        if (nn > 1) issue_item(w + 1, par ^ 1, 1, nxt + 1);
+      }
+      const int u = 2 * r + pair;
+      if (u < n) {
+        if (cur == 0) {
+          if (pair == 0) compute(ic<0>{}, par, u, o0, o1);
+          else compute(ic<1>{}, par, u, o0, o1);
+        } else {
+          if (pair == 0) compute(ic<2>{}, par, u, o0, o1);
+          else compute(ic<3>{}, par, u, o0, o1);
+        }
+      }
+      ++round;
     }
-  }
-  if (lse) {
-    for (int e = tid; e < kS * K; e += kThreads) {
-      const int q = e / K, s = e % K;
-      lse[e] = sJ[s] >= 0 ? sLse[s * kS + q] : -INFINITY;
+
+    // ---- finish chunk w: pair 1 hands its partial O^T to pair 0 through this
+    // round's ring slot, which no copy targets until the next round's barrier
+    const int64_t tok0 = w * kS;
+    T* out = reinterpret_cast<T*>(p.out) + tok0 * kD;
+    float* part = reinterpret_cast<float*>(((round - 1) & 1) == 0 ? ring1 : ring3);
+    block_barrier();
+    if (pair == 1 && n > 1) {
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        *reinterpret_cast<f32x4*>(part + ((half * 4 + gq) * 2 + 0) * 256 + lane * 4) =
+            f32x4{o0[4 * gq], o0[4 * gq + 1], o0[4 * gq + 2], o0[4 * gq + 3]};
+        *reinterpret_cast<f32x4*>(part + ((half * 4 + gq) * 2 + 1) * 256 + lane * 4) =
+            f32x4{o1[4 * gq], o1[4 * gq + 1], o1[4 * gq + 2], o1[4 * gq + 3]};
+      }
+    }
+    block_barrier();
+    if (pair == 0) {
+      T* orow = out + qi * kD;
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        f32x4 a{0.f, 0.f, 0.f, 0.f}, bq{0.f, 0.f, 0.f, 0.f};
+        if (n > 1) {
+          a = *reinterpret_cast<const f32x4*>(part + ((half * 4 + gq) * 2 + 0) * 256 + lane * 4);
+          bq = *reinterpret_cast<const f32x4*>(part + ((half * 4 + gq) * 2 + 1) * 256 + lane * 4);
+        }
+        store4(orow + 8 * gq + 4 * hh, o0[4 * gq] + a[0], o0[4 * gq + 1] + a[1], o0[4 * gq + 2] + a[2],
+               o0[4 * gq + 3] + a[3]);
+        store4(orow + 32 + 8 * gq + 4 * hh, o1[4 * gq] + bq[0], o1[4 * gq + 1] + bq[1], o1[4 * gq + 2] + bq[2],
+               o1[4 * gq + 3] + bq[3]);
+      }
+    }
+    if (p.lse) {
+      float* lse = p.lse + tok0 * K;
+      for (int e = tid; e < kS * K; e += kThreads) {
+        const int q = e / K, s = e % K;
+        lse[e] = sJ[par][s] >= 0 ? sLse[s * kS + q] : -INFINITY;
+      }
+    }
+    // the causal last row feeds no chunk: its weights go out with chunk 0
+    if (p.w && p.causal && (w % p.nQ) == 0 && wave == 1) {
+      int64_t ro, bh;
+      bool ex, ow;
+      row_of(w, ro, ex, ow, bh);
+      if (ow) {
+        const int64_t last_off = ((bh / p.H) * p.Hr + (p.Hr == 1 ? 0 : (int)(bh % p.H))) * p.nQ * K +
+                                 (p.nQ - 1) * K;
+        float wv;
+        int jv;
+        wave_row_weight(p.idx, p.sel, last_off, K, p.nKV, wv, jv);
+        if (lane < K) p.w[last_off + lane] = wv;
+      }
     }
   }
 }
@@ -216,7 +314,10 @@ hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const 
   p.nwork = (int64_t)s.B * s.H * s.nQ;
   p.causal = s.causal;
   p.attn_scale = s.attn_scale;
-  const dim3 grid((unsigned)round8(p.nwork)), block(kThreads);
+  // persistent workgroups: two per CU (256 CUs), each taking a contiguous run of chunks
+  const int64_t target = 512;
+  p.per = (p.nwork + target - 1) / target;
+  const dim3 grid((unsigned)round8((p.nwork + p.per - 1) / p.per)), block(kThreads);
   if (s.bf16) {
     if (s.off_by_one) {
       hipLaunchKernelGGL((xattn_fwd_kernel<__bf16, true>), grid, block, 0, stream, p);
