@@ -128,6 +128,21 @@ def valid_units(idx_host, w):
     return int(per_row) * heads_per_rhead
 
 
+def measured_traffic(kernel):
+    """HBM bytes per launch (fetch + write) for `kernel` from the committed rocprofv3
+    counter summary, or None when there is none or the kernels changed since."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        from paper_2410_01651_amd.profiling import source_hash
+        data = json.load(open(path))
+        if data.get("source_sha256") != source_hash():
+            return None
+        k = data["kernels"][kernel]
+        return k["fetch_bytes_per_launch"] + k["write_bytes_per_launch"]
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def flops_per_unit():
     # per valid (query token, slot, head): one S x d product is 2*S*d flops
     return {"xattn_fwd_kernel": 2 * (2 * S * DH),     # S = QK^T and PV
@@ -196,7 +211,7 @@ def bench_train(args, dev, gca):
     if dom in fpu:
         ach = kern[dom]["tflops"]
         roof = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": ach / BF16_PEAK_TFLOPS, "traffic": None,
+                "frac": ach / BF16_PEAK_TFLOPS, "traffic": measured_traffic(dom),
                 "algorithmic_flops_per_launch": units * S * fpu[dom], "avg_launch_ms": kern[dom]["avg_ms"]}
     else:
         roof = {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
@@ -300,7 +315,8 @@ def bench_decode(args, dev, gca):
         "config": {"workload": "decode_16m_bf16: B=1 H=8 d=64, 16,777,216 past tokens (262,144 chunks), "
                                "S=64, top-8, D=512, bf16"},
         "roofline": {"kernel": "decode_scan_kernel", "bound": "hbm", "achieved": scan_gbs, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": scan_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": scan_gbs / HBM_PEAK_GBS,
+                     "traffic": measured_traffic("decode_scan_kernel"),
                      "algorithmic_bytes_per_launch": key_bytes, "avg_launch_ms": scan_ms},
         "kernels": kern,
     }
@@ -314,6 +330,9 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="first run one plain device copy of this many MiB (a known-size reference for "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     ap.add_argument("--only", choices=["train", "decode"], default=None,
                     help="run one leg only (for profiling); the JSON line then carries that leg")
     args = ap.parse_args()
@@ -332,6 +351,13 @@ def main():
         _b.build()
     from paper_2410_01651_amd import gca
     dev = torch.device("cuda:0")
+    if args.copy_calibration_mb:
+        n = args.copy_calibration_mb << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     if args.only == "decode":
         print(json.dumps({"decode_scan": bench_decode(args, dev, gca)}), flush=True)

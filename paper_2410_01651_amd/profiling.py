@@ -1,0 +1,116 @@
+"""Summaries of rocprofv3 output for the profiles/ folder.
+
+    python -m paper_2410_01651_amd.profiling stats   --csv DIR/run_kernel_stats.csv --cmd "..." --out profiles/X.md
+    python -m paper_2410_01651_amd.profiling traffic --fetch DIR1/run_counter_collection.csv \
+        --write DIR2/run_counter_collection.csv --copy-bytes N --cmd "..." --out profiles/hbm_traffic.json
+
+`traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
+launch for every GCA kernel, scaled by what the same counters read for a plain
+device copy of N bytes in the same run (the copy kernel is the dispatch whose
+name contains "copy").  The result records a hash of the kernel sources, so a
+reader (bench.py) can tell when the kernels have changed since the counters
+were taken.
+"""
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import statistics
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(HERE, "csrc")
+
+
+def source_hash() -> str:
+    """sha256 over the kernel sources (file names and contents, sorted)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".hpp", ".cpp")):
+            h.update(name.encode())
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def short_name(kernel: str) -> str:
+    for key in ("xattn_fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel", "chunk_scores_kernel", "topk_kernel",
+                "fused_select_kernel", "decode_scan_kernel", "decode_merge_kernel", "weights_kernel",
+                "fill_zero_kernel", "csr_count_kernel", "csr_scan_kernel", "csr_fill_kernel", "csr_sort_kernel",
+                "dsel_kernel", "dlmk_q_kernel", "dlmk_k_kernel"):
+        if key in kernel:
+            return key
+    if "copy" in kernel.lower():
+        return "copy"
+    return kernel[:60]
+
+
+def stats_md(stats_csv: str, cmd: str) -> str:
+    rows = list(csv.DictReader(open(stats_csv)))
+    out = ["# rocprofv3 kernel statistics", "", "Command:", "", "```", cmd, "```", "",
+           "| kernel | calls | total (us) | average (us) | min (us) | max (us) | % |",
+           "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        name = short_name(r["Name"])
+        ns = lambda k: float(r[k]) / 1000.0
+        out.append(f"| {name} | {r['Calls']} | {ns('TotalDurationNs'):.1f} | {ns('AverageNs'):.2f} | "
+                   f"{ns('MinNs'):.2f} | {ns('MaxNs'):.2f} | {float(r['Percentage']):.2f} |")
+    return "\n".join(out) + "\n"
+
+
+def _per_kernel(counter_csv: str, counter: str):
+    vals = {}
+    for r in csv.DictReader(open(counter_csv)):
+        if r["Counter_Name"] != counter:
+            continue
+        vals.setdefault(short_name(r["Kernel_Name"]), []).append(float(r["Counter_Value"]))
+    return vals
+
+
+def traffic(fetch_csv: str, write_csv: str, copy_bytes: int, cmd: str) -> dict:
+    f = _per_kernel(fetch_csv, "FETCH_SIZE")
+    w = _per_kernel(write_csv, "WRITE_SIZE")
+    if "copy" not in f or "copy" not in w:
+        raise SystemExit("no copy kernel in the counter output (run bench.py with --copy-calibration-mb)")
+    # the calibration copy reads and writes copy_bytes each
+    f_scale = copy_bytes / (max(f["copy"]) * 1024.0)
+    w_scale = copy_bytes / (max(w["copy"]) * 1024.0)
+    kernels = {}
+    for k in sorted(set(f) & set(w)):
+        if k == "copy":
+            continue
+        kernels[k] = {
+            "fetch_bytes_per_launch": statistics.median(f[k]) * 1024.0 * f_scale,
+            "write_bytes_per_launch": statistics.median(w[k]) * 1024.0 * w_scale,
+            "dispatches": len(f[k]),
+        }
+    return {"source_sha256": source_hash(), "copy_bytes": copy_bytes,
+            "fetch_scale": f_scale, "write_scale": w_scale, "command": cmd, "kernels": kernels}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="what", required=True)
+    a = sub.add_parser("stats")
+    a.add_argument("--csv", required=True)
+    a.add_argument("--cmd", required=True)
+    a.add_argument("--out", required=True)
+    b = sub.add_parser("traffic")
+    b.add_argument("--fetch", required=True)
+    b.add_argument("--write", required=True)
+    b.add_argument("--copy-bytes", type=int, required=True)
+    b.add_argument("--cmd", required=True)
+    b.add_argument("--out", required=True)
+    args = ap.parse_args()
+    if args.what == "stats":
+        text = stats_md(args.csv, args.cmd)
+        open(args.out, "w").write(text)
+    else:
+        data = traffic(args.fetch, args.write, args.copy_bytes, args.cmd)
+        json.dump(data, open(args.out, "w"), indent=1)
+    print(args.out)
+
+
+if __name__ == "__main__":
+    main()
