@@ -59,6 +59,25 @@ def stats_md(stats_csv: str, cmd: str) -> str:
     return "\n".join(out) + "\n"
 
 
+def trace_md(trace_csv: str, cmd: str) -> str:
+    """Per (kernel, grid size) duration statistics from a rocprofv3 kernel trace, so
+    launches of one kernel on different workloads are reported apart."""
+    groups = {}
+    for r in csv.DictReader(open(trace_csv)):
+        grid = r.get("Grid_Size") or r.get("Grid_Size_X") or "?"
+        dur = (float(r["End_Timestamp"]) - float(r["Start_Timestamp"])) / 1000.0
+        groups.setdefault((short_name(r["Kernel_Name"]), grid), []).append(dur)
+    total = sum(sum(v) for v in groups.values())
+    out = ["# rocprofv3 kernel trace, per kernel and grid size", "", "Command:", "", "```", cmd, "```", "",
+           "| kernel | grid (work-items) | calls | average (us) | median (us) | min (us) | max (us) | % of GPU time |",
+           "|---|---|---|---|---|---|---|---|"]
+    for (name, grid), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        v = sorted(v)
+        out.append(f"| {name} | {grid} | {len(v)} | {sum(v) / len(v):.2f} | {v[len(v) // 2]:.2f} | {v[0]:.2f} | "
+                   f"{v[-1]:.2f} | {100 * sum(v) / total:.2f} |")
+    return "\n".join(out) + "\n"
+
+
 def _per_kernel(counter_csv: str, counter: str):
     vals = {}
     for r in csv.DictReader(open(counter_csv)):
@@ -93,7 +112,8 @@ def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="what", required=True)
     a = sub.add_parser("stats")
-    a.add_argument("--csv", required=True)
+    a.add_argument("--csv", required=True, help="run_kernel_stats.csv; a run_kernel_trace.csv beside it adds a "
+                                                "per-grid table")
     a.add_argument("--cmd", required=True)
     a.add_argument("--out", required=True)
     b = sub.add_parser("traffic")
@@ -105,6 +125,10 @@ def main():
     args = ap.parse_args()
     if args.what == "stats":
         text = stats_md(args.csv, args.cmd)
+        trace = os.path.join(os.path.dirname(args.csv), os.path.basename(args.csv).replace("kernel_stats",
+                                                                                         "kernel_trace"))
+        if os.path.exists(trace):
+            text += "\n" + trace_md(trace, args.cmd)
         open(args.out, "w").write(text)
     else:
         data = traffic(args.fetch, args.write, args.copy_bytes, args.cmd)
