@@ -68,7 +68,7 @@ __device__ __forceinline__ RowMeta load_row_meta(const FwdParams& p, int64_t row
 template <typename T, bool OBO>
 __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   constexpr int TILE = kS * kD;
-  GCA_RING4(T, 2 * TILE)           // each slot: one retrieved chunk's K and V tiles
+  __shared__ __attribute__((aligned(16))) T ring[4 * 2 * TILE];  // 4 slots: a chunk's K and V tiles
   __shared__ float sLse[32 * kS];  // current chunk: [slot][query]
   __shared__ float sW[2][32];      // slot lists of the current and the next chunk
   __shared__ int sJ[2][32];
@@ -150,7 +150,7 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   auto issue_item = [&](int64_t w, int par, int u, int slot) __device__ {
     const int64_t kv0 = (w / p.nQ) * p.nKV * TILE;
     const int64_t j = sJ[par][sSlot[par][u]];
-    T* dst = slot == 0 ? ring0 : slot == 1 ? ring1 : slot == 2 ? ring2 : ring3;
+    T* dst = ring + slot * (2 * TILE);
     dma_tile<T, 4>(reinterpret_cast<const T*>(p.k) + kv0 + j * TILE, dst, wave, lane);
     dma_tile<T, 4>(reinterpret_cast<const T*>(p.v) + kv0 + j * TILE, dst + TILE, wave, lane);
   };
@@ -158,15 +158,28 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   if (sN[0] > 0) issue_item(c_begin, 0, 0, 0);
   if (sN[0] > 1) issue_item(c_begin, 0, 1, 1);
 
-  auto compute = [&](auto B, int par, int u, f32x16& o0, f32x16& o1) __device__ {
+  auto compute = [&](const T* sK, int par, int u, f32x16& o0, f32x16& o1) __device__ {
     const int s = sSlot[par][u];
-    const T* sK = slot_buf(B);
     const T* sV = sK + TILE;
+    // all K fragments first, so the eight products issue back to back
+    Frag<T> ka[8];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      ka[2 * kb] = lds_frag(sK, lane & 31, 16 * kb + 8 * hh);
+      ka[2 * kb + 1] = lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh);
+    }
     f32x16 st0 = zero16(), st1 = zero16();
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      mma32(st0, lds_frag(sK, lane & 31, 16 * kb + 8 * hh), qf[kb]);
-      mma32(st1, lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh), qf[kb]);
+      mma32(st0, ka[2 * kb], qf[kb]);
+      mma32(st1, ka[2 * kb + 1], qf[kb]);
+    }
+    // V^T fragments are read while the softmax runs
+    Frag<T> va[8];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      va[2 * kb] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
+      va[2 * kb + 1] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
     }
     float mx = -INFINITY;
 #pragma unroll
@@ -191,8 +204,8 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     frag_from_acc(pf[3], st1, 1, coef);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      mma32(o0, lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), pf[kb]);
-      mma32(o1, lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), pf[kb]);
+      mma32(o0, va[2 * kb], pf[kb]);
+      mma32(o1, va[2 * kb + 1], pf[kb]);
     }
   };
 
@@ -234,15 +247,7 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
         if (nn > 1) issue_item(w + 1, par ^ 1, 1, nxt + 1);
       }
       const int u = 2 * r + pair;
-      if (u < n) {
-        if (cur == 0) {
-          if (pair == 0) compute(ic<0>{}, par, u, o0, o1);
-          else compute(ic<1>{}, par, u, o0, o1);
-        } else {
-          if (pair == 0) compute(ic<2>{}, par, u, o0, o1);
-          else compute(ic<3>{}, par, u, o0, o1);
-        }
-      }
+      if (u < n) compute(ring + (cur + pair) * (2 * TILE), par, u, o0, o1);
       ++round;
     }
 
@@ -250,7 +255,7 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     // round's ring slot, which no copy targets until the next round's barrier
     const int64_t tok0 = w * kS;
     T* out = reinterpret_cast<T*>(p.out) + tok0 * kD;
-    float* part = reinterpret_cast<float*>(((round - 1) & 1) == 0 ? ring1 : ring3);
+    float* part = reinterpret_cast<float*>(ring + (((round - 1) & 1) == 0 ? 1 : 3) * (2 * TILE));
     block_barrier();
     if (pair == 1 && n > 1) {
 #pragma unroll
