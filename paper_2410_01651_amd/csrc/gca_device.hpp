@@ -264,6 +264,44 @@ __device__ __forceinline__ void dma_tile(const T* __restrict__ g, T* lds, int wa
   }
 }
 
+// The same tile copy with this lane's global byte offsets computed once.  A copy
+// then takes the tile's global base in scalar registers and a 32-bit lane offset
+// (the scalar-base form of the instruction), so issuing a tile costs one scalar
+// move and one vector-memory instruction per 16-byte chunk and no vector address
+// arithmetic.  `g` and `lds` must hold the same value in every lane.
+template <typename T, int NW>
+struct TileCopy {
+  static constexpr int kVec = Swz<T>::kVec, kCPR = Swz<T>::kCPR, kN = kCPR / NW;
+  uint32_t goff[kN];
+  uint32_t lwave;  // this wave's first 1 KiB block of the tile in LDS
+
+  __device__ __forceinline__ TileCopy(int wave, int lane) {
+#pragma unroll
+    for (int ii = 0; ii < kN; ++ii) {
+      const int pch = (ii * NW + wave) * 64 + lane;
+      const int r = pch / kCPR;
+      const int c = (pch % kCPR) ^ (r & (kCPR - 1));
+      goff[ii] = (uint32_t)((r * kD + c * kVec) * sizeof(T));
+    }
+    lwave = (uint32_t)(wave * 64 * 16);
+  }
+  __device__ __forceinline__ void issue(const T* g, const T* lds) const {
+    const uint64_t ga = (uint64_t)(uintptr_t)g;
+    // (the builtin returns a signed int: widen through uint32_t, never sign-extend)
+    const uint64_t gs = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)ga) |
+                        ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(ga >> 32)) << 32);
+    // wave-uniform, but the wave index comes from the thread index: read it back
+    // from lane 0 so that it lives in a scalar register
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)lds) + lwave);
+#pragma unroll
+    for (int ii = 0; ii < kN; ++ii)
+      asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(goff[ii]), "s"(gs),
+                   "s"(lb + ii * NW * 64 * 16)
+                   : "m0");
+  }
+};
+
 // Copy 64 floats spaced `stride` apart into 64 consecutive LDS floats (one wave).
 __device__ __forceinline__ void dma_column(const float* __restrict__ g, int64_t stride, float* lds, int lane) {
   dma_copy<4>(g + lane * stride, lds);

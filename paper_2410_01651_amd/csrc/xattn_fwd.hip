@@ -55,6 +55,28 @@ struct RowMeta {
   float sv;
 };
 
+// Position (b, h, c) of work item w = (b * H + h) * nQ + c, stepped one chunk at a
+// time so the persistent loop needs no divisions.
+struct Geo {
+  int64_t b, c;
+  int h;
+  __device__ __forceinline__ Geo(int64_t w, int64_t nQ, int H) {
+    c = w % nQ;
+    const int64_t bh = w / nQ;
+    h = (int)(bh % H);
+    b = bh / H;
+  }
+  __device__ __forceinline__ void next(int64_t nQ, int H) {
+    if (++c == nQ) {
+      c = 0;
+      if (++h == H) {
+        h = 0;
+        ++b;
+      }
+    }
+  }
+};
+
 __device__ __forceinline__ RowMeta load_row_meta(const FwdParams& p, int64_t row_off, bool exists) {
   const int lane = threadIdx.x & 63;
   RowMeta m{-1, -INFINITY};
@@ -70,9 +92,10 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   constexpr int TILE = kS * kD;
   __shared__ __attribute__((aligned(16))) T ring[4 * 2 * TILE];  // 4 slots: a chunk's K and V tiles
   __shared__ float sLse[32 * kS];  // current chunk: [slot][query]
-  __shared__ float sW[2][32];      // slot lists of the current and the next chunk
-  __shared__ int sJ[2][32];
-  __shared__ int sSlot[2][32];
+  __shared__ int sJ[2][32];        // per slot: chunk index or -1 (current and next chunk)
+  __shared__ int sSlot[2][32];     // compacted lists of valid slots: slot, chunk, weight
+  __shared__ int sJc[2][32];
+  __shared__ float sWc[2][32];
   __shared__ int sN[2];
 
   const int64_t g = xcd_swizzle(blockIdx.x, gridDim.x);
@@ -87,22 +110,18 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   const int cb = 16 * ((lane >> 4) & 1);
 
   // work item w = (b, h, c): geometry helpers
-  auto row_of = [&](int64_t w, int64_t& row_off, bool& exists, bool& owner, int64_t& b_h) __device__ {
-    const int64_t c = w % p.nQ, bh = w / p.nQ;
-    const int h = (int)(bh % p.H);
-    const int64_t b = bh / p.H;
-    const int hr = p.Hr == 1 ? 0 : h;
-    const int64_t t = p.causal ? c - 1 : 0;
+  auto row_of = [&](const Geo& g, int64_t& row_off, bool& exists, bool& owner) __device__ {
+    const int hr = p.Hr == 1 ? 0 : g.h;
+    const int64_t t = p.causal ? g.c - 1 : 0;
     exists = t >= 0;
-    row_off = ((b * p.Hr + hr) * p.nQ + (exists ? t : 0)) * K;
-    owner = p.Hr != 1 || h == 0;  // writes the row's weights
-    b_h = bh;
+    row_off = ((g.b * p.Hr + hr) * p.nQ + (exists ? t : 0)) * K;
+    owner = p.Hr != 1 || g.h == 0;  // writes the row's weights
   };
   // wave 0: turn a row's metadata into the compacted slot list of buffer par
-  auto make_slots = [&](const RowMeta& m, int64_t w, int par) __device__ {
-    int64_t row_off, bh;
+  auto make_slots = [&](const RowMeta& m, const Geo& g, int par) __device__ {
+    int64_t row_off;
     bool exists, owner;
-    row_of(w, row_off, exists, owner, bh);
+    row_of(g, row_off, exists, owner);
     const bool valid = lane < K && m.j >= 0 && m.j < p.nKV;
     float mx = valid ? m.sv : -INFINITY;
 #pragma unroll
@@ -113,11 +132,13 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
     const float wv = valid ? e / sum : 0.f;
     const uint64_t mask = __ballot(valid);
-    if (lane < 32) {
-      sW[par][lane] = wv;
-      sJ[par][lane] = valid ? m.j : -1;
+    if (lane < 32) sJ[par][lane] = valid ? m.j : -1;
+    if (valid) {
+      const int rk = __popcll(mask & ((1ull << lane) - 1));
+      sSlot[par][rk] = lane;
+      sJc[par][rk] = m.j;
+      sWc[par][rk] = wv;
     }
-    if (valid) sSlot[par][__popcll(mask & ((1ull << lane) - 1))] = lane;
     if (lane == 0) sN[par] = __popcll(mask);
     if (p.w && exists && owner && lane < K) p.w[row_off + lane] = wv;
   };
@@ -128,17 +149,22 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   // ---- prologue: the first chunk's slot list and Q, the second chunk's metadata
   Frag<T> qf[4], qn[4];
   RowMeta meta{-1, -INFINITY};
+  Geo g0(c_begin, p.nQ, p.H);  // geometry of the current chunk and of the two after it
+  Geo g1 = g0;
+  g1.next(p.nQ, p.H);
+  Geo g2 = g1;
+  g2.next(p.nQ, p.H);
   {
-    int64_t ro, bh;
+    int64_t ro;
     bool ex, ow;
-    row_of(c_begin, ro, ex, ow, bh);
+    row_of(g0, ro, ex, ow);
     const RowMeta m0 = load_row_meta(p, ro, ex);
     const T* qr = qrow_ptr(c_begin);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qr + 16 * kb + 8 * hh);
-    if (wave == 0) make_slots(m0, c_begin, 0);
+    if (wave == 0) make_slots(m0, g0, 0);
     if (c_begin + 1 < c_end) {
-      row_of(c_begin + 1, ro, ex, ow, bh);
+      row_of(g1, ro, ex, ow);
       meta = load_row_meta(p, ro, ex);
     }
     wait_vmem<0>();
@@ -147,19 +173,28 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
 
   // the ring: global round counter picks the slot pair (rounds alternate slots 0,1 / 2,3)
   int round = 0;
-  auto issue_item = [&](int64_t w, int par, int u, int slot) __device__ {
-    const int64_t kv0 = (w / p.nQ) * p.nKV * TILE;
-    const int64_t j = sJ[par][sSlot[par][u]];
+  const TileCopy<T, 4> cp(wave, lane);
+  const T* const gk = reinterpret_cast<const T*>(p.k);
+  const T* const gv = reinterpret_cast<const T*>(p.v);
+  // element offset of the (batch, head) key/value slice of chunk w
+  auto slice_of = [&](const Geo& g) __device__ { return (g.b * p.H + g.h) * p.nKV * TILE; };
+  auto issue_item = [&](int64_t kvb, int j, int slot) __device__ {
     T* dst = ring + slot * (2 * TILE);
-    dma_tile<T, 4>(reinterpret_cast<const T*>(p.k) + kv0 + j * TILE, dst, wave, lane);
-    dma_tile<T, 4>(reinterpret_cast<const T*>(p.v) + kv0 + j * TILE, dst + TILE, wave, lane);
+    cp.issue(gk + kvb + (int64_t)j * TILE, dst);
+    cp.issue(gv + kvb + (int64_t)j * TILE, dst + TILE);
   };
+  // lane u < 32 of each list holds valid item u of the current chunk (slot, chunk,
+  // weight) or of the next chunk (chunk); items are picked with a lane read
+  const int l32 = lane & 31;
+  int ls = sSlot[0][l32], lj = sJc[0][l32], ljn = 0;
+  float lw = sWc[0][l32];
+  int64_t kvb = slice_of(g0), kvb_n = 0;
   // copies of round 0 of the first chunk
-  if (sN[0] > 0) issue_item(c_begin, 0, 0, 0);
-  if (sN[0] > 1) issue_item(c_begin, 0, 1, 1);
+  if (sN[0] > 0) issue_item(kvb, __builtin_amdgcn_readlane(lj, 0), 0);
+  if (sN[0] > 1) issue_item(kvb, __builtin_amdgcn_readlane(lj, 1), 1);
 
-  auto compute = [&](const T* sK, int par, int u, f32x16& o0, f32x16& o1) __device__ {
-    const int s = sSlot[par][u];
+  auto compute = [&](const T* sK, int u, f32x16& o0, f32x16& o1) __device__ {
+    const int s = __builtin_amdgcn_readlane(ls, u);
     const T* sV = sK + TILE;
     // all K fragments first, so the eight products issue back to back
     Frag<T> ka[8];
@@ -196,7 +231,8 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     sum = sum_xor32(sum);
     if (OBO) sum += __builtin_amdgcn_exp2f(-mx);
     if (hh == 0) sLse[s * kS + qi] = (mx + __builtin_amdgcn_logf(sum)) * kLn2;
-    const float coef = sW[par][s] * __builtin_amdgcn_rcpf(sum);
+    const int coef_bits = __builtin_amdgcn_readlane(__float_as_int(lw), u);
+    const float coef = __int_as_float(coef_bits) * __builtin_amdgcn_rcpf(sum);
     Frag<T> pf[4];
     frag_from_acc(pf[0], st0, 0, coef);
     frag_from_acc(pf[1], st0, 1, coef);
@@ -222,32 +258,40 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
         if (w != c_begin) {
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb) qf[kb] = qn[kb];
+          ls = sSlot[par][l32];
+          lj = sJc[par][l32];
+          lw = sWc[par][l32];
+          kvb = kvb_n;
         }
         if (has_next) {
           const T* qr = qrow_ptr(w + 1);
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb) qn[kb] = load_frag(qr + 16 * kb + 8 * hh);
-          if (wave == 0) make_slots(meta, w + 1, par ^ 1);
+          if (wave == 0) make_slots(meta, g1, par ^ 1);
           if (w + 2 < c_end) {
-            int64_t ro, bh;
+            int64_t ro;
             bool ex, ow;
-            row_of(w + 2, ro, ex, ow, bh);
+            row_of(g2, ro, ex, ow);
             meta = load_row_meta(p, ro, ex);
           }
         }
         block_barrier();  // the next chunk's slot list is visible
+        if (has_next) {
+          ljn = sJc[par ^ 1][l32];
+          kvb_n = slice_of(g1);
+        }
       }
       const int cur = 2 * (round & 1), nxt = 2 - cur;
       if (r + 1 < R) {
-        if (2 * r + 2 < n) issue_item(w, par, 2 * r + 2, nxt);
-        if (2 * r + 3 < n) issue_item(w, par, 2 * r + 3, nxt + 1);
+        if (2 * r + 2 < n) issue_item(kvb, __builtin_amdgcn_readlane(lj, 2 * r + 2), nxt);
+        if (2 * r + 3 < n) issue_item(kvb, __builtin_amdgcn_readlane(lj, 2 * r + 3), nxt + 1);
       } else if (has_next) {
         const int nn = sN[par ^ 1];
-        if (nn > 0) issue_item(w + 1, par ^ 1, 0, nxt);
-        if (nn > 1) issue_item(w + 1, par ^ 1, 1, nxt + 1);
+        if (nn > 0) issue_item(kvb_n, __builtin_amdgcn_readlane(ljn, 0), nxt);
+        if (nn > 1) issue_item(kvb_n, __builtin_amdgcn_readlane(ljn, 1), nxt + 1);
       }
       const int u = 2 * r + pair;
-      if (u < n) compute(ring + (cur + pair) * (2 * TILE), par, u, o0, o1);
+      if (u < n) compute(ring + (cur + pair) * (2 * TILE), u, o0, o1);
       ++round;
     }
 
@@ -283,26 +327,25 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
       }
     }
     if (p.lse) {
-      float* lse = p.lse + tok0 * K;
-      for (int e = tid; e < kS * K; e += kThreads) {
-        const int q = e / K, s = e % K;
-        lse[e] = sJ[par][s] >= 0 ? sLse[s * kS + q] : -INFINITY;
-      }
+      float* lse = p.lse + (tok0 + lane) * K;
+      for (int s = wave; s < K; s += 4) lse[s] = sJ[par][s] >= 0 ? sLse[s * kS + lane] : -INFINITY;
     }
     // the causal last row feeds no chunk: its weights go out with chunk 0
-    if (p.w && p.causal && (w % p.nQ) == 0 && wave == 1) {
-      int64_t ro, bh;
+    if (p.w && p.causal && g0.c == 0 && wave == 1) {
+      int64_t ro;
       bool ex, ow;
-      row_of(w, ro, ex, ow, bh);
+      row_of(g0, ro, ex, ow);
       if (ow) {
-        const int64_t last_off = ((bh / p.H) * p.Hr + (p.Hr == 1 ? 0 : (int)(bh % p.H))) * p.nQ * K +
-                                 (p.nQ - 1) * K;
+        const int64_t last_off = (g0.b * p.Hr + (p.Hr == 1 ? 0 : g0.h)) * p.nQ * K + (p.nQ - 1) * K;
         float wv;
         int jv;
         wave_row_weight(p.idx, p.sel, last_off, K, p.nKV, wv, jv);
         if (lane < K) p.w[last_off + lane] = wv;
       }
     }
+    g0 = g1;
+    g1 = g2;
+    g2.next(p.nQ, p.H);
   }
 }
 
