@@ -146,6 +146,7 @@ gca_status gca_grouped_xattn_fwd(const gca_problem* p, const void* q, const void
  * lse must be the one written by gca_grouped_xattn_fwd for the same inputs.
  * The result is deterministic (no floating-point atomics).
  * Workspace: gca_workspace_size(p, GCA_OP_BACKWARD) bytes, 256-byte aligned.
+ * GCA_ERR_UNSUPPORTED when nQ * topk exceeds INT32_MAX or nQ >= 2^26.
  */
 gca_status gca_grouped_xattn_bwd(const gca_problem* p, const void* q, const void* k,
                                  const void* v, const int32_t* idx, const float* sel,

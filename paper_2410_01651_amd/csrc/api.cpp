@@ -220,6 +220,8 @@ gca_status gca_grouped_xattn_bwd(const gca_problem* p, const void* q, const void
   gca::Shape s;
   GCA_TRY(check_problem(p, s));
   if (s.nQ * (int64_t)s.topk > 0x7fffffff) return fail(GCA_ERR_UNSUPPORTED, "nQ * topk must fit in int32");
+  // the key-stationary pass packs (query chunk, slot) into one int
+  if (s.nQ >= (int64_t(1) << 26)) return fail(GCA_ERR_UNSUPPORTED, "the backward takes fewer than 2^26 query chunks");
   GCA_TRY(check_ptr(q, "q", true, 16));
   GCA_TRY(check_ptr(k, "k", true, 16));
   GCA_TRY(check_ptr(v, "v", true, 16));

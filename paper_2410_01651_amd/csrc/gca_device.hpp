@@ -264,6 +264,19 @@ __device__ __forceinline__ void dma_tile(const T* __restrict__ g, T* lds, int wa
   }
 }
 
+// A wave-uniform global address in scalar registers (the read-back builtin returns
+// a signed int: each half is widened through uint32_t, never sign-extended).
+__device__ __forceinline__ uint64_t uniform_addr(const void* g) {
+  const uint64_t ga = (uint64_t)(uintptr_t)g;
+  return (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)ga) |
+         ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(ga >> 32)) << 32);
+}
+// A wave-uniform LDS byte address (plus a wave-uniform offset) in a scalar register.
+__device__ __forceinline__ uint32_t uniform_lds(const void* lds, uint32_t add = 0) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)lds) + add);
+}
+
 // The same tile copy with this lane's global byte offsets computed once.  A copy
 // then takes the tile's global base in scalar registers and a 32-bit lane offset
 // (the scalar-base form of the instruction), so issuing a tile costs one scalar
@@ -286,14 +299,10 @@ struct TileCopy {
     lwave = (uint32_t)(wave * 64 * 16);
   }
   __device__ __forceinline__ void issue(const T* g, const T* lds) const {
-    const uint64_t ga = (uint64_t)(uintptr_t)g;
-    // (the builtin returns a signed int: widen through uint32_t, never sign-extend)
-    const uint64_t gs = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)ga) |
-                        ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(ga >> 32)) << 32);
-    // wave-uniform, but the wave index comes from the thread index: read it back
-    // from lane 0 so that it lives in a scalar register
-    const uint32_t lb = __builtin_amdgcn_readfirstlane(
-        (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)lds) + lwave);
+    const uint64_t gs = uniform_addr(g);
+    // wave-uniform, but the wave index comes from the thread index: read back from
+    // lane 0 so that it lives in a scalar register
+    const uint32_t lb = uniform_lds(lds, lwave);
 #pragma unroll
     for (int ii = 0; ii < kN; ++ii)
       asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(goff[ii]), "s"(gs),
@@ -301,6 +310,14 @@ struct TileCopy {
                    : "m0");
   }
 };
+
+// One wave copies 64 floats at g + lane_off (bytes, lane_off = lane * stride
+// precomputed) into 64 consecutive LDS floats; g and lds wave-uniform.
+__device__ __forceinline__ void dma_column_s(const float* g, uint32_t lane_off, const float* lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dword %0, %1" ::"v"(lane_off), "s"(uniform_addr(g)),
+               "s"(uniform_lds(lds))
+               : "m0");
+}
 
 // Copy 64 floats spaced `stride` apart into 64 consecutive LDS floats (one wave).
 __device__ __forceinline__ void dma_column(const float* __restrict__ g, int64_t stride, float* lds, int lane) {

@@ -247,9 +247,13 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     if (lane == 0) sN = __popcll(mask);
   }
   if (t >= 0)
-    for (int e = tid; e < kS * K; e += kThreads) sL[(e % K) * kS + e / K] = p.lse[tok0 * K + e];
+    for (int s = wave; s < K; s += 4) sL[s * kS + lane] = p.lse[(tok0 + lane) * K + s];
   __syncthreads();
   const int n = sN;
+  // lane u < 32 holds valid item u's slot, chunk and weight (picked with a lane read)
+  const int ls = sSlot[lane & 31] & 31;
+  const int lj = sJ[ls];
+  const float lw = sW[ls];
 
   T* dq = reinterpret_cast<T*>(p.dq) + tok0 * kD;
   if (n == 0) {
@@ -276,14 +280,15 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
 
+  const TileCopy<T, 4> cp(wave, lane);
   auto issue = [&](auto B, int u) __device__ {
-    const int64_t j = sJ[sSlot[u]];
+    const int64_t j = __builtin_amdgcn_readlane(lj, u);
     T* dst = slot_buf(B);
-    dma_tile<T, 4>(kbase + j * TILE, dst, wave, lane);
-    dma_tile<T, 4>(vbase + j * TILE, dst + TILE, wave, lane);
+    cp.issue(kbase + j * TILE, dst);
+    cp.issue(vbase + j * TILE, dst + TILE);
   };
   auto run = [&](auto B, int u) __device__ {
-    const int s = sSlot[u];
+    const int s = __builtin_amdgcn_readlane(ls, u);
     const T* sK = slot_buf(B);
     const T* sV = sK + TILE;
     const float lse2 = sL[s * kS + qi] * kLog2e;
@@ -305,7 +310,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     }
     Dq = sum_xor32(Dq);
     if (hh == 0) sL[s * kS + qi] = Dq;  // this lane's pair alone reads the lse it replaces
-    const float ws = sW[s];
+    const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lw), u));
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       s0[i] = ws * s0[i] * (p0[i] - Dq);
@@ -361,11 +366,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     acc += __shfl_xor(acc, 4);
     if (s < K && part8 == 0) p.ws.dwp[(bh * p.nQ + t) * K + s] = acc;
   }
-  float* Dout = p.ws.Dbuf + tok0 * K;
-  for (int e = tid; e < kS * K; e += kThreads) {
-    const int q = e / K, s = e % K;
-    Dout[e] = sJ[s] >= 0 ? sL[s * kS + q] : 0.f;
-  }
+  float* Dout = p.ws.Dbuf + (tok0 + lane) * K;
+  for (int s = wave; s < K; s += 4) Dout[s] = sJ[s] >= 0 ? sL[s * kS + lane] : 0.f;
 }
 
 // ---------------------------------------------- key-stationary dK, dV ----
@@ -429,16 +431,18 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
   const float* Db = p.ws.Dbuf + bh * p.nQ * kS * K;
   const float* wrow = p.ws.w + bhr * p.nQ * K;
 
+  const TileCopy<T, 4> cp(wave, lane);
+  const uint32_t col_off = (uint32_t)(lane * K * sizeof(float));
   auto issue = [&](int slot, int u) __device__ {
-    const int e = sE[u];
-    const int64_t c = e / K + p.causal;
-    const int s = e % K;
+    const int cs = sE[u];  // (query chunk << 5) | slot
+    const int64_t c = cs >> 5;
+    const int s = cs & 31;
     T* dst = ring + slot * ENTRY;
-    dma_tile<T, 4>(qb + c * TILE, dst, wave, lane);
-    dma_tile<T, 4>(ob + c * TILE, dst + TILE, wave, lane);
+    cp.issue(qb + c * TILE, dst);
+    cp.issue(ob + c * TILE, dst + TILE);
     float* cols = reinterpret_cast<float*>(dst + 2 * TILE);
-    if (wave == 0) dma_column(lseb + c * kS * K + s, K, cols, lane);
-    else if (wave == 1) dma_column(Db + c * kS * K + s, K, cols + kS, lane);
+    if (wave == 0) dma_column_s(lseb + c * kS * K + s, col_off, cols);
+    else if (wave == 1) dma_column_s(Db + c * kS * K + s, col_off, cols + kS);
   };
 
   f32x16 dv0 = zero16(), dv1 = zero16(), dk0 = zero16(), dk1 = zero16();
@@ -521,8 +525,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
     const int nb = min(NE, n - b0);
     __syncthreads();
     for (int i = tid; i < nb; i += kThreads) {
-      const int e = list_g[b0 + i];
-      sE[i] = e;
+      const int e = list_g[b0 + i];  // t * K + s
+      sE[i] = ((e / K + p.causal) << 5) | (e % K);
       sWt[i] = wrow[e];
     }
     __syncthreads();
