@@ -193,9 +193,13 @@ struct Tile64 {
 // LDS with global_load_lds_dwordx4: each lane supplies a global address and the
 // 64 lanes of one instruction fill 1 KB of consecutive LDS.  The LDS copy is
 // XOR-swizzled at 16-byte granularity: LDS chunk c' of row r holds the row's
-// global chunk c' ^ (r mod chunks-per-row), so that reading one 16-byte chunk
-// per row from 32 consecutive rows, or the 8-byte transposed reads, spread over
-// the banks instead of hitting the same ones.
+// global chunk c' ^ (r mod chunks-per-row).  A bf16 row is 128 bytes, one pass
+// over the 32 LDS banks; a 16-byte read per row (A/B fragments) serves 8 lanes =
+// 8 consecutive rows per cycle, which this map spreads over all banks.  The
+// transposed 8-byte reads (16 lanes = 4 rows x 2 adjacent chunks per cycle) see
+// 2-way conflicts under it; a map that removes those too (f(r) = (2 (r mod 4) +
+// bit 2 of r) ^ (2 * bit 3 of r)) measured no faster, its address arithmetic
+// costing what the conflicts did, so the plain map stays.
 //
 // The copies are asynchronous: a wave's own copies are complete once its
 // vector-memory counter has dropped to the number issued after them
@@ -208,8 +212,9 @@ template <typename T>
 struct Swz {
   static constexpr int kVec = 16 / sizeof(T);  // elements per 16-byte chunk
   static constexpr int kCPR = kD / kVec;       // chunks per row (8 bf16, 16 fp32)
+  __device__ static __forceinline__ int sw(int r) { return r & (kCPR - 1); }
   __device__ static __forceinline__ int off(int r, int col) {
-    return r * kD + ((((col / kVec) ^ (r & (kCPR - 1)))) * kVec) + (col % kVec);
+    return r * kD + (((col / kVec) ^ sw(r)) * kVec) + (col % kVec);
   }
 };
 
@@ -259,7 +264,7 @@ __device__ __forceinline__ void dma_tile(const T* __restrict__ g, T* lds, int wa
     const int i = ii * NW + wave;
     const int pch = i * 64 + lane;
     const int r = pch / kCPR;
-    const int c = (pch % kCPR) ^ (r & (kCPR - 1));
+    const int c = (pch % kCPR) ^ Swz<T>::sw(r);
     dma_copy<16>(g + r * kD + c * kVec, lds + i * 64 * kVec);
   }
 }
@@ -293,7 +298,7 @@ struct TileCopy {
     for (int ii = 0; ii < kN; ++ii) {
       const int pch = (ii * NW + wave) * 64 + lane;
       const int r = pch / kCPR;
-      const int c = (pch % kCPR) ^ (r & (kCPR - 1));
+      const int c = (pch % kCPR) ^ Swz<T>::sw(r);
       goff[ii] = (uint32_t)((r * kD + c * kVec) * sizeof(T));
     }
     lwave = (uint32_t)(wave * 64 * 16);

@@ -329,16 +329,16 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
   };
   pair_ring(n, pair, issue, run);
 
-  // pair 1 hands its dQ^T partial to pair 0 through LDS
+  // pair 1 hands its dQ^T partial to pair 0 through LDS, laid out
+  // [half][register group][d half][lane] so that every access is lane-contiguous
   float* part = reinterpret_cast<float*>(ring0);
+  auto part_at = [&](int g, int dt) { return part + ((half * 4 + g) * 2 + dt) * 256 + lane * 4; };
   __syncthreads();
   if (pair == 1) {
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      *reinterpret_cast<f32x4*>(part + qi * kD + 8 * g + 4 * hh) =
-          f32x4{g0[4 * g], g0[4 * g + 1], g0[4 * g + 2], g0[4 * g + 3]};
-      *reinterpret_cast<f32x4*>(part + qi * kD + 32 + 8 * g + 4 * hh) =
-          f32x4{g1[4 * g], g1[4 * g + 1], g1[4 * g + 2], g1[4 * g + 3]};
+      *reinterpret_cast<f32x4*>(part_at(g, 0)) = f32x4{g0[4 * g], g0[4 * g + 1], g0[4 * g + 2], g0[4 * g + 3]};
+      *reinterpret_cast<f32x4*>(part_at(g, 1)) = f32x4{g1[4 * g], g1[4 * g + 1], g1[4 * g + 2], g1[4 * g + 3]};
     }
   }
   __syncthreads();
@@ -347,24 +347,21 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     T* drow = dq + qi * kD;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 x0 = *reinterpret_cast<const f32x4*>(part + qi * kD + 8 * g + 4 * hh);
-      const f32x4 x1 = *reinterpret_cast<const f32x4*>(part + qi * kD + 32 + 8 * g + 4 * hh);
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(part_at(g, 0));
+      const f32x4 x1 = *reinterpret_cast<const f32x4*>(part_at(g, 1));
       store4(drow + 8 * g + 4 * hh, as * (g0[4 * g] + x0[0]), as * (g0[4 * g + 1] + x0[1]),
              as * (g0[4 * g + 2] + x0[2]), as * (g0[4 * g + 3] + x0[3]));
       store4(drow + 32 + 8 * g + 4 * hh, as * (g1[4 * g] + x1[0]), as * (g1[4 * g + 1] + x1[1]),
              as * (g1[4 * g + 2] + x1[2]), as * (g1[4 * g + 3] + x1[3]));
     }
   }
-  // dw[t, s] = sum over the chunk's 64 queries of D_s (staged in sL): 8 threads per slot
-  {
-    const int s = tid >> 3, part8 = tid & 7;
-    float acc = 0.f;
-    if (s < K && sJ[s] >= 0)
-      for (int q = part8; q < kS; q += 8) acc += sL[s * kS + q];
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
-    acc += __shfl_xor(acc, 4);
-    if (s < K && part8 == 0) p.ws.dwp[(bh * p.nQ + t) * K + s] = acc;
+  // dw[t, s] = sum over the chunk's 64 queries of D_s (staged in sL): one wave per slot
+  for (int s = wave; s < K; s += 4) {
+    float acc = sJ[s] >= 0 ? sL[s * kS + lane] : 0.f;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) acc += __shfl_xor(acc, o);
+    acc = sum_xor32(acc);
+    if (lane == 0) p.ws.dwp[(bh * p.nQ + t) * K + s] = acc;
   }
   float* Dout = p.ws.Dbuf + (tok0 + lane) * K;
   for (int s = wave; s < K; s += 4) Dout[s] = sJ[s] >= 0 ? sL[s * kS + lane] : 0.f;

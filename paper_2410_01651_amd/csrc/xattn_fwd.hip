@@ -43,7 +43,6 @@ struct FwdParams {
   float* w;
   int H, Hr, topk;
   int64_t nQ, nKV, nwork;
-  int64_t per;  // chunks per workgroup
   int causal;
   float attn_scale;
 };
@@ -66,9 +65,10 @@ struct Geo {
     h = (int)(bh % H);
     b = bh / H;
   }
-  __device__ __forceinline__ void next(int64_t nQ, int H) {
-    if (++c == nQ) {
-      c = 0;
+  __device__ __forceinline__ void next(int64_t nQ, int H, int64_t step) {
+    c += step;
+    while (c >= nQ) {
+      c -= nQ;
       if (++h == H) {
         h = 0;
         ++b;
@@ -98,9 +98,17 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   __shared__ float sWc[2][32];
   __shared__ int sN[2];
 
-  const int64_t g = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int64_t c_begin = g * p.per;
-  const int64_t c_end = c_begin + p.per < p.nwork ? c_begin + p.per : p.nwork;
+  // Work order: workgroups are dealt to the eight XCDs round-robin (blockIdx mod
+  // 8).  XCD x owns the x-th eighth of the chunks, and its workgroups sweep that
+  // range side by side (workgroup k takes chunks begin + k, + k + G, ...; G = its
+  // XCD's workgroup count), so at any time each XCD works on a window of
+  // consecutive query chunks of one (batch, head) slice.  The retrieved key and
+  // value chunks then come from a few slices at a time, which the XCD's L2 and
+  // the shared last-level cache keep resident across the queries that reuse them.
+  const int64_t stride = gridDim.x >> 3;
+  const int xcd = (int)(blockIdx.x & 7);
+  const int64_t c_begin = p.nwork * xcd / 8 + (blockIdx.x >> 3);
+  const int64_t c_end = p.nwork * (xcd + 1) / 8;
   if (c_begin >= c_end) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
@@ -151,9 +159,9 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   RowMeta meta{-1, -INFINITY};
   Geo g0(c_begin, p.nQ, p.H);  // geometry of the current chunk and of the two after it
   Geo g1 = g0;
-  g1.next(p.nQ, p.H);
+  g1.next(p.nQ, p.H, stride);
   Geo g2 = g1;
-  g2.next(p.nQ, p.H);
+  g2.next(p.nQ, p.H, stride);
   {
     int64_t ro;
     bool ex, ow;
@@ -163,7 +171,7 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qr + 16 * kb + 8 * hh);
     if (wave == 0) make_slots(m0, g0, 0);
-    if (c_begin + 1 < c_end) {
+    if (c_begin + stride < c_end) {
       row_of(g1, ro, ex, ow);
       meta = load_row_meta(p, ro, ex);
     }
@@ -245,11 +253,11 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     }
   };
 
-  for (int64_t w = c_begin; w < c_end; ++w) {
-    const int par = (int)((w - c_begin) & 1);
+  int par = 0;
+  for (int64_t w = c_begin; w < c_end; w += stride, par ^= 1) {
     const int n = sN[par];
     const int R = n > 0 ? (n + 1) / 2 : 1;
-    const bool has_next = w + 1 < c_end;
+    const bool has_next = w + stride < c_end;
     f32x16 o0 = zero16(), o1 = zero16();
     for (int r = 0; r < R; ++r) {
       wait_vmem<0>();
@@ -264,11 +272,11 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
           kvb = kvb_n;
         }
         if (has_next) {
-          const T* qr = qrow_ptr(w + 1);
+          const T* qr = qrow_ptr(w + stride);
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb) qn[kb] = load_frag(qr + 16 * kb + 8 * hh);
           if (wave == 0) make_slots(meta, g1, par ^ 1);
-          if (w + 2 < c_end) {
+          if (w + 2 * stride < c_end) {
             int64_t ro;
             bool ex, ow;
             row_of(g2, ro, ex, ow);
@@ -345,7 +353,7 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     }
     g0 = g1;
     g1 = g2;
-    g2.next(p.nQ, p.H);
+    g2.next(p.nQ, p.H, stride);
   }
 }
 
@@ -362,10 +370,9 @@ hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const 
   p.nwork = (int64_t)s.B * s.H * s.nQ;
   p.causal = s.causal;
   p.attn_scale = s.attn_scale;
-  // persistent workgroups: two per CU (256 CUs), each taking a contiguous run of chunks
+  // persistent workgroups: two per CU (256 CUs), a multiple of 8 (one share per XCD)
   const int64_t target = 512;
-  p.per = (p.nwork + target - 1) / target;
-  const dim3 grid((unsigned)round8((p.nwork + p.per - 1) / p.per)), block(kThreads);
+  const dim3 grid((unsigned)(p.nwork < target ? round8(p.nwork) : target)), block(kThreads);
   if (s.bf16) {
     if (s.off_by_one) {
       hipLaunchKernelGGL((xattn_fwd_kernel<__bf16, true>), grid, block, 0, stream, p);
