@@ -276,6 +276,11 @@ __device__ __forceinline__ uint64_t uniform_addr(const void* g) {
   return (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)ga) |
          ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(ga >> 32)) << 32);
 }
+// A wave-uniform 64-bit integer forced into scalar registers.
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+  return (int64_t)((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)x) |
+                   ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32)) << 32));
+}
 // A wave-uniform LDS byte address (plus a wave-uniform offset) in a scalar register.
 __device__ __forceinline__ uint32_t uniform_lds(const void* lds, uint32_t add = 0) {
   return __builtin_amdgcn_readfirstlane(
@@ -291,7 +296,7 @@ template <typename T, int NW>
 struct TileCopy {
   static constexpr int kVec = Swz<T>::kVec, kCPR = Swz<T>::kCPR, kN = kCPR / NW;
   uint32_t goff[kN];
-  uint32_t lwave;  // this wave's first 1 KiB block of the tile in LDS
+  uint32_t lwave;  // this wave's first 1 KiB block of the tile in LDS (scalar)
 
   __device__ __forceinline__ TileCopy(int wave, int lane) {
 #pragma unroll
@@ -301,13 +306,11 @@ struct TileCopy {
       const int c = (pch % kCPR) ^ Swz<T>::sw(r);
       goff[ii] = (uint32_t)((r * kD + c * kVec) * sizeof(T));
     }
-    lwave = (uint32_t)(wave * 64 * 16);
+    lwave = __builtin_amdgcn_readfirstlane((uint32_t)(wave * 64 * 16));
   }
   __device__ __forceinline__ void issue(const T* g, const T* lds) const {
     const uint64_t gs = uniform_addr(g);
-    // wave-uniform, but the wave index comes from the thread index: read back from
-    // lane 0 so that it lives in a scalar register
-    const uint32_t lb = uniform_lds(lds, lwave);
+    const uint32_t lb = uniform_lds(lds) + lwave;
 #pragma unroll
     for (int ii = 0; ii < kN; ++ii)
       asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(goff[ii]), "s"(gs),
@@ -407,6 +410,25 @@ __device__ __forceinline__ f32x8 lds_frag(const float* tile, int r, int col) {
   f32x8 f;
   f.lo = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off(r, col));
   f.hi = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off(r, col + 4));
+  return f;
+}
+
+// Fragment reads at precomputed LDS byte addresses (address space 3), so that a
+// constant displacement folds into the instruction's offset field.
+typedef __attribute__((address_space(3))) char lds_char;
+__device__ __forceinline__ bf16x8 lds_b128_at(const lds_char* p) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(p);
+}
+// Transposed fragment (see lds_frag_t): the two 8-byte transposed reads at p and
+// p + gap bytes (rows r0.. and r1.. of the same 16 columns).
+template <int GAP>
+__device__ __forceinline__ bf16x8 lds_tr_at(const lds_char* p) {
+  typedef __attribute__((address_space(3))) bf16x4_tr lds_v4;
+  bf16x4_tr a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p));
+  bf16x4_tr b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p + GAP));
+  bf16x8 f;
+  f[0] = a[0]; f[1] = a[1]; f[2] = a[2]; f[3] = a[3];
+  f[4] = b[0]; f[5] = b[1]; f[6] = b[2]; f[7] = b[3];
   return f;
 }
 

@@ -1,18 +1,19 @@
 // Grouped cross attention forward (Eq. 2-3 of the method; Algorithm 1 in the
 // appendix is its tiled form).
 //
-// One workgroup of four waves per (batch, head, query chunk): two pairs of
-// waves take alternate retrieved chunks, and within a pair each wave owns 32 of
-// the chunk's 64 query tokens and keeps their Q fragments in registers.  The
-// retrieved chunks' keys and values stream through a four-slot LDS ring filled
-// by asynchronous direct-to-LDS copies one round ahead of the compute (two
-// waves per SIMD hide each other's MFMA, LDS and cross-lane latencies).  For
-// every retrieved chunk (slot) a pair computes S^T = K Q^T on the
-// matrix cores, takes each query's softmax over the 64 keys (one retrieved
-// chunk is exactly one tile, so no running rescale is needed), folds the
-// fusion weight w_s / l_s into P, and accumulates O^T += V^T (w_s P_s)^T into one
-// fp32 accumulator per pair; the two pairs' accumulators are summed at the end.  The per-chunk outputs O'_s of
-// Algorithm 1 are never written; the log-sum-exp of every (row, slot) is.
+// Persistent workgroups of four waves: each pair of waves is a stream of
+// (batch, head, query chunk) work items, and within a pair each wave owns 32 of
+// the chunk's 64 query tokens and keeps their Q fragments in registers.  A pair
+// takes its chunk's retrieved chunks one per round; their keys and values stream
+// through the pair's two LDS ring slots, filled by asynchronous direct-to-LDS
+// copies one round ahead of the compute (two waves per SIMD hide each other's
+// MFMA, LDS and cross-lane latencies).  For every retrieved chunk (slot) a wave
+// computes S^T = K Q^T on the matrix cores, takes each query's softmax over the
+// 64 keys (one retrieved chunk is exactly one tile, so no running rescale is
+// needed), folds the fusion weight w_s / l_s into P, and accumulates
+// O^T += V^T (w_s P_s)^T in registers; at the end of the chunk each wave stores
+// its rows.  The per-chunk outputs O'_s of Algorithm 1 are never written; the
+// log-sum-exp of every (row, slot) is.
 //
 // Computing the transposed products keeps every query's statistics inside one
 // lane (query = accumulator column): the softmax needs one cross-lane step, and
@@ -90,32 +91,38 @@ __device__ __forceinline__ RowMeta load_row_meta(const FwdParams& p, int64_t row
 template <typename T, bool OBO>
 __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   constexpr int TILE = kS * kD;
-  __shared__ __attribute__((aligned(16))) T ring[4 * 2 * TILE];  // 4 slots: a chunk's K and V tiles
-  __shared__ float sLse[32 * kS];  // current chunk: [slot][query]
-  __shared__ int sJ[2][32];        // per slot: chunk index or -1 (current and next chunk)
-  __shared__ int sSlot[2][32];     // compacted lists of valid slots: slot, chunk, weight
-  __shared__ int sJc[2][32];
-  __shared__ float sWc[2][32];
-  __shared__ int sN[2];
+  __shared__ __attribute__((aligned(16))) T ring[4 * 2 * TILE];  // pair p: slots 2p, 2p+1 (K and V tiles)
+  __shared__ int sJ[2][2][32];     // [pair][chunk parity][slot]: chunk index or -1
+  __shared__ int sSlot[2][2][32];  // compacted lists of the valid slots: slot, chunk, weight
+  __shared__ int sJc[2][2][32];
+  __shared__ float sWc[2][2][32];
+  __shared__ int sN[2][2];
 
-  // Work order: workgroups are dealt to the eight XCDs round-robin (blockIdx mod
-  // 8).  XCD x owns the x-th eighth of the chunks, and its workgroups sweep that
-  // range side by side (workgroup k takes chunks begin + k, + k + G, ...; G = its
-  // XCD's workgroup count), so at any time each XCD works on a window of
-  // consecutive query chunks of one (batch, head) slice.  The retrieved key and
-  // value chunks then come from a few slices at a time, which the XCD's L2 and
-  // the shared last-level cache keep resident across the queries that reuse them.
-  const int64_t stride = gridDim.x >> 3;
-  const int xcd = (int)(blockIdx.x & 7);
-  const int64_t c_begin = p.nwork * xcd / 8 + (blockIdx.x >> 3);
-  const int64_t c_end = p.nwork * (xcd + 1) / 8;
-  if (c_begin >= c_end) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
+  // Work order: workgroups are dealt to the eight XCDs round-robin (blockIdx mod
+  // 8) and each wave pair is a stream of query chunks.  XCD x owns the x-th eighth
+  // of the chunks and its streams sweep that range side by side (stream t takes
+  // chunks begin + t, + t + S, ...; S = the XCD's stream count), so at any time
+  // an XCD works on a window of consecutive query chunks of one (batch, head)
+  // slice, whose retrieved key/value chunks its L2 and the shared last-level cache
+  // keep resident across the queries that reuse them.
+  const int64_t stride = (int64_t)(gridDim.x >> 3) * 2;
+  const int xcd = (int)(blockIdx.x & 7);
+  const int64_t r_lo = p.nwork * xcd / 8, r_hi = p.nwork * (xcd + 1) / 8;
+  const int64_t st_wg = (int64_t)(blockIdx.x >> 3) * 2;
+  auto stream_len = [&](int64_t st) -> int64_t {
+    return r_lo + st < r_hi ? (r_hi - r_lo - st + stride - 1) / stride : 0;
+  };
+  const int64_t my_n = stream_len(st_wg + pair);
+  const int64_t nch = max(stream_len(st_wg), stream_len(st_wg + 1));  // both pairs run nch chunks of rounds
+  if (nch == 0) return;
+  const int64_t c_begin = r_lo + st_wg + pair;
   const int K = p.topk;
   const int qi = 32 * half + (lane & 31);  // this lane's query token within a chunk
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
+  const int l32 = lane & 31;
 
   // work item w = (b, h, c): geometry helpers
   auto row_of = [&](const Geo& g, int64_t& row_off, bool& exists, bool& owner) __device__ {
@@ -125,8 +132,8 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     row_off = ((g.b * p.Hr + hr) * p.nQ + (exists ? t : 0)) * K;
     owner = p.Hr != 1 || g.h == 0;  // writes the row's weights
   };
-  // wave 0: turn a row's metadata into the compacted slot list of buffer par
-  auto make_slots = [&](const RowMeta& m, const Geo& g, int par) __device__ {
+  // first wave of a pair: turn a row's metadata into the pair's compacted slot list
+  auto make_slots = [&](const RowMeta& m, const Geo& g, int buf) __device__ {
     int64_t row_off;
     bool exists, owner;
     row_of(g, row_off, exists, owner);
@@ -140,14 +147,14 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
     const float wv = valid ? e / sum : 0.f;
     const uint64_t mask = __ballot(valid);
-    if (lane < 32) sJ[par][lane] = valid ? m.j : -1;
+    if (lane < 32) sJ[pair][buf][lane] = valid ? m.j : -1;
     if (valid) {
       const int rk = __popcll(mask & ((1ull << lane) - 1));
-      sSlot[par][rk] = lane;
-      sJc[par][rk] = m.j;
-      sWc[par][rk] = wv;
+      sSlot[pair][buf][rk] = lane;
+      sJc[pair][buf][rk] = m.j;
+      sWc[pair][buf][rk] = wv;
     }
-    if (lane == 0) sN[par] = __popcll(mask);
+    if (lane == 0) sN[pair][buf] = __popcll(mask);
     if (p.w && exists && owner && lane < K) p.w[row_off + lane] = wv;
   };
   auto qrow_ptr = [&](int64_t w) __device__ {
@@ -162,7 +169,7 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   g1.next(p.nQ, p.H, stride);
   Geo g2 = g1;
   g2.next(p.nQ, p.H, stride);
-  {
+  if (my_n > 0) {
     int64_t ro;
     bool ex, ow;
     row_of(g0, ro, ex, ow);
@@ -170,46 +177,71 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     const T* qr = qrow_ptr(c_begin);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qr + 16 * kb + 8 * hh);
-    if (wave == 0) make_slots(m0, g0, 0);
-    if (c_begin + stride < c_end) {
+    if (half == 0) make_slots(m0, g0, 0);
+    if (my_n > 1) {
       row_of(g1, ro, ex, ow);
       meta = load_row_meta(p, ro, ex);
     }
-    wait_vmem<0>();
-    __syncthreads();
   }
+  wait_vmem<0>();
+  __syncthreads();
 
-  // the ring: global round counter picks the slot pair (rounds alternate slots 0,1 / 2,3)
-  int round = 0;
-  const TileCopy<T, 4> cp(wave, lane);
+  // the pair's two ring slots alternate: cs is the slot of the next item to compute
+  const TileCopy<T, 2> cp(half, lane);
   const T* const gk = reinterpret_cast<const T*>(p.k);
   const T* const gv = reinterpret_cast<const T*>(p.v);
   // element offset of the (batch, head) key/value slice of chunk w
   auto slice_of = [&](const Geo& g) __device__ { return (g.b * p.H + g.h) * p.nKV * TILE; };
   auto issue_item = [&](int64_t kvb, int j, int slot) __device__ {
-    T* dst = ring + slot * (2 * TILE);
+    T* dst = ring + (2 * pair + slot) * (2 * TILE);
     cp.issue(gk + kvb + (int64_t)j * TILE, dst);
     cp.issue(gv + kvb + (int64_t)j * TILE, dst + TILE);
   };
-  // lane u < 32 of each list holds valid item u of the current chunk (slot, chunk,
-  // weight) or of the next chunk (chunk); items are picked with a lane read
-  const int l32 = lane & 31;
-  int ls = sSlot[0][l32], lj = sJc[0][l32], ljn = 0;
-  float lw = sWc[0][l32];
-  int64_t kvb = slice_of(g0), kvb_n = 0;
-  // copies of round 0 of the first chunk
-  if (sN[0] > 0) issue_item(kvb, __builtin_amdgcn_readlane(lj, 0), 0);
-  if (sN[0] > 1) issue_item(kvb, __builtin_amdgcn_readlane(lj, 1), 1);
+  // lane u < 32 of the lists holds valid item u of the current chunk (slot, chunk,
+  // weight); items are picked with a lane read
+  int ls = sSlot[pair][0][l32], lj = sJc[pair][0][l32];
+  float lw = sWc[pair][0][l32];
+  int64_t kvb = uniform64(slice_of(g0)), kvb_n = 0;
+  int cs = 0;
+  if (my_n > 0 && sN[pair][0] > 0) issue_item(kvb, __builtin_amdgcn_readlane(lj, 0), cs);
 
-  auto compute = [&](const T* sK, int u, f32x16& o0, f32x16& o1) __device__ {
+  // bf16 fragment addresses: this lane's byte offsets inside its pair's first ring
+  // slot, computed once; a round adds its slot's offset and every fragment read is
+  // one of these six addresses plus an immediate (row +32, key block, V tile,
+  // transposed-row gap).
+  constexpr bool kB16 = std::is_same<T, __bf16>::value;
+  constexpr uint32_t kTileB = TILE * sizeof(T), kRowB = kD * sizeof(T);
+  const lds_char* const lds0 = (const lds_char*)(ring);
+  uint32_t kofs[4], vofs[2];
+  {
+    const uint32_t pb = (uint32_t)pair * 4 * kTileB;
+    const int s16 = lane & 15;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) kofs[kb] = pb + Swz<T>::off(lane & 31, 16 * kb + 8 * hh) * sizeof(T);
+#pragma unroll
+    for (int dh = 0; dh < 2; ++dh)
+      vofs[dh] = pb + kTileB + Swz<T>::off(4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
+  }
+
+  // one retrieved chunk (item u of the current chunk, tokens from tok0) against
+  // this wave's 32 queries; its tiles are in the pair's ring slot `slot`
+  auto compute = [&](int slot, int u, int64_t tok0, f32x16& o0, f32x16& o1) __device__ {
+    const uint32_t co = (uint32_t)slot * 2 * kTileB;
     const int s = __builtin_amdgcn_readlane(ls, u);
+    const T* sK = ring + (2 * pair + slot) * (2 * TILE);
     const T* sV = sK + TILE;
     // all K fragments first, so the eight products issue back to back
     Frag<T> ka[8];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      ka[2 * kb] = lds_frag(sK, lane & 31, 16 * kb + 8 * hh);
-      ka[2 * kb + 1] = lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh);
+      if constexpr (kB16) {
+        const lds_char* kp = lds0 + (kofs[kb] + co);
+        ka[2 * kb] = lds_b128_at(kp);
+        ka[2 * kb + 1] = lds_b128_at(kp + 32 * kRowB);
+      } else {
+        ka[2 * kb] = lds_frag(sK, lane & 31, 16 * kb + 8 * hh);
+        ka[2 * kb + 1] = lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh);
+      }
     }
     f32x16 st0 = zero16(), st1 = zero16();
 #pragma unroll
@@ -221,24 +253,30 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     Frag<T> va[8];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      va[2 * kb] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
-      va[2 * kb + 1] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
+      if constexpr (kB16) {
+        va[2 * kb] = lds_tr_at<8 * kRowB>(lds0 + (vofs[0] + co) + 16 * kb * kRowB);
+        va[2 * kb + 1] = lds_tr_at<8 * kRowB>(lds0 + (vofs[1] + co) + 16 * kb * kRowB);
+      } else {
+        va[2 * kb] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
+        va[2 * kb + 1] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
+      }
     }
-    float mx = -INFINITY;
+    float mx = fmaxf(st0[0], st1[0]);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(st0[i], st1[i]));
+    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, fmaxf(st0[i], st1[i]));
     mx = max_xor32(mx) * sc;
     if (OBO) mx = fmaxf(mx, 0.f);
-    float sum = 0.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       st0[i] = __builtin_amdgcn_exp2f(fmaf(st0[i], sc, -mx));
       st1[i] = __builtin_amdgcn_exp2f(fmaf(st1[i], sc, -mx));
-      sum += st0[i] + st1[i];
     }
+    float sum = st0[0] + st1[0];
+#pragma unroll
+    for (int i = 1; i < 16; ++i) sum += st0[i] + st1[i];
     sum = sum_xor32(sum);
     if (OBO) sum += __builtin_amdgcn_exp2f(-mx);
-    if (hh == 0) sLse[s * kS + qi] = (mx + __builtin_amdgcn_logf(sum)) * kLn2;
+    if (p.lse && hh == 0) p.lse[(tok0 + qi) * K + s] = (mx + __builtin_amdgcn_logf(sum)) * kLn2;
     const int coef_bits = __builtin_amdgcn_readlane(__float_as_int(lw), u);
     const float coef = __int_as_float(coef_bits) * __builtin_amdgcn_rcpf(sum);
     Frag<T> pf[4];
@@ -253,104 +291,87 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     }
   };
 
-  int par = 0;
-  for (int64_t w = c_begin; w < c_end; w += stride, par ^= 1) {
-    const int n = sN[par];
-    const int R = n > 0 ? (n + 1) / 2 : 1;
-    const bool has_next = w + stride < c_end;
-    f32x16 o0 = zero16(), o1 = zero16();
-    for (int r = 0; r < R; ++r) {
+  // Every chunk takes K rounds (a pair whose chunk has fewer valid slots, or that
+  // has run out of chunks, idles), so both pairs meet the same barriers.  Each
+  // round: wait for this wave's copies, barrier (the partner's copies are visible
+  // and the slot read last round is free), copy the pair's next item into that
+  // slot, then compute this round's item.
+  f32x16 o0 = zero16(), o1 = zero16();
+  for (int64_t ci = 0; ci < nch; ++ci) {
+    const bool live = ci < my_n, live_next = ci + 1 < my_n;
+    const int buf = (int)(ci & 1);
+    const int n = live ? sN[pair][buf] : 0;
+    const int64_t w = c_begin + ci * stride;
+    const int64_t tok0 = w * kS;
+    for (int u = 0; u < K; ++u) {
       wait_vmem<0>();
       block_barrier();
-      if (r == 0) {
-        if (w != c_begin) {
+      if (u == 0) {
+        if (ci > 0 && live) {
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb) qf[kb] = qn[kb];
-          ls = sSlot[par][l32];
-          lj = sJc[par][l32];
-          lw = sWc[par][l32];
+          ls = sSlot[pair][buf][l32];
+          lj = sJc[pair][buf][l32];
+          lw = sWc[pair][buf][l32];
           kvb = kvb_n;
         }
-        if (has_next) {
+        if (live_next) {
           const T* qr = qrow_ptr(w + stride);
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb) qn[kb] = load_frag(qr + 16 * kb + 8 * hh);
-          if (wave == 0) make_slots(meta, g1, par ^ 1);
-          if (w + 2 * stride < c_end) {
+          if (half == 0) make_slots(meta, g1, buf ^ 1);
+          if (ci + 2 < my_n) {
             int64_t ro;
             bool ex, ow;
             row_of(g2, ro, ex, ow);
             meta = load_row_meta(p, ro, ex);
           }
+          kvb_n = uniform64(slice_of(g1));
         }
-        block_barrier();  // the next chunk's slot list is visible
-        if (has_next) {
-          ljn = sJc[par ^ 1][l32];
-          kvb_n = slice_of(g1);
-        }
+        if (K == 1) block_barrier();  // the next chunk's list is needed this round
       }
-      const int cur = 2 * (round & 1), nxt = 2 - cur;
-      if (r + 1 < R) {
-        if (2 * r + 2 < n) issue_item(kvb, __builtin_amdgcn_readlane(lj, 2 * r + 2), nxt);
-        if (2 * r + 3 < n) issue_item(kvb, __builtin_amdgcn_readlane(lj, 2 * r + 3), nxt + 1);
-      } else if (has_next) {
-        const int nn = sN[par ^ 1];
-        if (nn > 0) issue_item(kvb_n, __builtin_amdgcn_readlane(ljn, 0), nxt);
-        if (nn > 1) issue_item(kvb_n, __builtin_amdgcn_readlane(ljn, 1), nxt + 1);
+      const bool comp = u < n;
+      const int is = comp ? cs ^ 1 : cs;
+      if (u + 1 < n) {
+        issue_item(kvb, __builtin_amdgcn_readlane(lj, u + 1), is);
+      } else if (u == K - 1 && live_next && sN[pair][buf ^ 1] > 0) {
+        issue_item(kvb_n, sJc[pair][buf ^ 1][0], is);
       }
-      const int u = 2 * r + pair;
-      if (u < n) compute(ring + (cur + pair) * (2 * TILE), u, o0, o1);
-      ++round;
+      if (comp) {
+        compute(cs, u, tok0, o0, o1);
+        cs ^= 1;
+      }
     }
 
-    // ---- finish chunk w: pair 1 hands its partial O^T to pair 0 through this
-    // round's ring slot, which no copy targets until the next round's barrier
-    const int64_t tok0 = w * kS;
-    T* out = reinterpret_cast<T*>(p.out) + tok0 * kD;
-    float* part = reinterpret_cast<float*>(ring + (((round - 1) & 1) == 0 ? 1 : 3) * (2 * TILE));
-    block_barrier();
-    if (pair == 1 && n > 1) {
+    // ---- finish the chunk: each wave stores its 32 query rows
+    if (live) {
+      T* orow = reinterpret_cast<T*>(p.out) + (tok0 + qi) * kD;
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq) {
-        *reinterpret_cast<f32x4*>(part + ((half * 4 + gq) * 2 + 0) * 256 + lane * 4) =
-            f32x4{o0[4 * gq], o0[4 * gq + 1], o0[4 * gq + 2], o0[4 * gq + 3]};
-        *reinterpret_cast<f32x4*>(part + ((half * 4 + gq) * 2 + 1) * 256 + lane * 4) =
-            f32x4{o1[4 * gq], o1[4 * gq + 1], o1[4 * gq + 2], o1[4 * gq + 3]};
+        store4(orow + 8 * gq + 4 * hh, o0[4 * gq], o0[4 * gq + 1], o0[4 * gq + 2], o0[4 * gq + 3]);
+        store4(orow + 32 + 8 * gq + 4 * hh, o1[4 * gq], o1[4 * gq + 1], o1[4 * gq + 2], o1[4 * gq + 3]);
       }
-    }
-    block_barrier();
-    if (pair == 0) {
-      T* orow = out + qi * kD;
-#pragma unroll
-      for (int gq = 0; gq < 4; ++gq) {
-        f32x4 a{0.f, 0.f, 0.f, 0.f}, bq{0.f, 0.f, 0.f, 0.f};
-        if (n > 1) {
-          a = *reinterpret_cast<const f32x4*>(part + ((half * 4 + gq) * 2 + 0) * 256 + lane * 4);
-          bq = *reinterpret_cast<const f32x4*>(part + ((half * 4 + gq) * 2 + 1) * 256 + lane * 4);
+      if (p.lse && n < K && hh == 0) {
+        float* lse = p.lse + (tok0 + qi) * K;
+        for (int s = 0; s < K; ++s)
+          if (sJ[pair][buf][s] < 0) lse[s] = -INFINITY;
+      }
+      // the causal last row feeds no chunk: its weights go out with chunk 0
+      if (p.w && p.causal && g0.c == 0 && half == 1) {
+        int64_t ro;
+        bool ex, ow;
+        row_of(g0, ro, ex, ow);
+        if (ow) {
+          const int64_t last_off = (g0.b * p.Hr + (p.Hr == 1 ? 0 : g0.h)) * p.nQ * K + (p.nQ - 1) * K;
+          float wv;
+          int jv;
+          wave_row_weight(p.idx, p.sel, last_off, K, p.nKV, wv, jv);
+          if (lane < K) p.w[last_off + lane] = wv;
         }
-        store4(orow + 8 * gq + 4 * hh, o0[4 * gq] + a[0], o0[4 * gq + 1] + a[1], o0[4 * gq + 2] + a[2],
-               o0[4 * gq + 3] + a[3]);
-        store4(orow + 32 + 8 * gq + 4 * hh, o1[4 * gq] + bq[0], o1[4 * gq + 1] + bq[1], o1[4 * gq + 2] + bq[2],
-               o1[4 * gq + 3] + bq[3]);
       }
     }
-    if (p.lse) {
-      float* lse = p.lse + (tok0 + lane) * K;
-      for (int s = wave; s < K; s += 4) lse[s] = sJ[par][s] >= 0 ? sLse[s * kS + lane] : -INFINITY;
-    }
-    // the causal last row feeds no chunk: its weights go out with chunk 0
-    if (p.w && p.causal && g0.c == 0 && wave == 1) {
-      int64_t ro;
-      bool ex, ow;
-      row_of(g0, ro, ex, ow);
-      if (ow) {
-        const int64_t last_off = (g0.b * p.Hr + (p.Hr == 1 ? 0 : g0.h)) * p.nQ * K + (p.nQ - 1) * K;
-        float wv;
-        int jv;
-        wave_row_weight(p.idx, p.sel, last_off, K, p.nKV, wv, jv);
-        if (lane < K) p.w[last_off + lane] = wv;
-      }
-    }
+    o0 = zero16();
+    o1 = zero16();
     g0 = g1;
     g1 = g2;
     g2.next(p.nQ, p.H, stride);
@@ -370,9 +391,10 @@ hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const 
   p.nwork = (int64_t)s.B * s.H * s.nQ;
   p.causal = s.causal;
   p.attn_scale = s.attn_scale;
-  // persistent workgroups: two per CU (256 CUs), a multiple of 8 (one share per XCD)
-  const int64_t target = 512;
-  const dim3 grid((unsigned)(p.nwork < target ? round8(p.nwork) : target)), block(kThreads);
+  // persistent workgroups: two per CU (256 CUs), a multiple of 8 (one share per
+  // XCD), each running two chunk streams
+  const int64_t target = 512, wgs = (p.nwork + 1) / 2;
+  const dim3 grid((unsigned)(wgs < target ? round8(wgs) : target)), block(kThreads);
   if (s.bf16) {
     if (s.off_by_one) {
       hipLaunchKernelGGL((xattn_fwd_kernel<__bf16, true>), grid, block, 0, stream, p);
