@@ -481,6 +481,29 @@ __device__ __forceinline__ int64_t xcd_swizzle(int64_t bid, int64_t grid) {
   return (bid & 7) * per + (bid >> 3);
 }
 
+// Position (b, h, c) of work item w = (b * H + h) * nQ + c, advanced a fixed
+// number of chunks at a time so that persistent loops need no divisions.
+struct Geo {
+  int64_t b, c;
+  int h;
+  __device__ __forceinline__ Geo(int64_t w, int64_t nQ, int H) {
+    c = w % nQ;
+    const int64_t bh = w / nQ;
+    h = (int)(bh % H);
+    b = bh / H;
+  }
+  __device__ __forceinline__ void next(int64_t nQ, int H, int64_t step) {
+    c += step;
+    while (c >= nQ) {
+      c -= nQ;
+      if (++h == H) {
+        h = 0;
+        ++b;
+      }
+    }
+  }
+};
+
 // ---------------------------------------------------- top-k selection ----
 
 // Ordering of retrieval candidates: higher score first, ties to lower chunk index.

@@ -34,7 +34,8 @@ template <> struct LdsLd<float> { static constexpr int v = 68; };
 struct Ws {
   float* w;        // [B*Hr, nQ, K] fusion weights
   float* Dbuf;     // [B*H, Lq, K]  D_s per query token
-  float* dwp;      // [B*H, nQ, K]  per-head dw partials
+  float* Lbuf;     // [B*H, Lq, K]  log2 of 1 / (w_s exp(-lse)): log2(e) lse - log2(w_s)
+  float* dwp;      // [B*H, nQ, K, 2] dw partials per head and query half
   int* counts;     // [B*Hr, nKV]
   int* cursor;     // [B*Hr, nKV]
   int* offs;       // [B*Hr, nKV+1]
@@ -49,7 +50,8 @@ Ws carve(const Shape& s, void* base) {
   auto take = [&](size_t bytes) { char* r = p; p += align256(bytes); return r; };
   w.w = (float*)take(sizeof(float) * BHr * s.nQ * s.topk);
   w.Dbuf = (float*)take(sizeof(float) * BH * s.nQ * kS * s.topk);
-  w.dwp = (float*)take(sizeof(float) * BH * s.nQ * s.topk);
+  w.Lbuf = (float*)take(sizeof(float) * BH * s.nQ * kS * s.topk);
+  w.dwp = (float*)take(sizeof(float) * BH * s.nQ * s.topk * 2);
   w.counts = (int*)take(sizeof(int) * BHr * s.nKV);
   w.cursor = (int*)take(sizeof(int) * BHr * s.nKV);
   w.offs = (int*)take(sizeof(int) * BHr * (s.nKV + 1));
@@ -62,8 +64,8 @@ size_t carve_size(const Shape& s) {
   const int64_t BHr = (int64_t)s.B * s.Hr, BH = (int64_t)s.B * s.H;
   size_t n = 0;
   n += align256(sizeof(float) * BHr * s.nQ * s.topk);
-  n += align256(sizeof(float) * BH * s.nQ * kS * s.topk);
-  n += align256(sizeof(float) * BH * s.nQ * s.topk);
+  n += align256(sizeof(float) * BH * s.nQ * kS * s.topk) * 2;
+  n += align256(sizeof(float) * BH * s.nQ * s.topk * 2);
   n += align256(sizeof(int) * BHr * s.nKV) * 2;
   n += align256(sizeof(int) * BHr * (s.nKV + 1));
   n += align256(sizeof(int) * BHr * s.nQ * s.topk) * 2;
@@ -201,120 +203,177 @@ __global__ __launch_bounds__(256) void csr_sort_kernel(const int* __restrict__ o
 
 // ------------------------------------------------- query-stationary dQ ----
 
-// One workgroup of four waves per (batch, head, query chunk); the two wave pairs
-// take alternate retrieved chunks from a four-slot LDS ring (K_j and V_j tiles),
-// each wave owning 32 query tokens.  dQ partials of the pairs are summed at the end.
+// Persistent workgroups of four waves; each wave pair is a stream of (batch,
+// head, query chunk) items, taking the chunk's retrieved chunks one per round
+// from its two LDS ring slots (K_j and V_j tiles, copied one round ahead), each
+// wave owning 32 query tokens.  Per retrieved chunk it writes D_s and the
+// shifted log-sum-exp used by the key-stationary pass, and the wave's partial
+// sum of D_s for dw; dQ stays in registers until the chunk ends.  The work order
+// is the forward's (each XCD sweeps consecutive chunks of one slice at a time).
 template <typename T>
-__global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t nwork) {
+__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_t nwork) {
   constexpr int TILE = kS * kD;
-  GCA_RING4(T, 2 * TILE)
-  __shared__ float sL[32 * kS];  // [slot][query]: lse on entry, D_s on exit
-  __shared__ float sW[32];
-  __shared__ int sJ[32];
-  __shared__ int sSlot[32];
-  __shared__ int sN;
+  __shared__ __attribute__((aligned(16))) T ring[4 * 2 * TILE];  // pair p: slots 2p, 2p+1
+  __shared__ int sJ[2][2][32];     // [pair][chunk parity][slot]: chunk index or -1
+  __shared__ int sSlot[2][2][32];  // compacted valid slots: slot, chunk, weight
+  __shared__ int sJc[2][2][32];
+  __shared__ float sWc[2][2][32];
+  __shared__ int sN[2][2];
 
-  const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
-  if (wid >= nwork) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
-  const int64_t c = wid % p.nQ;
-  const int64_t bh = wid / p.nQ;
-  const int h = (int)(bh % p.H);
-  const int64_t b = bh / p.H;
-  const int hr = p.Hr == 1 ? 0 : h;
-  const int64_t t = p.causal ? c - 1 : 0;
+  const int64_t stride = (int64_t)(gridDim.x >> 3) * 2;
+  const int xcd = (int)(blockIdx.x & 7);
+  const int64_t r_lo = nwork * xcd / 8, r_hi = nwork * (xcd + 1) / 8;
+  const int64_t st_wg = (int64_t)(blockIdx.x >> 3) * 2;
+  auto stream_len = [&](int64_t st) -> int64_t {
+    return r_lo + st < r_hi ? (r_hi - r_lo - st + stride - 1) / stride : 0;
+  };
+  const int64_t my_n = stream_len(st_wg + pair);
+  const int64_t nch = max(stream_len(st_wg), stream_len(st_wg + 1));
+  if (nch == 0) return;
+  const int64_t c_begin = r_lo + st_wg + pair;
   const int K = p.K;
-  const int64_t row_base = (b * p.Hr + hr) * p.nQ;
-  const int64_t tok0 = ((b * p.H + h) * p.nQ + c) * kS;
-
-  if (wave == 0) {
-    int jv = -1;
-    float wv = 0.f;
-    if (t >= 0 && lane < K) {
-      const int j = p.idx[(row_base + t) * K + lane];
-      if (j >= 0 && j < p.nKV) {
-        jv = j;
-        wv = p.ws.w[(row_base + t) * K + lane];
-      }
-    }
-    const uint64_t mask = __ballot(jv >= 0);
-    if (lane < 32) {
-      sW[lane] = wv;
-      sJ[lane] = jv;
-    }
-    if (jv >= 0) sSlot[__popcll(mask & ((1ull << lane) - 1))] = lane;
-    if (lane == 0) sN = __popcll(mask);
-  }
-  if (t >= 0)
-    for (int s = wave; s < K; s += 4) sL[s * kS + lane] = p.lse[(tok0 + lane) * K + s];
-  __syncthreads();
-  const int n = sN;
-  // lane u < 32 holds valid item u's slot, chunk and weight (picked with a lane read)
-  const int ls = sSlot[lane & 31] & 31;
-  const int lj = sJ[ls];
-  const float lw = sW[ls];
-
-  T* dq = reinterpret_cast<T*>(p.dq) + tok0 * kD;
-  if (n == 0) {
-    for (int e = tid; e < kS * kD / 4; e += kThreads) store4(dq + 4 * e, 0.f, 0.f, 0.f, 0.f);
-    if (t >= 0 && tid < K) p.ws.dwp[(bh * p.nQ + t) * K + tid] = 0.f;
-    return;
-  }
-
   const int qi = 32 * half + (lane & 31);
-  const T* qrow = reinterpret_cast<const T*>(p.q) + (tok0 + qi) * kD;
-  const T* dorow = reinterpret_cast<const T*>(p.dout) + (tok0 + qi) * kD;
-  Frag<T> qf[4], df[4];
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    qf[kb] = load_frag(qrow + 16 * kb + 8 * hh);
-    df[kb] = load_frag(dorow + 16 * kb + 8 * hh);
-  }
-  wait_vmem<0>();
-
-  const int64_t kv0 = (b * p.H + h) * p.nKV * TILE;
-  const T* kbase = reinterpret_cast<const T*>(p.k) + kv0;
-  const T* vbase = reinterpret_cast<const T*>(p.v) + kv0;
-  f32x16 g0 = zero16(), g1 = zero16();  // dQ^T, d rows 0-31 / 32-63
+  const int l32 = lane & 31;
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
 
-  const TileCopy<T, 4> cp(wave, lane);
-  auto issue = [&](auto B, int u) __device__ {
-    const int64_t j = __builtin_amdgcn_readlane(lj, u);
-    T* dst = slot_buf(B);
-    cp.issue(kbase + j * TILE, dst);
-    cp.issue(vbase + j * TILE, dst + TILE);
+  // retrieval row t of a chunk: its offset in idx / w, or -1
+  auto row_off_of = [&](const Geo& g) -> int64_t {
+    const int hr = p.Hr == 1 ? 0 : g.h;
+    const int64_t t = p.causal ? g.c - 1 : 0;
+    return t >= 0 ? ((g.b * p.Hr + hr) * p.nQ + t) * K : -1;
   };
-  auto run = [&](auto B, int u) __device__ {
+  struct Meta {
+    int j;
+    float w;
+  };
+  auto load_meta = [&](const Geo& g) -> Meta {
+    Meta m{-1, 0.f};
+    const int64_t ro = row_off_of(g);
+    if (ro >= 0 && lane < K) {
+      m.j = p.idx[ro + lane];
+      m.w = p.ws.w[ro + lane];
+    }
+    return m;
+  };
+  // first wave of a pair: the pair's compacted slot list of a chunk
+  auto make_slots = [&](const Meta& m, int buf) __device__ {
+    const bool valid = lane < K && m.j >= 0 && m.j < p.nKV;
+    const uint64_t mask = __ballot(valid);
+    if (lane < 32) sJ[pair][buf][lane] = valid ? m.j : -1;
+    if (valid) {
+      const int rk = __popcll(mask & ((1ull << lane) - 1));
+      sSlot[pair][buf][rk] = lane;
+      sJc[pair][buf][rk] = m.j;
+      sWc[pair][buf][rk] = m.w;
+    }
+    if (lane == 0) sN[pair][buf] = __popcll(mask);
+  };
+  auto tok_of = [&](const Geo& g) -> int64_t { return ((g.b * p.H + g.h) * p.nQ + g.c) * kS; };
+
+  // ---- prologue
+  Frag<T> qf[4], df[4];  // the current chunk's Q and dO rows of this lane's query
+  Meta meta{-1, 0.f};
+  Geo g0(c_begin, p.nQ, p.H);
+  Geo g1 = g0;
+  g1.next(p.nQ, p.H, stride);
+  Geo g2 = g1;
+  g2.next(p.nQ, p.H, stride);
+  auto load_qdo = [&](const Geo& g, Frag<T>* qd, Frag<T>* dd) __device__ {
+    const int64_t row = tok_of(g) + qi;
+    const T* qr = reinterpret_cast<const T*>(p.q) + row * kD;
+    const T* dr = reinterpret_cast<const T*>(p.dout) + row * kD;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      qd[kb] = load_frag(qr + 16 * kb + 8 * hh);
+      dd[kb] = load_frag(dr + 16 * kb + 8 * hh);
+    }
+  };
+  if (my_n > 0) {
+    const Meta m0 = load_meta(g0);
+    load_qdo(g0, qf, df);
+    if (half == 0) make_slots(m0, 0);
+    if (my_n > 1) meta = load_meta(g1);
+  }
+  wait_vmem<0>();
+  __syncthreads();
+
+  const TileCopy<T, 2> cp(half, lane);
+  const T* const gk = reinterpret_cast<const T*>(p.k);
+  const T* const gv = reinterpret_cast<const T*>(p.v);
+  auto slice_of = [&](const Geo& g) __device__ { return (g.b * p.H + g.h) * p.nKV * TILE; };
+  auto issue_item = [&](int64_t kvb, int j, int slot) __device__ {
+    T* dst = ring + (2 * pair + slot) * (2 * TILE);
+    cp.issue(gk + kvb + (int64_t)j * TILE, dst);
+    cp.issue(gv + kvb + (int64_t)j * TILE, dst + TILE);
+  };
+  int ls = sSlot[pair][0][l32], lj = sJc[pair][0][l32];
+  float lw = sWc[pair][0][l32];
+  int64_t kvb = uniform64(slice_of(g0)), kvb_n = 0;
+  int cs = 0;
+  // this lane's saved lse of the next item to compute (loaded a round ahead)
+  float lse_next = 0.f;
+  if (my_n > 0 && sN[pair][0] > 0) {
+    issue_item(kvb, __builtin_amdgcn_readlane(lj, 0), cs);
+    lse_next = p.lse[(tok_of(g0) + qi) * K + __builtin_amdgcn_readlane(ls, 0)];
+  }
+
+  constexpr bool kB16 = std::is_same<T, __bf16>::value;
+  constexpr uint32_t kTileB = TILE * sizeof(T), kRowB = kD * sizeof(T);
+  const lds_char* const lds0 = (const lds_char*)(ring);
+  uint32_t kofs[4], tofs[2];
+  {
+    const uint32_t pb = (uint32_t)pair * 4 * kTileB;
+    const int s16 = lane & 15;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) kofs[kb] = pb + Swz<T>::off(lane & 31, 16 * kb + 8 * hh) * sizeof(T);
+#pragma unroll
+    for (int dh = 0; dh < 2; ++dh)
+      tofs[dh] = pb + Swz<T>::off(4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
+  }
+
+  f32x16 g0a = zero16(), g1a = zero16();  // dQ^T, d rows 0-31 / 32-63
+  auto run = [&](int slot, int u, float lse_q, int64_t tok0, int64_t t) __device__ {
+    const uint32_t co = (uint32_t)slot * 2 * kTileB;
     const int s = __builtin_amdgcn_readlane(ls, u);
-    const T* sK = slot_buf(B);
+    const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lw), u));
+    const T* sK = ring + (2 * pair + slot) * (2 * TILE);
     const T* sV = sK + TILE;
-    const float lse2 = sL[s * kS + qi] * kLog2e;
     f32x16 s0 = zero16(), s1 = zero16(), p0 = zero16(), p1 = zero16();
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      mma32(s0, lds_frag(sK, lane & 31, 16 * kb + 8 * hh), qf[kb]);
-      mma32(s1, lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh), qf[kb]);
-      mma32(p0, lds_frag(sV, lane & 31, 16 * kb + 8 * hh), df[kb]);
-      mma32(p1, lds_frag(sV, 32 + (lane & 31), 16 * kb + 8 * hh), df[kb]);
+      if constexpr (kB16) {
+        const lds_char* kp = lds0 + (kofs[kb] + co);
+        mma32(s0, lds_b128_at(kp), qf[kb]);
+        mma32(s1, lds_b128_at(kp + 32 * kRowB), qf[kb]);
+        mma32(p0, lds_b128_at(kp + kTileB), df[kb]);
+        mma32(p1, lds_b128_at(kp + (kTileB + 32 * kRowB)), df[kb]);
+      } else {
+        mma32(s0, lds_frag(sK, lane & 31, 16 * kb + 8 * hh), qf[kb]);
+        mma32(s1, lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh), qf[kb]);
+        mma32(p0, lds_frag(sV, lane & 31, 16 * kb + 8 * hh), df[kb]);
+        mma32(p1, lds_frag(sV, 32 + (lane & 31), 16 * kb + 8 * hh), df[kb]);
+      }
     }
-    // P^T and D = rowsum(P o dP) for this lane's query
-    float Dq = 0.f;
+    // w P^T (the weight folded into the exponent: wsf = max(ws, 1e-30) keeps the
+    // shift finite), D = rowsum(P o dP) for this lane's query, w dS
+    const float wsf = fmaxf(ws, 1e-30f);
+    const float off = lse_q * kLog2e - __builtin_amdgcn_logf(wsf);
+    float Dw = 0.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      s0[i] = __builtin_amdgcn_exp2f(fmaf(s0[i], sc, -lse2));
-      s1[i] = __builtin_amdgcn_exp2f(fmaf(s1[i], sc, -lse2));
-      Dq += s0[i] * p0[i] + s1[i] * p1[i];
+      s0[i] = __builtin_amdgcn_exp2f(fmaf(s0[i], sc, -off));
+      s1[i] = __builtin_amdgcn_exp2f(fmaf(s1[i], sc, -off));
+      Dw = fmaf(s0[i], p0[i], Dw);
+      Dw = fmaf(s1[i], p1[i], Dw);
     }
-    Dq = sum_xor32(Dq);
-    if (hh == 0) sL[s * kS + qi] = Dq;  // this lane's pair alone reads the lse it replaces
-    const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lw), u));
+    const float Dq = sum_xor32(Dw) * __builtin_amdgcn_rcpf(wsf);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      s0[i] = ws * s0[i] * (p0[i] - Dq);
-      s1[i] = ws * s1[i] * (p1[i] - Dq);
+      s0[i] = s0[i] * (p0[i] - Dq);
+      s1[i] = s1[i] * (p1[i] - Dq);
     }
     Frag<T> f[4];
     frag_from_acc(f[0], s0, 0, 1.f);
@@ -323,65 +382,106 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(BwdParams p, int64_t n
     frag_from_acc(f[3], s1, 1, 1.f);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      mma32(g0, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), f[kb]);
-      mma32(g1, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), f[kb]);
+      if constexpr (kB16) {
+        mma32(g0a, lds_tr_at<8 * kRowB>(lds0 + (tofs[0] + co) + 16 * kb * kRowB), f[kb]);
+        mma32(g1a, lds_tr_at<8 * kRowB>(lds0 + (tofs[1] + co) + 16 * kb * kRowB), f[kb]);
+      } else {
+        mma32(g0a, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), f[kb]);
+        mma32(g1a, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), f[kb]);
+      }
     }
+    // D_s and the shifted lse of this (query, slot) for the key-stationary pass
+    if (hh == 0) {
+      p.ws.Dbuf[(tok0 + qi) * K + s] = Dq;
+      p.ws.Lbuf[(tok0 + qi) * K + s] = lse_q * kLog2e - __builtin_amdgcn_logf(ws);
+    }
+    // this wave's 32 queries' share of dw[t, s]
+    float dsum = Dq;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) dsum += __shfl_xor(dsum, o);
+    if (lane == 0) p.ws.dwp[(t * K + s) * 2 + half] = dsum;
   };
-  pair_ring(n, pair, issue, run);
 
-  // pair 1 hands its dQ^T partial to pair 0 through LDS, laid out
-  // [half][register group][d half][lane] so that every access is lane-contiguous
-  float* part = reinterpret_cast<float*>(ring0);
-  auto part_at = [&](int g, int dt) { return part + ((half * 4 + g) * 2 + dt) * 256 + lane * 4; };
-  __syncthreads();
-  if (pair == 1) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      *reinterpret_cast<f32x4*>(part_at(g, 0)) = f32x4{g0[4 * g], g0[4 * g + 1], g0[4 * g + 2], g0[4 * g + 3]};
-      *reinterpret_cast<f32x4*>(part_at(g, 1)) = f32x4{g1[4 * g], g1[4 * g + 1], g1[4 * g + 2], g1[4 * g + 3]};
+  for (int64_t ci = 0; ci < nch; ++ci) {
+    const bool live = ci < my_n, live_next = ci + 1 < my_n;
+    const int buf = (int)(ci & 1);
+    const int n = live ? sN[pair][buf] : 0;
+    const int64_t tok0 = tok_of(g0);
+    const int64_t tglob = (g0.b * p.H + g0.h) * p.nQ + (p.causal ? g0.c - 1 : 0);  // dw row (b, h, t)
+    const int64_t tok_n = tok_of(g1);
+    for (int u = 0; u < K; ++u) {
+      wait_vmem<0>();
+      block_barrier();
+      if (u == 0) {
+        if (ci > 0 && live) {
+          ls = sSlot[pair][buf][l32];
+          lj = sJc[pair][buf][l32];
+          lw = sWc[pair][buf][l32];
+          kvb = kvb_n;
+        }
+        if (live_next) {
+          if (half == 0) make_slots(meta, buf ^ 1);
+          if (ci + 2 < my_n) meta = load_meta(g2);
+          kvb_n = uniform64(slice_of(g1));
+        }
+        if (K == 1) block_barrier();  // the next chunk's list is needed this round
+      }
+      const bool comp = u < n;
+      const int is = comp ? cs ^ 1 : cs;
+      const float lse_q = lse_next;
+      if (u + 1 < n) {
+        issue_item(kvb, __builtin_amdgcn_readlane(lj, u + 1), is);
+        lse_next = p.lse[(tok0 + qi) * K + __builtin_amdgcn_readlane(ls, u + 1)];
+      } else if (u == K - 1 && live_next && sN[pair][buf ^ 1] > 0) {
+        issue_item(kvb_n, sJc[pair][buf ^ 1][0], is);
+        lse_next = p.lse[(tok_n + qi) * K + sSlot[pair][buf ^ 1][0]];
+      }
+      if (comp) {
+        run(cs, u, lse_q, tok0, tglob);
+        cs ^= 1;
+      }
+      // the next chunk's Q and dO rows arrive with the copies of its first item
+      if (u == K - 1 && live_next) load_qdo(g1, qf, df);
     }
-  }
-  __syncthreads();
-  if (pair == 0) {
-    const float as = p.attn_scale;
-    T* drow = dq + qi * kD;
+
+    // ---- finish the chunk: dQ rows of this wave; zero dw partials of empty slots
+    if (live) {
+      const float as = p.attn_scale;
+      T* drow = reinterpret_cast<T*>(p.dq) + (tok0 + qi) * kD;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 x0 = *reinterpret_cast<const f32x4*>(part_at(g, 0));
-      const f32x4 x1 = *reinterpret_cast<const f32x4*>(part_at(g, 1));
-      store4(drow + 8 * g + 4 * hh, as * (g0[4 * g] + x0[0]), as * (g0[4 * g + 1] + x0[1]),
-             as * (g0[4 * g + 2] + x0[2]), as * (g0[4 * g + 3] + x0[3]));
-      store4(drow + 32 + 8 * g + 4 * hh, as * (g1[4 * g] + x1[0]), as * (g1[4 * g + 1] + x1[1]),
-             as * (g1[4 * g + 2] + x1[2]), as * (g1[4 * g + 3] + x1[3]));
+      for (int g = 0; g < 4; ++g) {
+        store4(drow + 8 * g + 4 * hh, as * g0a[4 * g], as * g0a[4 * g + 1], as * g0a[4 * g + 2],
+               as * g0a[4 * g + 3]);
+        store4(drow + 32 + 8 * g + 4 * hh, as * g1a[4 * g], as * g1a[4 * g + 1], as * g1a[4 * g + 2],
+               as * g1a[4 * g + 3]);
+      }
+      const bool has_row = !p.causal || g0.c > 0;
+      if (has_row && n < K && lane < K && sJ[pair][buf][lane] < 0) p.ws.dwp[(tglob * K + lane) * 2 + half] = 0.f;
     }
+    g0a = zero16();
+    g1a = zero16();
+    g0 = g1;
+    g1 = g2;
+    g2.next(p.nQ, p.H, stride);
   }
-  // dw[t, s] = sum over the chunk's 64 queries of D_s (staged in sL): one wave per slot
-  for (int s = wave; s < K; s += 4) {
-    float acc = sJ[s] >= 0 ? sL[s * kS + lane] : 0.f;
-#pragma unroll
-    for (int o = 1; o < 32; o <<= 1) acc += __shfl_xor(acc, o);
-    acc = sum_xor32(acc);
-    if (lane == 0) p.ws.dwp[(bh * p.nQ + t) * K + s] = acc;
-  }
-  float* Dout = p.ws.Dbuf + (tok0 + lane) * K;
-  for (int s = wave; s < K; s += 4) Dout[s] = sJ[s] >= 0 ? sL[s * kS + lane] : 0.f;
 }
 
 // ---------------------------------------------- key-stationary dK, dV ----
 
 // One workgroup of four waves per (batch, head, key chunk j); the two wave pairs
 // take alternate retrievers (row t, slot s) of chunk j from a four-slot LDS ring
-// (Q_c and dO_c tiles plus the lse and D columns of slot s), each wave owning 32
-// of chunk j's keys.  dK/dV partials of the pairs are summed at the end.
+// (Q_c and dO_c tiles plus the shifted-lse and D columns of slot s, which the
+// query-stationary pass wrote), each wave owning 32 of chunk j's keys.  With the
+// shifted lse L = log2(e) lse - log2(w_s), exp2(S log2(e) scale - L) is w_s P_s
+// directly.  dK/dV partials of the pairs are summed at the end.
 template <typename T>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int64_t nwork) {
   constexpr int TILE = kS * kD;
-  // ring slot: Q_c tile, dO_c tile, lse column, D column
+  // ring slot: Q_c tile, dO_c tile, shifted-lse column, D column
   constexpr int ENTRY = 2 * TILE + 2 * kS * (int)(sizeof(float) / sizeof(T));
   __shared__ __attribute__((aligned(16))) T ring[4 * ENTRY];
   constexpr int NE = 256;  // retrievers staged in LDS per batch
   __shared__ int sE[NE];
-  __shared__ float sWt[NE];
 
   const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
   if (wid >= nwork) return;
@@ -424,9 +524,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
 
   const T* qb = reinterpret_cast<const T*>(p.q) + bh * p.nQ * kS * kD;
   const T* ob = reinterpret_cast<const T*>(p.dout) + bh * p.nQ * kS * kD;
-  const float* lseb = p.lse + bh * p.nQ * kS * K;
+  const float* Lb = p.ws.Lbuf + bh * p.nQ * kS * K;
   const float* Db = p.ws.Dbuf + bh * p.nQ * kS * K;
-  const float* wrow = p.ws.w + bhr * p.nQ * K;
 
   const TileCopy<T, 4> cp(wave, lane);
   const uint32_t col_off = (uint32_t)(lane * K * sizeof(float));
@@ -438,7 +537,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
     cp.issue(qb + c * TILE, dst);
     cp.issue(ob + c * TILE, dst + TILE);
     float* cols = reinterpret_cast<float*>(dst + 2 * TILE);
-    if (wave == 0) dma_column_s(lseb + c * kS * K + s, col_off, cols);
+    if (wave == 0) dma_column_s(Lb + c * kS * K + s, col_off, cols);
     else if (wave == 1) dma_column_s(Db + c * kS * K + s, col_off, cols + kS);
   };
 
@@ -447,7 +546,6 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
   const int cb = 16 * ((lane >> 4) & 1);
 
   auto run = [&](int slot, int u) __device__ {
-    const float wt = sWt[u];
     const T* sQ = ring + slot * ENTRY;
     const T* sO = sQ + TILE;
     const float* sL = reinterpret_cast<const float*>(sQ + 2 * TILE);
@@ -468,8 +566,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
         const f32x4 l1 = *reinterpret_cast<const f32x4*>(sL + 32 + 8 * g + 4 * hh);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          s0[4 * g + r] = wt * __builtin_amdgcn_exp2f(fmaf(s0[4 * g + r], sc, -l0[r] * kLog2e));
-          s1[4 * g + r] = wt * __builtin_amdgcn_exp2f(fmaf(s1[4 * g + r], sc, -l1[r] * kLog2e));
+          s0[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s0[4 * g + r], sc, -l0[r]));
+          s1[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s1[4 * g + r], sc, -l1[r]));
         }
       }
       frag_from_acc(wp[0], s0, 0, 1.f);
@@ -524,7 +622,6 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
     for (int i = tid; i < nb; i += kThreads) {
       const int e = list_g[b0 + i];  // t * K + s
       sE[i] = ((e / K + p.causal) << 5) | (e % K);
-      sWt[i] = wrow[e];
     }
     __syncthreads();
     pair_ring_dyn(nb, pair, issue, run);
@@ -589,7 +686,10 @@ __global__ __launch_bounds__(64) void dsel_kernel(const float* __restrict__ w, c
     ws = w[row * K + s];
     if (t + causal < nQ) {
       const int h0 = Hr == 1 ? 0 : hr, h1 = Hr == 1 ? H : hr + 1;
-      for (int h = h0; h < h1; ++h) dw += dwp[((b * H + h) * nQ + t) * K + s];
+      for (int h = h0; h < h1; ++h) {
+        const float* d2 = dwp + (((b * H + h) * nQ + t) * K + s) * 2;
+        dw += d2[0] + d2[1];
+      }
     }
   }
   float tot = ws * dw;
@@ -663,7 +763,9 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
                      w.sorted, BHr, s.nQ, s.topk, s.nKV);
   note_launch("csr_sort_kernel", st);
   const int64_t nq_work = BH * s.nQ, nk_work = BH * s.nKV;
-  hipLaunchKernelGGL(bwd_dq_kernel<T>, dim3((unsigned)round8(nq_work)), dim3(kThreads), 0, st, p, nq_work);
+  // persistent: two workgroups per CU, two chunk streams each
+  const int64_t dq_wgs = std::min<int64_t>(512, round8((nq_work + 1) / 2));
+  hipLaunchKernelGGL(bwd_dq_kernel<T>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
   note_launch("bwd_dq_kernel", st);
   hipLaunchKernelGGL(bwd_dkdv_kernel<T>, dim3((unsigned)round8(nk_work)), dim3(kThreads), 0, st, p, nk_work);
   note_launch("bwd_dkdv_kernel", st);

@@ -55,29 +55,6 @@ struct RowMeta {
   float sv;
 };
 
-// Position (b, h, c) of work item w = (b * H + h) * nQ + c, stepped one chunk at a
-// time so the persistent loop needs no divisions.
-struct Geo {
-  int64_t b, c;
-  int h;
-  __device__ __forceinline__ Geo(int64_t w, int64_t nQ, int H) {
-    c = w % nQ;
-    const int64_t bh = w / nQ;
-    h = (int)(bh % H);
-    b = bh / H;
-  }
-  __device__ __forceinline__ void next(int64_t nQ, int H, int64_t step) {
-    c += step;
-    while (c >= nQ) {
-      c -= nQ;
-      if (++h == H) {
-        h = 0;
-        ++b;
-      }
-    }
-  }
-};
-
 __device__ __forceinline__ RowMeta load_row_meta(const FwdParams& p, int64_t row_off, bool exists) {
   const int lane = threadIdx.x & 63;
   RowMeta m{-1, -INFINITY};
