@@ -133,8 +133,14 @@ __device__ __forceinline__ void frag_from_acc(f32x8& f, const f32x16& acc, int h
   f.hi = f32x4{acc[8 * half + 4], acc[8 * half + 5], acc[8 * half + 6], acc[8 * half + 7]} * scale;
 }
 
-// Entry m of a fragment as fp32.
-__device__ __forceinline__ float frag_elem(const bf16x8& f, int m) { return (float)f[m]; }
+// Entry m of a fragment as fp32.  For bf16 this reads the packed bits (one shift
+// or mask), so the compiler cannot re-derive the value by converting the fp32
+// source again (two instructions per entry).
+__device__ __forceinline__ float frag_elem(const bf16x8& f, int m) {
+  const u32x4 w = __builtin_bit_cast(u32x4, f);
+  const uint32_t x = w[m >> 1];
+  return __uint_as_float((m & 1) ? (x & 0xffff0000u) : (x << 16));
+}
 __device__ __forceinline__ float frag_elem(const f32x8& f, int m) { return m < 4 ? f.lo[m] : f.hi[m - 4]; }
 
 // ------------------------------------------------------- element stores ----
@@ -233,7 +239,11 @@ __device__ __forceinline__ void wait_slots(int m) {
   else wait_vmem<0>();
 }
 
-__device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
+// Workgroup barrier that leaves vector-memory operations (the asynchronous tile
+// copies) in flight: it first drains this wave's LDS operations, so that LDS
+// written before the barrier is visible to every wave after it (s_barrier alone
+// does not wait for a wave's outstanding LDS writes).
+__device__ __forceinline__ void block_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // One direct-to-LDS copy: every lane moves `Bytes` (16 or 4) from its global
 // address to LDS at lds_base + lane * Bytes.  Issued as inline assembly so that

@@ -305,6 +305,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_
   const T* const gv = reinterpret_cast<const T*>(p.v);
   auto slice_of = [&](const Geo& g) __device__ { return (g.b * p.H + g.h) * p.nKV * TILE; };
   auto issue_item = [&](int64_t kvb, int j, int slot) __device__ {
+    j = min(max(j, 0), (int)p.nKV - 1);  // lists hold valid chunks; never copy from outside the slice
     T* dst = ring + (2 * pair + slot) * (2 * TILE);
     cp.issue(gk + kvb + (int64_t)j * TILE, dst);
     cp.issue(gv + kvb + (int64_t)j * TILE, dst + TILE);
@@ -545,9 +546,40 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
   const float sc = p.attn_scale * kLog2e;
   const int cb = 16 * ((lane >> 4) & 1);
 
+  // bf16 fragment addresses: this lane's byte offsets inside a ring slot, computed
+  // once; a round adds its slot's offset and every fragment read is one of these
+  // addresses plus an immediate (row +32, key block, dO tile, transposed-row gap)
+  constexpr bool kB16 = std::is_same<T, __bf16>::value;
+  constexpr uint32_t kTileB = TILE * sizeof(T), kRowB = kD * sizeof(T), kEntryB = ENTRY * sizeof(T);
+  const lds_char* const lds0 = (const lds_char*)(ring);
+  uint32_t rofs[4], tofs[2];
+  {
+    const int s16 = lane & 15;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) rofs[kb] = Swz<T>::off(lane & 31, 16 * kb + 8 * hh) * sizeof(T);
+#pragma unroll
+    for (int dh = 0; dh < 2; ++dh)
+      tofs[dh] = Swz<T>::off(4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
+  }
+  auto row_frag = [&](const T* tile, uint32_t so, int kb, int half32) __device__ -> Frag<T> {
+    if constexpr (kB16) {
+      return lds_b128_at(lds0 + (rofs[kb] + so) + half32 * 32 * kRowB);
+    } else {
+      return lds_frag(tile, 32 * half32 + (lane & 31), 16 * kb + 8 * hh);
+    }
+  };
+  auto col_frag = [&](const T* tile, uint32_t so, int kb, int dh) __device__ -> Frag<T> {
+    if constexpr (kB16) {
+      return lds_tr_at<8 * kRowB>(lds0 + (tofs[dh] + so) + 16 * kb * kRowB);
+    } else {
+      return lds_frag_t(tile, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 * dh + cb);
+    }
+  };
+
   auto run = [&](int slot, int u) __device__ {
     const T* sQ = ring + slot * ENTRY;
     const T* sO = sQ + TILE;
+    const uint32_t qo = (uint32_t)slot * kEntryB, oo = qo + kTileB;
     const float* sL = reinterpret_cast<const float*>(sQ + 2 * TILE);
     const float* sD = sL + kS;
     // S = Q K^T for this wave's keys; queries 0-31 in s0, 32-63 in s1
@@ -556,8 +588,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
       f32x16 s0 = zero16(), s1 = zero16();
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        mma32(s0, lds_frag(sQ, lane & 31, 16 * kb + 8 * hh), kf[kb]);
-        mma32(s1, lds_frag(sQ, 32 + (lane & 31), 16 * kb + 8 * hh), kf[kb]);
+        mma32(s0, row_frag(sQ, qo, kb, 0), kf[kb]);
+        mma32(s1, row_frag(sQ, qo, kb, 1), kf[kb]);
       }
       // w P; accumulator row i holds query 32*qt + 8*(i/4) + 4*hh + i%4
 #pragma unroll
@@ -578,8 +610,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
     // dV^T += dO^T (w P)  (contraction over the 64 queries)
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      mma32(dv0, lds_frag_t(sO, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), wp[kb]);
-      mma32(dv1, lds_frag_t(sO, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), wp[kb]);
+      mma32(dv0, col_frag(sO, oo, kb, 0), wp[kb]);
+      mma32(dv1, col_frag(sO, oo, kb, 1), wp[kb]);
     }
     // dP = dO V^T, then dS = w P o (dP - D) from the w P fragments
     Frag<T> ds[4];
@@ -587,8 +619,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
       f32x16 p0 = zero16(), p1 = zero16();
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        mma32(p0, lds_frag(sO, lane & 31, 16 * kb + 8 * hh), vf[kb]);
-        mma32(p1, lds_frag(sO, 32 + (lane & 31), 16 * kb + 8 * hh), vf[kb]);
+        mma32(p0, row_frag(sO, oo, kb, 0), vf[kb]);
+        mma32(p1, row_frag(sO, oo, kb, 1), vf[kb]);
       }
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -609,8 +641,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
     // dK^T += Q^T dS
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      mma32(dk0, lds_frag_t(sQ, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), ds[kb]);
-      mma32(dk1, lds_frag_t(sQ, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), ds[kb]);
+      mma32(dk0, col_frag(sQ, qo, kb, 0), ds[kb]);
+      mma32(dk1, col_frag(sQ, qo, kb, 1), ds[kb]);
     }
   };
 

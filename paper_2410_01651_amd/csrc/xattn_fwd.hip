@@ -170,6 +170,7 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   // element offset of the (batch, head) key/value slice of chunk w
   auto slice_of = [&](const Geo& g) __device__ { return (g.b * p.H + g.h) * p.nKV * TILE; };
   auto issue_item = [&](int64_t kvb, int j, int slot) __device__ {
+    j = min(max(j, 0), (int)p.nKV - 1);  // lists hold valid chunks; never copy from outside the slice
     T* dst = ring + (2 * pair + slot) * (2 * TILE);
     cp.issue(gk + kvb + (int64_t)j * TILE, dst);
     cp.issue(gv + kvb + (int64_t)j * TILE, dst + TILE);

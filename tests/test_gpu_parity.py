@@ -118,6 +118,7 @@ SWEEP = [
     ("train_16k_bf16", dict(B=1, H=4, n_chunks=9, topk=1), False),       # k = 1
     ("train_16k_bf16", dict(B=1, H=4, Hr=4, D=64, n_chunks=33, topk=3), False),   # per-head retrieval
     ("train_16k_bf16", dict(B=2, H=2, n_chunks=65, topk=32), True),      # off-by-one, k = 32
+    ("train_16k_bf16", dict(B=1, H=2, n_chunks=700, topk=3), False),     # 1,400 chunks: uneven streams
     ("tiny_fp32_1k", dict(B=2, H=3, n_chunks=37, topk=6, whole_reseed=False), True),
     ("tiny_fp32_1k", dict(B=1, H=2, Hr=2, D=128, n_chunks=20, topk=9, whole_reseed=False), False),
     ("decode_16m_bf16", dict(H=4, n_chunks=3000, device_kv=False), False),
@@ -142,6 +143,8 @@ BWD = [
     ("fwdbwd_64k_bf16", dict(B=2, H=3, n_chunks=40, topk=8), False),
     ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=70, topk=20), True),
     ("fwdbwd_64k_bf16", dict(B=1, H=2, Hr=2, D=128, n_chunks=33, topk=5), False),
+    ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=700, topk=1), False),    # k = 1, uneven streams
+    ("tiny_fp32_1k", dict(B=1, H=2, n_chunks=600, topk=1, whole_reseed=False), True),
     ("decode_16m_bf16", dict(H=2, n_chunks=300, planted=0, backward=True, device_kv=False), False),
     ("decode_16m_bf16", dict(H=2, n_chunks=100, topk=4, planted=0, dtype="fp32", backward=True,
                              device_kv=False), False),
