@@ -79,48 +79,6 @@ __device__ __forceinline__ f32x8 load_frag(const float* p) {
   return f;
 }
 
-__device__ __forceinline__ bf16x8 zero_frag(const __bf16*) {
-  bf16x8 z;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) z[i] = (__bf16)0.f;
-  return z;
-}
-__device__ __forceinline__ f32x8 zero_frag(const float*) {
-  f32x8 z;
-  z.lo = f32x4{0.f, 0.f, 0.f, 0.f};
-  z.hi = z.lo;
-  return z;
-}
-
-// Fragment whose contraction runs down a column of a row-major LDS tile M
-// (leading dimension ld): lane l gets M[r0 + e][col] for e = 0..3 followed by
-// M[r1 + e][col], where col = cbase + l%16 and cbase is the column base of the
-// lane's 16-lane group.  For bf16 this is two ds_read_b64_tr_b16: within a
-// 16-lane group, source lane s reads 4 elements of row r + s/4 at column
-// cbase + 4*(s%4), and the hardware hands lane i element i%4 of source lane
-// 4e + i/4, i.e. M[r + e][cbase + i].
-__device__ __forceinline__ bf16x8 load_frag_t(const __bf16* M, int ld, int r0, int r1, int cbase) {
-  const int s = threadIdx.x & 15;
-  const __bf16* p0 = M + (r0 + (s >> 2)) * ld + cbase + 4 * (s & 3);
-  const __bf16* p1 = M + (r1 + (s >> 2)) * ld + cbase + 4 * (s & 3);
-  typedef __attribute__((address_space(3))) bf16x4_tr lds_v4;
-  bf16x4_tr a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p0));
-  bf16x4_tr b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p1));
-  bf16x8 f;
-  f[0] = a[0]; f[1] = a[1]; f[2] = a[2]; f[3] = a[3];
-  f[4] = b[0]; f[5] = b[1]; f[6] = b[2]; f[7] = b[3];
-  return f;
-}
-__device__ __forceinline__ f32x8 load_frag_t(const float* M, int ld, int r0, int r1, int cbase) {
-  const int col = cbase + (threadIdx.x & 15);
-  f32x8 f;
-  f.lo = f32x4{M[(r0 + 0) * ld + col], M[(r0 + 1) * ld + col], M[(r0 + 2) * ld + col],
-               M[(r0 + 3) * ld + col]};
-  f.hi = f32x4{M[(r1 + 0) * ld + col], M[(r1 + 1) * ld + col], M[(r1 + 2) * ld + col],
-               M[(r1 + 3) * ld + col]};
-  return f;
-}
-
 // Build a B/A fragment from accumulator registers: entries 8*half .. 8*half+7
 // of a 32x32 accumulator, scaled.  Used to feed a softmax tile held in the
 // accumulator layout back into the next product without leaving registers.
@@ -159,40 +117,6 @@ __device__ __forceinline__ void store4(float* p, float a, float b, float c, floa
 __device__ __forceinline__ float to_f32(__bf16 x) { return (float)x; }
 __device__ __forceinline__ float to_f32(float x) { return x; }
 
-// 16-byte global <-> LDS staging of a 64 x 64 tile (row-major source, leading
-// dimension 64) into an LDS tile with leading dimension ld, by nthreads threads.
-template <typename T, int NTHREADS>
-struct Tile64 {
-  static constexpr int kVec = 16 / sizeof(T);               // elements per 16 bytes
-  static constexpr int kPerThread = kS * kD / kVec / NTHREADS;
-  u32x4 r[kPerThread];
-
-  __device__ __forceinline__ void load(const T* __restrict__ src, int tid) {
-#pragma unroll
-    for (int it = 0; it < kPerThread; ++it) {
-      const int u = tid + NTHREADS * it;
-      const int row = u / (kD / kVec), col = (u % (kD / kVec)) * kVec;
-      r[it] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + row * kD + col));
-    }
-  }
-  __device__ __forceinline__ void load_cached(const T* __restrict__ src, int tid) {
-#pragma unroll
-    for (int it = 0; it < kPerThread; ++it) {
-      const int u = tid + NTHREADS * it;
-      const int row = u / (kD / kVec), col = (u % (kD / kVec)) * kVec;
-      r[it] = *reinterpret_cast<const u32x4*>(src + row * kD + col);
-    }
-  }
-  __device__ __forceinline__ void store(T* dst, int ld, int tid) const {
-#pragma unroll
-    for (int it = 0; it < kPerThread; ++it) {
-      const int u = tid + NTHREADS * it;
-      const int row = u / (kD / kVec), col = (u % (kD / kVec)) * kVec;
-      *reinterpret_cast<u32x4*>(dst + row * ld + col) = r[it];
-    }
-  }
-};
-
 // ------------------------------------------- asynchronous tile staging ----
 //
 // Chunk tiles (64 tokens x 64 dims, row-major in HBM) are copied straight into
@@ -230,54 +154,11 @@ __device__ __forceinline__ void wait_vmem() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// Wait until at most m * L of this wave's vector-memory operations are pending.
-template <int L>
-__device__ __forceinline__ void wait_slots(int m) {
-  if (m >= 3) wait_vmem<3 * L>();
-  else if (m == 2) wait_vmem<2 * L>();
-  else if (m == 1) wait_vmem<L>();
-  else wait_vmem<0>();
-}
-
 // Workgroup barrier that leaves vector-memory operations (the asynchronous tile
 // copies) in flight: it first drains this wave's LDS operations, so that LDS
 // written before the barrier is visible to every wave after it (s_barrier alone
 // does not wait for a wave's outstanding LDS writes).
 __device__ __forceinline__ void block_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
-// One direct-to-LDS copy: every lane moves `Bytes` (16 or 4) from its global
-// address to LDS at lds_base + lane * Bytes.  Issued as inline assembly so that
-// the compiler neither drains the vector-memory counter for it nor orders LDS
-// reads behind it: completion is tracked only by the explicit wait_vmem /
-// wait_slots calls and the barrier that follows them.  The statement is volatile
-// (kept in order with the barrier) but does not clobber memory: the LDS it
-// writes is never touched between the issuing barrier and the next wait, and
-// leaving other memory unclobbered lets uniform global reads stay scalar.
-template <int Bytes>
-__device__ __forceinline__ void dma_copy(const void* g, const void* lds_base) {
-  const uint32_t base = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)lds_base));
-  if constexpr (Bytes == 16) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(base) : "m0");
-  } else {
-    static_assert(Bytes == 4, "copy size");
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(g), "s"(base) : "m0");
-  }
-}
-
-// Copy one 64x64 tile into swizzled LDS using NW waves (each issues kCPR/NW copies).
-template <typename T, int NW>
-__device__ __forceinline__ void dma_tile(const T* __restrict__ g, T* lds, int wave, int lane) {
-  constexpr int kVec = Swz<T>::kVec, kCPR = Swz<T>::kCPR;
-#pragma unroll
-  for (int ii = 0; ii < kCPR / NW; ++ii) {
-    const int i = ii * NW + wave;
-    const int pch = i * 64 + lane;
-    const int r = pch / kCPR;
-    const int c = (pch % kCPR) ^ Swz<T>::sw(r);
-    dma_copy<16>(g + r * kD + c * kVec, lds + i * 64 * kVec);
-  }
-}
 
 // A wave-uniform global address in scalar registers (the read-back builtin returns
 // a signed int: each half is widened through uint32_t, never sign-extended).
@@ -337,29 +218,6 @@ __device__ __forceinline__ void dma_column_s(const float* g, uint32_t lane_off, 
                : "m0");
 }
 
-// Copy 64 floats spaced `stride` apart into 64 consecutive LDS floats (one wave).
-__device__ __forceinline__ void dma_column(const float* __restrict__ g, int64_t stride, float* lds, int lane) {
-  dma_copy<4>(g + lane * stride, lds);
-}
-
-// Four LDS ring slots as separate variables (so each access names its slot at
-// compile time) and slot_buf(ic<b>) returning slot b.
-template <int V>
-using ic = std::integral_constant<int, V>;
-
-#define GCA_RING4(T, SIZE)                                \
-  __shared__ __attribute__((aligned(16))) T ring0[SIZE];  \
-  __shared__ __attribute__((aligned(16))) T ring1[SIZE];  \
-  __shared__ __attribute__((aligned(16))) T ring2[SIZE];  \
-  __shared__ __attribute__((aligned(16))) T ring3[SIZE];  \
-  auto slot_buf = [&](auto B) __device__ -> T* {          \
-    constexpr int b_ = decltype(B)::value;                \
-    if constexpr (b_ == 0) return ring0;                  \
-    else if constexpr (b_ == 1) return ring1;             \
-    else if constexpr (b_ == 2) return ring2;             \
-    else return ring3;                                    \
-  };
-
 // The same loop over one ring array with runtime slot indices (no per-slot code
 // copies, so the compiler keeps one set of lane address offsets).
 template <typename Issue, typename Run>
@@ -374,40 +232,6 @@ __device__ __forceinline__ void pair_ring_dyn(int n, int pair, Issue&& issue, Ru
     if (2 * v + 3 < n) issue(3 - base, 2 * v + 3);
     const int u = 2 * v + pair;
     if (u < n) run(base + pair, u);
-  }
-}
-
-// Work loop of a 4-wave workgroup whose two wave pairs take alternate items of
-// a list of n items streamed through the 4-slot ring: round v computes items
-// 2v (pair 0) and 2v+1 (pair 1) from slots 2(v%2) and 2(v%2)+1 while the copies
-// for round v+1 fill the other two slots.  issue(ic<slot>, item) starts an
-// item's copies (all waves take part); run(ic<slot>, item) computes one item on
-// the calling pair.  Before each round every wave waits for all of its copies
-// (only the current round's are outstanding) and the barrier makes everyone's
-// copies visible and frees the slots of the previous round.
-template <typename Issue, typename Run>
-__device__ __forceinline__ void pair_ring(int n, int pair, Issue&& issue, Run&& run) {
-  issue(ic<0>{}, 0);
-  if (n > 1) issue(ic<1>{}, 1);
-  for (int v = 0; 2 * v < n; ++v) {
-    wait_vmem<0>();
-    block_barrier();
-    const int u = 2 * v + pair;
-    if ((v & 1) == 0) {
-      if (2 * v + 2 < n) issue(ic<2>{}, 2 * v + 2);
-      if (2 * v + 3 < n) issue(ic<3>{}, 2 * v + 3);
-      if (u < n) {
-        if (pair == 0) run(ic<0>{}, u);
-        else run(ic<1>{}, u);
-      }
-    } else {
-      if (2 * v + 2 < n) issue(ic<0>{}, 2 * v + 2);
-      if (2 * v + 3 < n) issue(ic<1>{}, 2 * v + 3);
-      if (u < n) {
-        if (pair == 0) run(ic<2>{}, u);
-        else run(ic<3>{}, u);
-      }
-    }
   }
 }
 
@@ -442,8 +266,13 @@ __device__ __forceinline__ bf16x8 lds_tr_at(const lds_char* p) {
   return f;
 }
 
-// ... and down a column (see load_frag_t): lane gets rows r0..r0+3 then r1..r1+3 of
-// column cbase + lane%16.
+// Fragment whose contraction runs down a column of a row-major swizzled LDS
+// tile M: lane l gets M[r0 + e][col] for e = 0..3 followed by M[r1 + e][col],
+// where col = cbase + l%16 and cbase is the column base of the lane's 16-lane
+// group.  For bf16 this is two ds_read_b64_tr_b16: within a
+// 16-lane group, source lane s reads 4 elements of row r + s/4 at column
+// cbase + 4*(s%4), and the hardware hands lane i element i%4 of source lane
+// 4e + i/4, i.e. M[r + e][cbase + i].
 __device__ __forceinline__ bf16x8 lds_frag_t(const __bf16* tile, int r0, int r1, int cbase) {
   const int s = threadIdx.x & 15;
   typedef __attribute__((address_space(3))) bf16x4_tr lds_v4;

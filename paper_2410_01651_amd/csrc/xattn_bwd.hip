@@ -27,10 +27,6 @@ namespace {
 
 constexpr int kThreads = 256;  // two pairs of waves
 
-template <typename T> struct LdsLd;
-template <> struct LdsLd<__bf16> { static constexpr int v = 72; };
-template <> struct LdsLd<float> { static constexpr int v = 68; };
-
 struct Ws {
   float* w;        // [B*Hr, nQ, K] fusion weights
   float* Dbuf;     // [B*H, Lq, K]  D_s per query token

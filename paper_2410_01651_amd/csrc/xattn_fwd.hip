@@ -29,10 +29,6 @@ namespace {
 
 constexpr int kThreads = 256;  // two pairs of waves
 
-template <typename T> struct LdsLd;
-template <> struct LdsLd<__bf16> { static constexpr int v = 72; };  // 144-byte rows
-template <> struct LdsLd<float> { static constexpr int v = 68; };   // 272-byte rows
-
 struct FwdParams {
   const void* q;
   const void* k;
