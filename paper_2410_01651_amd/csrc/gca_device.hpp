@@ -298,7 +298,71 @@ __device__ __forceinline__ f32x8 lds_frag_t(const float* tile, int r0, int r1, i
 
 // ------------------------------------------------------ cross-lane ops ----
 
-__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
+// ------------------------------------------------ cross-lane exchange ----
+//
+// Butterfly reductions without the LDS crossbar (ds_bpermute costs a round trip
+// per step): DPP quad permutes swap lanes l ^ 1 and l ^ 2, DPP row rotations by
+// 4 and 8 reach the other quads of a 16-lane row (the half-row mirror the other
+// quad of an 8-lane group), and v_permlane16_swap /
+// v_permlane32_swap hand every lane the pair {x[l], x[l ^ 16]} / {x[l], x[l ^ 32]}.
+constexpr int kDppXor1 = 0xB1;   // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;   // quad_perm [2, 3, 0, 1]
+constexpr int kDppRor4 = 0x124;  // row_ror:4
+constexpr int kDppRor8 = 0x128;  // row_ror:8
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror: lane i of 8 <-> lane 7 - i
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __uint_as_float(dpp<CTRL>(__float_as_uint(x)));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp(int x) {
+  return (int)dpp<CTRL>((uint32_t)x);
+}
+// {x[l], x[l ^ 16]} and {x[l], x[l ^ 32]} (in either order)
+__device__ __forceinline__ void pair16(uint32_t x, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  a = r[0];
+  b = r[1];
+}
+__device__ __forceinline__ void pair32(uint32_t x, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  a = r[0];
+  b = r[1];
+}
+
+// Sum over each 32-lane half (every lane of the half gets it).
+__device__ __forceinline__ float sum32(float x) {
+  x += dpp<kDppXor1>(x);
+  x += dpp<kDppXor2>(x);
+  x += dpp<kDppRor4>(x);
+  x += dpp<kDppRor8>(x);
+  uint32_t a, b;
+  pair16(__float_as_uint(x), a, b);
+  return __uint_as_float(a) + __uint_as_float(b);
+}
+// Sum / max over the whole wave.
+__device__ __forceinline__ float sum64(float x) {
+  x = sum32(x);
+  uint32_t a, b;
+  pair32(__float_as_uint(x), a, b);
+  return __uint_as_float(a) + __uint_as_float(b);
+}
+__device__ __forceinline__ float max64(float x) {
+  x = fmaxf(x, dpp<kDppXor1>(x));
+  x = fmaxf(x, dpp<kDppXor2>(x));
+  x = fmaxf(x, dpp<kDppRor4>(x));
+  x = fmaxf(x, dpp<kDppRor8>(x));
+  uint32_t a, b;
+  pair16(__float_as_uint(x), a, b);
+  x = fmaxf(__uint_as_float(a), __uint_as_float(b));
+  pair32(__float_as_uint(x), a, b);
+  return fmaxf(__uint_as_float(a), __uint_as_float(b));
+}
 
 // x[l] op x[l ^ 32] in every lane with one v_permlane32_swap (no LDS round
 // trip): swapping the wave's halves hands each lane the pair {x[l], x[l ^ 32]}.
@@ -382,14 +446,29 @@ struct TopList {
   }
 };
 
-// Wave-wide best of one (score, chunk) per lane.
-__device__ __forceinline__ void wave_best(float& s, int& j) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float os = __shfl_xor(s, off);
-    const int oj = __shfl_xor(j, off);
-    if (better(os, oj, s, j)) { s = os; j = oj; }
+// Wave-wide best of one (score, chunk) per lane (every lane gets it).
+__device__ __forceinline__ void take_better(float& s, int& j, float os, int oj) {
+  if (better(os, oj, s, j)) {
+    s = os;
+    j = oj;
   }
+}
+__device__ __forceinline__ void wave_best(float& s, int& j) {
+  take_better(s, j, dpp<kDppXor1>(s), dpp<kDppXor1>(j));
+  take_better(s, j, dpp<kDppXor2>(s), dpp<kDppXor2>(j));
+  take_better(s, j, dpp<kDppRor4>(s), dpp<kDppRor4>(j));
+  take_better(s, j, dpp<kDppRor8>(s), dpp<kDppRor8>(j));
+  uint32_t s0, s1, j0, j1;
+  pair16(__float_as_uint(s), s0, s1);
+  pair16((uint32_t)j, j0, j1);
+  s = __uint_as_float(s0);
+  j = (int)j0;
+  take_better(s, j, __uint_as_float(s1), (int)j1);
+  pair32(__float_as_uint(s), s0, s1);
+  pair32((uint32_t)j, j0, j1);
+  s = __uint_as_float(s0);
+  j = (int)j0;
+  take_better(s, j, __uint_as_float(s1), (int)j1);
 }
 
 // Merge the 64 lanes' lists into the wave's best k (k <= 64).  Lane r < *count
@@ -417,7 +496,7 @@ __device__ __forceinline__ void wave_merge(TopList<KM>& L, int k, float& my_s, i
 __device__ __forceinline__ int rank_by_chunk(int my_j, int count) {
   int rank = 0;
   for (int r = 0; r < count; ++r) {
-    const int oj = __shfl(my_j, r);
+    const int oj = __builtin_amdgcn_readlane(my_j, r);
     rank += (oj < my_j) ? 1 : 0;
   }
   return rank;
@@ -437,13 +516,11 @@ __device__ __forceinline__ bool wave_row_weight(const int32_t* __restrict__ idx,
   }
   const bool valid = lane < K && jj >= 0 && jj < nKV;
   float m = valid ? sv : -INFINITY;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  m = max64(m);
   const bool any = __ballot(valid) != 0;
   const float e = valid ? expf(sv - m) : 0.f;
   float sum = e;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+  sum = sum64(sum);
   w = valid ? e / sum : 0.f;
   j = valid ? jj : -1;
   return any;

@@ -197,12 +197,13 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
       acc0 = dot8(a0, b, acc0);
       acc1 = dot8(a1, b, acc1);
     }
-    acc0 += __shfl_xor(acc0, 1);
-    acc1 += __shfl_xor(acc1, 1);
-    acc0 += __shfl_xor(acc0, 2);
-    acc1 += __shfl_xor(acc1, 2);
-    acc0 += __shfl_xor(acc0, 4);
-    acc1 += __shfl_xor(acc1, 4);
+    // sum over the key's 8 lanes (lanes 8m .. 8m+7: quad swaps, then the other quad)
+    acc0 += dpp<kDppXor1>(acc0);
+    acc1 += dpp<kDppXor1>(acc1);
+    acc0 += dpp<kDppXor2>(acc0);
+    acc1 += dpp<kDppXor2>(acc1);
+    acc0 += dpp<kDppHalfMirror>(acc0);
+    acc1 += dpp<kDppHalfMirror>(acc1);
     // spread the insertions of one key group over its 8 lanes
     if (key0 < hi && sub == (it & 7)) {
       const float v = acc0 * scale;
@@ -322,12 +323,8 @@ __global__ __launch_bounds__(256) void fused_select_kernel(const T* __restrict__
   for (int s = 0; s < K; ++s) {
     float bs = L.s[0];
     int bj = L.j[0];
-#pragma unroll
-    for (int off = 1; off <= 2; off <<= 1) {
-      const float os = __shfl_xor(bs, off);
-      const int oj = __shfl_xor(bj, off);
-      if (better(os, oj, bs, bj)) { bs = os; bj = oj; }
-    }
+    take_better(bs, bj, dpp<kDppXor1>(bs), dpp<kDppXor1>(bj));
+    take_better(bs, bj, dpp<kDppXor2>(bs), dpp<kDppXor2>(bj));
     if (bj != kNoChunk) {
       if (L.j[0] == bj) L.pop();
       if (u == 0) { sRs[r][cnt] = bs; sRj[r][cnt] = bj; }

@@ -393,9 +393,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_
       p.ws.Lbuf[(tok0 + qi) * K + s] = lse_q * kLog2e - __builtin_amdgcn_logf(ws);
     }
     // this wave's 32 queries' share of dw[t, s]
-    float dsum = Dq;
-#pragma unroll
-    for (int o = 1; o < 32; o <<= 1) dsum += __shfl_xor(dsum, o);
+    const float dsum = sum32(Dq);
     if (lane == 0) p.ws.dwp[(t * K + s) * 2 + half] = dsum;
   };
 
@@ -721,8 +719,7 @@ __global__ __launch_bounds__(64) void dsel_kernel(const float* __restrict__ w, c
     }
   }
   float tot = ws * dw;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) tot += __shfl_xor(tot, o);
+  tot = sum64(tot);
   if (s < K) dsel[row * K + s] = ws * (dw - tot);
 }
 

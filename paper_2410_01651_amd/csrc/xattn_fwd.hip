@@ -112,12 +112,10 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     row_of(g, row_off, exists, owner);
     const bool valid = lane < K && m.j >= 0 && m.j < p.nKV;
     float mx = valid ? m.sv : -INFINITY;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+    mx = max64(mx);
     const float e = valid ? expf(m.sv - mx) : 0.f;
     float sum = e;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+    sum = sum64(sum);
     const float wv = valid ? e / sum : 0.f;
     const uint64_t mask = __ballot(valid);
     if (lane < 32) sJ[pair][buf][lane] = valid ? m.j : -1;
