@@ -226,6 +226,12 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
 
 constexpr int kMergeThreads = 1024;
 
+// Final top-k of one row from the slices' lists (each sorted best first).  The
+// k-th best slice maximum T is a lower bound for the row's k-th best, so only
+// candidates at or above T can win, and they come from the k slices whose
+// maximum is at or above T: at most k * k candidates.  One pass finds T from
+// the slice maxima, one pass gathers the candidates into LDS, one wave merges
+// them.
 template <int KM>
 __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(const float* __restrict__ cs,
                                                                      const int* __restrict__ cj,
@@ -233,33 +239,67 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(const float
                                                                      float* __restrict__ sel, int K,
                                                                      int64_t slices) {
   constexpr int NW = kMergeThreads / 64;
+  constexpr int kMaxCand = 32 * 32;
   __shared__ float sS[NW * 32];
   __shared__ int sJ[NW * 32];
   __shared__ int sCnt[NW];
+  __shared__ float sCs[kMaxCand];
+  __shared__ int sCj[kMaxCand];
+  __shared__ int sNc;
+  __shared__ float sTs;
+  __shared__ int sTj;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t bhr = blockIdx.x;
   const int64_t n = slices * K;
   const float* c_s = cs + bhr * n;
   const int* c_j = cj + bhr * n;
+
+  // 1. the threshold: k-th best of the slice maxima (slices <= kMergeThreads)
   TopList<KM> L;
   L.init();
-  // eight independent loads in flight per thread per round
-  for (int64_t base = threadIdx.x; base < n; base += 8 * kMergeThreads) {
-    float v[8];
-    int jv[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int64_t e = base + q * kMergeThreads;
-      jv[q] = e < n ? c_j[e] : -1;
-      v[q] = e < n ? c_s[e] : -INFINITY;
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q)
-      if (jv[q] >= 0) L.insert(v[q], jv[q]);
+  if (tid < slices) {
+    const int j = c_j[(int64_t)tid * K];
+    if (j >= 0) L.insert(c_s[(int64_t)tid * K], j);
   }
   float ms;
   int mj, cnt;
   block_merge<KM, NW>(L, K, sS, sJ, sCnt, ms, mj, cnt);
-  if ((threadIdx.x >> 6) == 0) write_sorted<KM>(idx + bhr * K, sel + bhr * K, K, ms, mj, cnt);
+  if (wave == 0) {
+    const float ts = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ms), K - 1));
+    const int tj = __builtin_amdgcn_readlane(mj, K - 1);
+    if (lane == 0) {
+      sTs = cnt >= K ? ts : -INFINITY;  // fewer than k maxima: every candidate qualifies
+      sTj = cnt >= K ? tj : kNoChunk;
+      sNc = 0;
+    }
+  }
+  __syncthreads();
+
+  // 2. gather the candidates at or above the threshold
+  const float ts = sTs;
+  const int tj = sTj;
+  for (int64_t e = tid; e < n; e += kMergeThreads) {
+    const int j = c_j[e];
+    if (j < 0) continue;
+    const float v = c_s[e];
+    if (!better(ts, tj, v, j)) {
+      const int pos = atomicAdd(&sNc, 1);
+      if (pos < kMaxCand) {
+        sCs[pos] = v;
+        sCj[pos] = j;
+      }
+    }
+  }
+  __syncthreads();
+
+  // 3. one wave merges them
+  if (wave == 0) {
+    const int nc = min(sNc, kMaxCand);
+    L.init();
+    for (int i = lane; i < nc; i += 64) L.insert(sCs[i], sCj[i]);
+    wave_merge(L, K, ms, mj, cnt);
+    write_sorted<KM>(idx + bhr * K, sel + bhr * K, K, ms, mj, cnt);
+  }
 }
 
 // ------------------------------------------------ fused causal select ----

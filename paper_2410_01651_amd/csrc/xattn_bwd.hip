@@ -723,43 +723,158 @@ __global__ __launch_bounds__(64) void dsel_kernel(const float* __restrict__ w, c
   if (s < K) dsel[row * K + s] = ws * (dw - tot);
 }
 
+// Weighted sum of gathered landmark rows by one 256-thread workgroup:
+//   out[x] = scale * sum_u w_u src[row_u][x],  x < D,
+// for the n (row, weight) pairs staged in sRow / sW.  A thread owns a 16-byte
+// column block and a residue class of u (the groups), so every load is an
+// independent 16-byte read and four are in flight; the groups' partial sums are
+// added in a fixed order (deterministic).
+constexpr int kMaxGatherPasses = 8;  // D <= 8192: at most 8 passes of 256 blocks (fp32)
+
+template <typename T>
+__device__ __forceinline__ float elem16(const u32x4& r, int m) {
+  if constexpr (sizeof(T) == 2) return __uint_as_float((m & 1) ? (r[m >> 1] & 0xffff0000u) : (r[m >> 1] << 16));
+  else return __uint_as_float(r[m]);
+}
+
+template <typename T>
+__device__ __forceinline__ void gather_rows(const T* __restrict__ src, int D, const int64_t* sRow, const float* sW,
+                                            int n, float (&acc)[kMaxGatherPasses][16 / sizeof(T)], int pass_cols,
+                                            int groups) {
+  constexpr int V = 16 / sizeof(T);
+  const int tid = threadIdx.x, cb = tid % pass_cols, grp = tid / pass_cols;
+  const int nb = D / V;
+  auto ld = [&](int u, int b) { return *reinterpret_cast<const u32x4*>(src + sRow[u] * D + b * V); };
+#pragma unroll
+  for (int pass = 0; pass < kMaxGatherPasses; ++pass) {
+    const int b = pass * pass_cols + cb;
+    if (pass * pass_cols >= nb) break;
+    if (grp < groups && b < nb) {
+      int u = grp;
+      for (; u + 3 * groups < n; u += 4 * groups) {
+        const u32x4 f0 = ld(u, b), f1 = ld(u + groups, b), f2 = ld(u + 2 * groups, b), f3 = ld(u + 3 * groups, b);
+        const float w0 = sW[u], w1 = sW[u + groups], w2 = sW[u + 2 * groups], w3 = sW[u + 3 * groups];
+#pragma unroll
+        for (int m = 0; m < V; ++m)
+          acc[pass][m] += w0 * elem16<T>(f0, m) + w1 * elem16<T>(f1, m) + w2 * elem16<T>(f2, m) +
+                          w3 * elem16<T>(f3, m);
+      }
+      for (; u < n; u += groups) {
+        const u32x4 f0 = ld(u, b);
+#pragma unroll
+        for (int m = 0; m < V; ++m) acc[pass][m] += sW[u] * elem16<T>(f0, m);
+      }
+    }
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void gather_store(float* __restrict__ out, int D, float scale, float* sAcc,
+                                             float (&acc)[kMaxGatherPasses][16 / sizeof(T)], int pass_cols,
+                                             int groups) {
+  constexpr int V = 16 / sizeof(T);
+  const int tid = threadIdx.x, cb = tid % pass_cols, grp = tid / pass_cols;
+  const int nb = D / V;
+#pragma unroll
+  for (int pass = 0; pass < kMaxGatherPasses; ++pass) {
+    const int b = pass * pass_cols + cb;
+    if (pass * pass_cols >= nb) break;
+    __syncthreads();
+    if (grp < groups && b < nb)
+#pragma unroll
+      for (int m = 0; m < V; ++m) sAcc[(grp * pass_cols + cb) * V + m] = acc[pass][m];
+    __syncthreads();
+    if (grp == 0 && b < nb) {
+      float r[V];
+#pragma unroll
+      for (int m = 0; m < V; ++m) r[m] = sAcc[cb * V + m];
+      for (int g = 1; g < groups; ++g)
+#pragma unroll
+        for (int m = 0; m < V; ++m) r[m] += sAcc[(g * pass_cols + cb) * V + m];
+#pragma unroll
+      for (int m = 0; m < V; m += 4)
+        store4(out + b * V + m, scale * r[m], scale * r[m + 1], scale * r[m + 2], scale * r[m + 3]);
+    }
+  }
+}
+
+// column blocks per pass and retriever groups for a 256-thread workgroup
+struct GatherShape {
+  int pass_cols, groups;
+};
+inline GatherShape gather_shape(int D, int elem_bytes) {
+  const int nb = D / (16 / elem_bytes);
+  GatherShape g;
+  g.pass_cols = nb < 256 ? nb : 256;
+  g.groups = 256 / g.pass_cols;
+  return g;
+}
+
 // dlmk_q[t] = score_scale * sum_s dsel[t, s] lmk_k[idx[t, s]]
 template <typename T>
 __global__ __launch_bounds__(256) void dlmk_q_kernel(const T* __restrict__ lk, const int32_t* __restrict__ idx,
                                                      const float* __restrict__ dsel, float* __restrict__ dlq,
-                                                     int64_t nQ, int64_t nKV, int D, int K, float scale) {
+                                                     int64_t nQ, int64_t nKV, int D, int K, float scale,
+                                                     GatherShape gs) {
+  constexpr int V = 16 / sizeof(T);
+  __shared__ int64_t sRow[32];
+  __shared__ float sW[32];
+  __shared__ int sN;
+  __shared__ float sAcc[256 * 8];
   const int64_t row = blockIdx.x;
   const int64_t bhr = row / nQ;
-  for (int x = threadIdx.x; x < D; x += 256) {
-    float acc = 0.f;
-    for (int s = 0; s < K; ++s) {
-      const int j = idx[row * K + s];
-      if (j >= 0 && j < nKV) acc += dsel[row * K + s] * to_f32(lk[(bhr * nKV + j) * D + x]);
+  if (threadIdx.x < 64) {
+    const int s = threadIdx.x;
+    const int j = s < K ? idx[row * K + s] : -1;
+    const bool ok = j >= 0 && j < nKV;
+    const uint64_t mask = __ballot(ok);
+    if (ok) {
+      const int rk = __popcll(mask & ((1ull << s) - 1));
+      sRow[rk] = bhr * nKV + j;
+      sW[rk] = dsel[row * K + s];
     }
-    dlq[row * D + x] = scale * acc;
+    if (s == 0) sN = __popcll(mask);
   }
+  __syncthreads();
+  float acc[kMaxGatherPasses][V];
+  for (int q = 0; q < kMaxGatherPasses; ++q)
+    for (int m = 0; m < V; ++m) acc[q][m] = 0.f;
+  gather_rows<T>(lk, D, sRow, sW, sN, acc, gs.pass_cols, gs.groups);
+  gather_store<T>(dlq + row * D, D, scale, sAcc, acc, gs.pass_cols, gs.groups);
 }
 
-// dlmk_k[j] = score_scale * sum over the rows (t, s) that retrieved j of dsel[t, s] lmk_q[t]
+// dlmk_k[j] = score_scale * sum over the rows (t, s) that retrieved j of dsel[t, s] lmk_q[t],
+// in (t, s) order within each group of the list
 template <typename T>
 __global__ __launch_bounds__(256) void dlmk_k_kernel(const T* __restrict__ lq, const int* __restrict__ offs,
                                                      const int* __restrict__ sorted, const float* __restrict__ dsel,
                                                      float* __restrict__ dlk, int64_t nQ, int64_t nKV, int D, int K,
-                                                     float scale) {
+                                                     float scale, GatherShape gs) {
+  constexpr int V = 16 / sizeof(T);
+  constexpr int NB = 256;
+  __shared__ int64_t sRow[NB];
+  __shared__ float sW[NB];
+  __shared__ float sAcc[256 * 8];
   const int64_t wid = blockIdx.x;  // (b, hr, j)
   const int64_t bhr = wid / nKV, j = wid % nKV;
   const int* off = offs + bhr * (nKV + 1);
   const int lo = off[j], hi = off[j + 1];
   const int* list = sorted + bhr * nQ * K;
-  for (int x = threadIdx.x; x < D; x += 256) {
-    float acc = 0.f;
-    for (int u = lo; u < hi; ++u) {
-      const int e = list[u];
-      const int64_t t = e / K;
-      acc += dsel[(bhr * nQ) * K + e] * to_f32(lq[(bhr * nQ + t) * D + x]);
+  float acc[kMaxGatherPasses][V];
+  for (int q = 0; q < kMaxGatherPasses; ++q)
+    for (int m = 0; m < V; ++m) acc[q][m] = 0.f;
+  for (int b0 = lo; b0 < hi; b0 += NB) {
+    const int nb = min(NB, hi - b0);
+    __syncthreads();
+    if (threadIdx.x < nb) {
+      const int e = list[b0 + threadIdx.x];  // t * K + s
+      sRow[threadIdx.x] = bhr * nQ + e / K;
+      sW[threadIdx.x] = dsel[(bhr * nQ) * K + e];
     }
-    dlk[wid * D + x] = scale * acc;
+    __syncthreads();
+    gather_rows<T>(lq, D, sRow, sW, nb, acc, gs.pass_cols, gs.groups);
   }
+  gather_store<T>(dlk + wid * D, D, scale, sAcc, acc, gs.pass_cols, gs.groups);
 }
 
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
@@ -799,12 +914,12 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
   note_launch("dsel_kernel", st);
   if (dlmk_q) {
     hipLaunchKernelGGL(dlmk_q_kernel<T>, dim3((unsigned)(BHr * s.nQ)), dim3(256), 0, st, (const T*)lmk_k, p.idx,
-                       dsel, dlmk_q, s.nQ, s.nKV, s.D, s.topk, s.score_scale);
+                       dsel, dlmk_q, s.nQ, s.nKV, s.D, s.topk, s.score_scale, gather_shape(s.D, sizeof(T)));
     note_launch("dlmk_q_kernel", st);
   }
   if (dlmk_k) {
     hipLaunchKernelGGL(dlmk_k_kernel<T>, dim3((unsigned)(BHr * s.nKV)), dim3(256), 0, st, (const T*)lmk_q, w.offs,
-                       w.sorted, dsel, dlmk_k, s.nQ, s.nKV, s.D, s.topk, s.score_scale);
+                       w.sorted, dsel, dlmk_k, s.nQ, s.nKV, s.D, s.topk, s.score_scale, gather_shape(s.D, sizeof(T)));
     note_launch("dlmk_k_kernel", st);
   }
   return take_launch_error();
