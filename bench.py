@@ -223,7 +223,7 @@ def bench_train(args, dev, gca):
     }
 
 
-def cpu_baseline(w, t, heads=2):
+def cpu_baseline(w, t, heads=16):
     """The oracle (as it stands) on a bounded sample: batch 0's scores and top-k over
     all 1,024 landmark rows, then attention forward and backward for `heads` heads of
     batch 0 over every chunk.  Extrapolated to the whole batch in tokens/s."""
