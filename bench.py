@@ -316,7 +316,7 @@ def bench_decode(args, dev, gca):
                                "S=64, top-8, D=512, bf16"},
         "roofline": {"kernel": "decode_scan_kernel", "bound": "hbm", "achieved": scan_gbs, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": scan_gbs / HBM_PEAK_GBS,
-                     "traffic": measured_traffic("decode_scan_kernel"),
+                     "traffic": measured_traffic("decode_scan_kernel@decode_16m"),
                      "algorithmic_bytes_per_launch": key_bytes, "avg_launch_ms": scan_ms},
         "kernels": kern,
     }

@@ -18,12 +18,13 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(HERE, "libgca.so")
 OBJ_DIR = os.path.join(HERE, "_build")
 
-SOURCES = ["api.cpp", "scores.hip", "xattn_fwd.hip", "xattn_bwd.hip"]
+SOURCES = ["api.cpp", "scores.hip", "xattn_fwd.hip", "xattn_decode.hip", "xattn_bwd.hip"]
 # The attention kernels never rely on NaN semantics: without IEEE mode the
 # softmax max needs no operand canonicalisation, and MFMA accumulators in
 # ordinary VGPRs need no copies out of the accumulation registers.
 PER_SOURCE = {
     "xattn_fwd.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "xattn_decode.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form"],
     "xattn_bwd.hip": ["-mno-amdgpu-ieee", "-fno-honor-nans", "-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 ARCH = "gfx950"

@@ -265,7 +265,14 @@ gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_
   (void)gca::take_launch_error();
   hipError_t e;
   if (!s.causal) {
-    e = gca::launch_decode_select(s, lmk_q, lmk_k, idx, sel, workspace, stream);
+    // decode: the scan leaves per-range lists; the attention merges them into
+    // idx/sel and attends in the same launch
+    e = gca::launch_decode_scan(s, lmk_q, lmk_k, workspace, stream);
+    if (e != hipSuccess) return from_hip(e, "gca_forward (decode scan)");
+    return from_hip(gca::launch_xattn_decode(s, gca::decode_list_scores(s, workspace),
+                                             gca::decode_list_chunks(s, workspace), q, k, v, idx, sel, out, lse,
+                                             w, stream),
+                    "gca_forward (decode attention)");
   } else if (fused_path(p, s)) {
     e = gca::launch_fused_select(s, lmk_q, lmk_k, idx, sel, workspace, stream);
   } else {

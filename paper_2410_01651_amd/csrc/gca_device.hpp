@@ -453,27 +453,103 @@ __device__ __forceinline__ void take_better(float& s, int& j, float os, int oj) 
     j = oj;
   }
 }
-__device__ __forceinline__ void wave_best(float& s, int& j) {
-  take_better(s, j, dpp<kDppXor1>(s), dpp<kDppXor1>(j));
-  take_better(s, j, dpp<kDppXor2>(s), dpp<kDppXor2>(j));
-  take_better(s, j, dpp<kDppRor4>(s), dpp<kDppRor4>(j));
-  take_better(s, j, dpp<kDppRor8>(s), dpp<kDppRor8>(j));
-  uint32_t s0, s1, j0, j1;
-  pair16(__float_as_uint(s), s0, s1);
-  pair16((uint32_t)j, j0, j1);
-  s = __uint_as_float(s0);
-  j = (int)j0;
-  take_better(s, j, __uint_as_float(s1), (int)j1);
-  pair32(__float_as_uint(s), s0, s1);
-  pair32((uint32_t)j, j0, j1);
-  s = __uint_as_float(s0);
-  j = (int)j0;
-  take_better(s, j, __uint_as_float(s1), (int)j1);
+
+// A candidate as one 64-bit key that orders like `better`: the score's bits made
+// order-preserving (sign bit set for non-negative scores, all bits flipped for
+// negative ones; -0 is taken as +0) above the complemented chunk index, so the
+// larger key is the better candidate and the empty entry (-inf, kNoChunk) is
+// below every real one.
+__device__ __forceinline__ uint64_t pack_key(float s, int j) {
+  uint32_t u = s == 0.f ? 0u : __float_as_uint(s);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)u << 32) | (uint64_t)(~(uint32_t)j);
+}
+__device__ __forceinline__ float key_score(uint64_t k) {
+  const uint32_t u = (uint32_t)(k >> 32);
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
+}
+__device__ __forceinline__ int key_chunk(uint64_t k) { return (int)~(uint32_t)k; }
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t x) {
+  return (uint64_t)dpp<CTRL>((uint32_t)x) | ((uint64_t)dpp<CTRL>((uint32_t)(x >> 32)) << 32);
+}
+__device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+// Wave-wide maximum key (every lane gets it).
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
+  k = umax64(k, dpp64<kDppXor1>(k));
+  k = umax64(k, dpp64<kDppXor2>(k));
+  k = umax64(k, dpp64<kDppRor4>(k));
+  k = umax64(k, dpp64<kDppRor8>(k));
+  uint32_t l0, l1, h0, h1;
+  pair16((uint32_t)k, l0, l1);
+  pair16((uint32_t)(k >> 32), h0, h1);
+  k = umax64((uint64_t)l0 | ((uint64_t)h0 << 32), (uint64_t)l1 | ((uint64_t)h1 << 32));
+  pair32((uint32_t)k, l0, l1);
+  pair32((uint32_t)(k >> 32), h0, h1);
+  return umax64((uint64_t)l0 | ((uint64_t)h0 << 32), (uint64_t)l1 | ((uint64_t)h1 << 32));
+}
+
+__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
+// x of lane l ^ 4 (within each 32-lane half): ds_swizzle in bit-mask mode,
+// lane l reads lane ((l & 31) ^ 4).
+__device__ __forceinline__ uint32_t swz_xor4(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (4 << 10));
+}
+
+// Bitonic sort of one key per lane across the wave, largest first: lane r
+// receives the r-th largest key.  Stage (size kk, distance j) pairs lane l with
+// l ^ j; inside a block whose bit kk is clear the lower lane keeps the larger
+// key, inside the others the smaller, so the final stage leaves one descending
+// run.  Distances 16 and 32 use the permlane swaps, which hand every lane both
+// keys of its pair, so the kept key is their max or min.
+__device__ __forceinline__ uint64_t wave_sort_desc(uint64_t k) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int kk = 2; kk <= 64; kk <<= 1) {
+#pragma unroll
+    for (int j = kk >> 1; j > 0; j >>= 1) {
+      const bool keep_max = ((lane & j) == 0) == ((lane & kk) == 0);
+      uint64_t a, b;
+      if (j == 16 || j == 32) {
+        uint32_t l0, l1, h0, h1;
+        if (j == 16) {
+          pair16((uint32_t)k, l0, l1);
+          pair16((uint32_t)(k >> 32), h0, h1);
+        } else {
+          pair32((uint32_t)k, l0, l1);
+          pair32((uint32_t)(k >> 32), h0, h1);
+        }
+        a = (uint64_t)l0 | ((uint64_t)h0 << 32);
+        b = (uint64_t)l1 | ((uint64_t)h1 << 32);
+      } else {
+        a = k;
+        if (j == 1) b = dpp64<kDppXor1>(k);
+        else if (j == 2) b = dpp64<kDppXor2>(k);
+        else if (j == 4) b = (uint64_t)swz_xor4((uint32_t)k) | ((uint64_t)swz_xor4((uint32_t)(k >> 32)) << 32);
+        else b = dpp64<kDppRor8>(k);  // j == 8: rotating a 16-lane row by 8 pairs l with l ^ 8
+      }
+      k = keep_max ? umax64(a, b) : umin64(a, b);
+    }
+  }
+  return k;
+}
+
+// The wave's best k (k <= 64) when every lane holds at most one candidate
+// (empty lanes pass -inf / kNoChunk), in wave_merge's form.
+__device__ __forceinline__ void wave_top_one(float s, int j, int k, float& my_s, int& my_j, int& count) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t key = wave_sort_desc(pack_key(s, j));
+  const bool real = key_chunk(key) != kNoChunk;
+  count = __popcll(__ballot(real && lane < k));
+  my_s = lane < count ? key_score(key) : -INFINITY;
+  my_j = lane < count ? key_chunk(key) : kNoChunk;
 }
 
 // Merge the 64 lanes' lists into the wave's best k (k <= 64).  Lane r < *count
 // receives the r-th best (score, chunk); *count <= k is the number of real
-// candidates.  Lists are consumed.
+// candidates.  Lists are consumed.  Each round takes the wave's best list head
+// as one 64-bit maximum.
 template <int KM>
 __device__ __forceinline__ void wave_merge(TopList<KM>& L, int k, float& my_s, int& my_j, int& count) {
   const int lane = threadIdx.x & 63;
@@ -481,14 +557,118 @@ __device__ __forceinline__ void wave_merge(TopList<KM>& L, int k, float& my_s, i
   my_j = kNoChunk;
   count = 0;
   for (int r = 0; r < k; ++r) {
-    float bs = L.s[0];
-    int bj = L.j[0];
-    wave_best(bs, bj);
+    const uint64_t own = pack_key(L.s[0], L.j[0]);
+    const uint64_t best = wave_max_key(own);
+    const int bj = key_chunk(best);
     if (bj == kNoChunk) break;
-    if (L.j[0] == bj) L.pop();
-    if (lane == r) { my_s = bs; my_j = bj; }
+    if (own == best) L.pop();
+    if (lane == r) {
+      my_s = key_score(best);
+      my_j = bj;
+    }
     ++count;
   }
+}
+
+// Merge of NW waves' results (lane r < cnt: the wave's r-th best, r < 32) by
+// wave 0, which receives the workgroup's best (<= K <= 32) as wave_merge leaves
+// it.  sS/sJ hold NW * 32 entries, sCnt NW.  Contains a workgroup barrier.
+template <int KM, int NW>
+__device__ __forceinline__ void merge_wave_results(int K, float* sS, int* sJ, int* sCnt, float& ms, int& mj,
+                                                   int& cnt) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane < 32) {
+    sS[wave * 32 + lane] = ms;
+    sJ[wave * 32 + lane] = mj;
+  }
+  if (lane == 0) sCnt[wave] = cnt;
+  __syncthreads();
+  if (wave == 0) {
+    if (NW * K <= 64) {
+      // one candidate per lane: lane l takes entry l % K of wave l / K
+      const int w = lane / K, r = lane - w * K;
+      const bool has = w < NW && r < sCnt[w < NW ? w : 0];
+      const int at = has ? w * 32 + r : 0;
+      const float cs = sS[at];
+      const int cj = sJ[at];
+      wave_top_one(has ? cs : -INFINITY, has ? cj : kNoChunk, K, ms, mj, cnt);
+    } else {
+      TopList<KM> L;
+      L.init();
+#pragma unroll
+      for (int w0 = 0; w0 < NW; w0 += 2) {
+        const int w = w0 + (lane >> 5);  // lanes 0-31 take wave w0, lanes 32-63 wave w0 + 1
+        if (w < NW && (lane & 31) < sCnt[w]) L.insert(sS[w * 32 + (lane & 31)], sJ[w * 32 + (lane & 31)]);
+      }
+      wave_merge(L, K, ms, mj, cnt);
+    }
+  }
+}
+
+// Best k (<= 32) of one retrieval row from per-range lists: list l (of `lists`)
+// holds the best k of chunks [l * pw, (l + 1) * pw), sorted best first and
+// padded with chunk -1, at ls/lj[(row * lists + l) * K ..].  Every wave takes a
+// contiguous share of the lists and the best k of their maxima; an entry of the
+// row's top k can only sit in a list whose maximum is among the k best of its
+// share (k better maxima would all beat it), so the wave merges the k-lists of
+// those lists, and wave 0 merges the waves' results.  Result in wave 0 as
+// wave_merge leaves it.  Scratch: sS/sJ/sCnt as merge_wave_results.
+template <int KM, int NW>
+__device__ void merge_lists(const float* __restrict__ ls, const int* __restrict__ lj, int64_t row, int64_t lists,
+                            int64_t pw, int K, float* sS, int* sJ, int* sCnt, float& ms, int& mj, int& cnt) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float* rs = ls + row * lists * K;
+  const int* rj = lj + row * lists * K;
+  const int64_t share = (lists + NW - 1) / NW;
+  const int64_t l_lo = wave * share, l_hi = l_lo + share < lists ? l_lo + share : lists;
+  TopList<KM> L;
+  L.init();
+  // 1. the share's list maxima, four loads per lane in flight
+  for (int64_t l0 = l_lo; l0 < l_hi; l0 += 256) {
+    float v[4];
+    int j[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t l = l0 + 64 * u + lane;
+      const int64_t lc = l < l_hi ? l : l_lo;
+      v[u] = rs[lc * K];
+      j[u] = l < l_hi ? rj[lc * K] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (j[u] >= 0) L.insert(v[u], j[u]);
+  }
+  wave_merge(L, K, ms, mj, cnt);
+  // 2. the k entries of each list they head (entry e: list e / K, rank e % K)
+  const int ne = cnt * K;
+  if (K * K <= 64) {
+    float cs = -INFINITY;
+    int cj = kNoChunk;
+    const int src = lane / K;
+    const int head = __shfl(mj, src);  // every lane takes part in the exchange
+    if (lane < ne) {
+      const int64_t l = (int64_t)head / pw;
+      const int64_t off = l * K + (lane - src * K);
+      const int jj = rj[off];
+      if (jj >= 0) {
+        cs = rs[off];
+        cj = jj;
+      }
+    }
+    wave_top_one(cs, cj, K, ms, mj, cnt);
+  } else {
+    L.init();
+    for (int e = lane; e < ne; e += 64) {
+      const int src = e / K;
+      const int64_t l = (int64_t)__shfl(mj, src) / pw;
+      const int64_t off = l * K + (e - src * K);
+      const int jj = rj[off];
+      if (jj >= 0) L.insert(rs[off], jj);
+    }
+    wave_merge(L, K, ms, mj, cnt);
+  }
+  // 3. across the waves
+  merge_wave_results<KM, NW>(K, sS, sJ, sCnt, ms, mj, cnt);
 }
 
 // Position of lane r's chunk among the first `count` lanes' chunks in

@@ -25,10 +25,25 @@ hipError_t launch_chunk_scores(const Shape& s, const void* lmk_q, const void* lm
 // Eq. 1 top-k over a score matrix.
 hipError_t launch_topk(const Shape& s, const float* scores, int32_t* idx, float* sel,
                        hipStream_t stream);
-// Decode: split scan of all past landmark keys, then merge into idx/sel.
+// Decode selection, first half: a split scan of all past landmark keys (Eq. 1)
+// that leaves, for every retrieval row, `lists` lists of the best k of `pw`
+// consecutive chunks each (in the workspace).  The decode attention merges them.
+struct DecodePlan {
+  int64_t pw;     // chunks per list (one scan wave's contiguous range)
+  int64_t lists;  // lists per retrieval row
+  int64_t wgs;    // scan workgroups per row
+};
+DecodePlan decode_plan(const Shape& s);
 size_t decode_workspace(const Shape& s);
-hipError_t launch_decode_select(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx,
-                                float* sel, void* ws, hipStream_t stream);
+float* decode_list_scores(const Shape& s, void* ws);
+int* decode_list_chunks(const Shape& s, void* ws);
+hipError_t launch_decode_scan(const Shape& s, const void* lmk_q, const void* lmk_k, void* ws, hipStream_t stream);
+// Decode attention (Eq. 2-3 for the one query chunk of every (batch, head)).
+// With lists (list_s != null) it first merges them into the row's top-k and
+// writes idx/sel; without, idx/sel are its inputs.
+hipError_t launch_xattn_decode(const Shape& s, const float* list_s, const int* list_j, const void* q,
+                               const void* k, const void* v, int32_t* idx, float* sel, void* out, float* lse,
+                               float* w, hipStream_t stream);
 // Causal: scores and top-k in one pass, no score matrix.
 size_t fused_workspace(const Shape& s);
 hipError_t launch_fused_select(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx,

@@ -8,11 +8,11 @@
 //   columns it visits, and the 64 lists are merged k times with a wave-wide
 //   lexicographic (score desc, chunk asc) reduction.  The chosen chunks are
 //   then written in ascending chunk order.
-// decode select: one landmark query against every past landmark key.  The
-//   keys are read once, coalesced, by many workgroups that each own a slice;
-//   8 lanes share one key row (16 bytes each per step) and reduce the dot
-//   product with two cross-lane steps.  Each workgroup leaves its slice's best
-//   k in the workspace and one workgroup per row merges them.
+// decode scan: one landmark query against every past landmark key.  The keys
+//   are streamed once, coalesced, by ~512 workgroups whose waves each own a
+//   contiguous range; 8 lanes share one key row and reduce the dot product
+//   with three cross-lane steps.  Each wave leaves its range's best k in the
+//   workspace; the decode attention kernel merges them (xattn_decode.hip).
 #include "gca_device.hpp"
 #include "gca_launch.hpp"
 
@@ -97,208 +97,163 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ sco
   write_sorted<KM>(idx + row * K, sel + row * K, K, ms, mj, cnt);
 }
 
-// ------------------------------------------------------- decode select ----
+// ------------------------------------------------------- decode scan ----
 
 constexpr int kScanThreads = 256;
-constexpr int kMaxScanSlices = 1024;
+constexpr int kScanWaves = kScanThreads / 64;
+constexpr int kScanBatch = 8;  // column blocks per lane in one batch of loads
 
-struct ScanPlan {
-  int64_t per;     // keys per slice
-  int64_t slices;  // slices per retrieval row
-};
+// Buffer descriptor over `bytes` bytes from `base` (wave-uniform): reads at
+// offsets past the end return zero and touch no memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t range_rsrc(const char* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, (int)bytes, 0x00020000);
+}
+constexpr int kLoadNonTemporal = 2;  // cache policy: streamed once
 
-// 8-element dot product accumulated in fp32 (bf16 products are exact in fp32).
-__device__ __forceinline__ float dot8(const bf16x8& a, const bf16x8& b, float acc) {
-#pragma unroll
-  for (int m = 0; m < 8; ++m) acc = fmaf((float)a[m], (float)b[m], acc);
+// Partial dot product of one lane's 8 elements of a key column block with the
+// query's (both 16 bytes of bf16, or 32 bytes of fp32 as two records).
+__device__ __forceinline__ float dot_block(const u32x4* v, const __bf16* q, float acc) {
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+  const bf16x8 a = __builtin_bit_cast(bf16x8, v[0]);
+  const bf16x8 b = load_frag(q);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 0, 1), __builtin_shufflevector(b, b, 0, 1),
+                                        acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 2, 3), __builtin_shufflevector(b, b, 2, 3),
+                                        acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 4, 5), __builtin_shufflevector(b, b, 4, 5),
+                                        acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 6, 7), __builtin_shufflevector(b, b, 6, 7),
+                                        acc, false);
   return acc;
 }
-__device__ __forceinline__ float dot8(const f32x8& a, const f32x8& b, float acc) {
-  acc = fmaf(a.lo[0], b.lo[0], acc); acc = fmaf(a.lo[1], b.lo[1], acc);
-  acc = fmaf(a.lo[2], b.lo[2], acc); acc = fmaf(a.lo[3], b.lo[3], acc);
-  acc = fmaf(a.hi[0], b.hi[0], acc); acc = fmaf(a.hi[1], b.hi[1], acc);
-  acc = fmaf(a.hi[2], b.hi[2], acc); acc = fmaf(a.hi[3], b.hi[3], acc);
+__device__ __forceinline__ float dot_block(const u32x4* v, const float* q, float acc) {
+  const f32x8 b = load_frag(q);
+  const f32x4 a0 = __builtin_bit_cast(f32x4, v[0]), a1 = __builtin_bit_cast(f32x4, v[1]);
+#pragma unroll
+  for (int m = 0; m < 4; ++m) acc = fmaf(a0[m], b.lo[m], acc);
+#pragma unroll
+  for (int m = 0; m < 4; ++m) acc = fmaf(a1[m], b.hi[m], acc);
   return acc;
 }
 
-ScanPlan scan_plan(int64_t nC) {
-  int64_t per = (nC + kMaxScanSlices - 1) / kMaxScanSlices;
-  if (per < 256) per = 256;
-  per = (per + 31) & ~int64_t(31);
-  ScanPlan p;
-  p.per = per;
-  p.slices = (nC + per - 1) / per;
-  return p;
-}
-
-// Wave-level merge, then merge of the workgroup's NW wave results by wave 0.
-// Leaves the workgroup's best (<= K) in lanes of wave 0: (ms, mj), cnt.
-// sS/sJ hold NW * 32 entries, sCnt NW.
-template <int KM, int NW>
-__device__ __forceinline__ void block_merge(TopList<KM>& L, int K, float* sS, int* sJ, int* sCnt, float& ms,
-                                            int& mj, int& cnt) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  wave_merge(L, K, ms, mj, cnt);
-  if (lane < 32) {
-    sS[wave * 32 + lane] = ms;
-    sJ[wave * 32 + lane] = mj;
-  }
-  if (lane == 0) sCnt[wave] = cnt;
-  __syncthreads();
-  if (wave == 0) {
-    L.init();
-#pragma unroll
-    for (int w0 = 0; w0 < NW; w0 += 2) {
-      const int w = w0 + (lane >> 5);  // lanes 0-31 take wave w0, lanes 32-63 wave w0 + 1
-      if (w < NW && (lane & 31) < sCnt[w]) L.insert(sS[w * 32 + (lane & 31)], sJ[w * 32 + (lane & 31)]);
-    }
-    wave_merge(L, K, ms, mj, cnt);
-  }
-}
-
+// Every wave scans one contiguous range of `pw` landmark keys of its row and
+// leaves that range's best k (sorted best first, padded with chunk -1) as list
+// number (workgroup * 4 + wave) of the row.  8 lanes share a key: lane
+// 8m + s reads bytes 16 s .. 16 s + 15 (bf16) of every 128-byte column block of
+// key m of the current group of 8 keys, so one load instruction covers 8 keys x
+// 128 contiguous bytes.  Loads are streamed (non-temporal) through a buffer
+// descriptor per key group, whose range check zeroes the lanes past the end of
+// the wave's range with no memory access, and run one batch of 8 column blocks
+// ahead of the arithmetic.
 template <typename T, int KM>
 __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __restrict__ lq,
                                                                    const T* __restrict__ lk, float* __restrict__ cs,
                                                                    int* __restrict__ cj, int64_t nC, int D,
-                                                                   float scale, int K, int64_t per,
-                                                                   int64_t slices) {
+                                                                   float scale, int K, int64_t pw, int64_t lists,
+                                                                   int64_t wgs) {
+  constexpr int LPS = (int)sizeof(T) / 2;  // 16-byte records per lane per column block
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   T* sq = reinterpret_cast<T*>(smem);
-  __shared__ float sS[kScanThreads / 64 * 32];
-  __shared__ int sJ[kScanThreads / 64 * 32];
-  __shared__ int sCnt[kScanThreads / 64];
 
-  const int64_t g = blockIdx.x % slices;
-  const int64_t bhr = blockIdx.x / slices;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, sub = lane & 7;
-  const T* q = lq + bhr * D;  // the one landmark query of this row
+  const int64_t row = blockIdx.x / wgs, g = blockIdx.x % wgs;
+  const int tid = threadIdx.x, lane = tid & 63, sub = lane & 7, kl = lane >> 3;
+  const T* q = lq + row * D;  // the one landmark query of this row
   for (int x = tid * (16 / (int)sizeof(T)); x < D; x += kScanThreads * (16 / (int)sizeof(T)))
     *reinterpret_cast<u32x4*>(sq + x) = *reinterpret_cast<const u32x4*>(q + x);
   __syncthreads();
 
-  const int64_t lo = g * per;
-  const int64_t hi = lo + per < nC ? lo + per : nC;
-  TopList<KM> L;
-  L.init();
-  // a wave scores two groups of 8 keys per round (lane: key lane/8, 16-byte
-  // column block lane%8 of every 128 bytes), so 2 * D/64 loads are in flight
-  constexpr int kWaves = kScanThreads / 64;
-  int it = 0;
-  for (int64_t base = lo + wave * 16; base < hi; base += 16 * kWaves, it += 2) {
-    const int64_t key0 = base + (lane >> 3), key1 = key0 + 8;
-    const T* kr0 = lk + (bhr * nC + (key0 < hi ? key0 : lo)) * D;
-    const T* kr1 = lk + (bhr * nC + (key1 < hi ? key1 : lo)) * D;
-    float acc0 = 0.f, acc1 = 0.f;
-#pragma unroll 4
-    for (int x = sub * 8; x < D; x += 64) {
-      const Frag<T> a0 = load_frag(kr0 + x);
-      const Frag<T> a1 = load_frag(kr1 + x);
-      const Frag<T> b = load_frag(sq + x);
-      acc0 = dot8(a0, b, acc0);
-      acc1 = dot8(a1, b, acc1);
-    }
-    // sum over the key's 8 lanes (lanes 8m .. 8m+7: quad swaps, then the other quad)
-    acc0 += dpp<kDppXor1>(acc0);
-    acc1 += dpp<kDppXor1>(acc1);
-    acc0 += dpp<kDppXor2>(acc0);
-    acc1 += dpp<kDppXor2>(acc1);
-    acc0 += dpp<kDppHalfMirror>(acc0);
-    acc1 += dpp<kDppHalfMirror>(acc1);
-    // spread the insertions of one key group over its 8 lanes
-    if (key0 < hi && sub == (it & 7)) {
-      const float v = acc0 * scale;
-      if (__builtin_isfinite(v)) L.insert(v, (int)key0);
-    }
-    if (key1 < hi && sub == ((it + 1) & 7)) {
-      const float v = acc1 * scale;
-      if (__builtin_isfinite(v)) L.insert(v, (int)key1);
-    }
-  }
-  float ms;
-  int mj, cnt;
-  block_merge<KM, kScanThreads / 64>(L, K, sS, sJ, sCnt, ms, mj, cnt);
-  if (wave == 0 && lane < K) {
-    const int64_t o = (bhr * slices + g) * K + lane;
-    cs[o] = lane < cnt ? ms : -INFINITY;
-    cj[o] = lane < cnt ? mj : -1;
-  }
-}
+  const int64_t list = uniform64(g * kScanWaves + (tid >> 6));
+  if (list >= lists) return;
+  const int64_t lo = list * pw;
+  const int64_t n = pw < nC - lo ? pw : nC - lo;  // keys in this wave's range (>= 1)
+  const int NB = D / 64;                          // column blocks per key
+  const int64_t KB = (int64_t)D * sizeof(T);      // bytes per key
+  const int64_t ngroups = (n + 7) / 8;
+  const int64_t nsteps = ngroups * NB;
+  const int64_t nbatch = (nsteps + kScanBatch - 1) / kScanBatch;
+  const char* const wbase = reinterpret_cast<const char*>(lk + (row * nC + lo) * D);
+  const uint32_t lane_off = (uint32_t)(kl * KB) + (uint32_t)(sub * 16 * LPS);
 
-constexpr int kMergeThreads = 1024;
-
-// Final top-k of one row from the slices' lists (each sorted best first).  The
-// k-th best slice maximum T is a lower bound for the row's k-th best, so only
-// candidates at or above T can win, and they come from the k slices whose
-// maximum is at or above T: at most k * k candidates.  One pass finds T from
-// the slice maxima, one pass gathers the candidates into LDS, one wave merges
-// them.
-template <int KM>
-__global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(const float* __restrict__ cs,
-                                                                     const int* __restrict__ cj,
-                                                                     int32_t* __restrict__ idx,
-                                                                     float* __restrict__ sel, int K,
-                                                                     int64_t slices) {
-  constexpr int NW = kMergeThreads / 64;
-  constexpr int kMaxCand = 32 * 32;
-  __shared__ float sS[NW * 32];
-  __shared__ int sJ[NW * 32];
-  __shared__ int sCnt[NW];
-  __shared__ float sCs[kMaxCand];
-  __shared__ int sCj[kMaxCand];
-  __shared__ int sNc;
-  __shared__ float sTs;
-  __shared__ int sTj;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t bhr = blockIdx.x;
-  const int64_t n = slices * K;
-  const float* c_s = cs + bhr * n;
-  const int* c_j = cj + bhr * n;
-
-  // 1. the threshold: k-th best of the slice maxima (slices <= kMergeThreads)
-  TopList<KM> L;
-  L.init();
-  if (tid < slices) {
-    const int j = c_j[(int64_t)tid * K];
-    if (j >= 0) L.insert(c_s[(int64_t)tid * K], j);
-  }
-  float ms;
-  int mj, cnt;
-  block_merge<KM, NW>(L, K, sS, sJ, sCnt, ms, mj, cnt);
-  if (wave == 0) {
-    const float ts = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ms), K - 1));
-    const int tj = __builtin_amdgcn_readlane(mj, K - 1);
-    if (lane == 0) {
-      sTs = cnt >= K ? ts : -INFINITY;  // fewer than k maxima: every candidate qualifies
-      sTj = cnt >= K ? tj : kNoChunk;
-      sNc = 0;
-    }
-  }
-  __syncthreads();
-
-  // 2. gather the candidates at or above the threshold
-  const float ts = sTs;
-  const int tj = sTj;
-  for (int64_t e = tid; e < n; e += kMergeThreads) {
-    const int j = c_j[e];
-    if (j < 0) continue;
-    const float v = c_s[e];
-    if (!better(ts, tj, v, j)) {
-      const int pos = atomicAdd(&sNc, 1);
-      if (pos < kMaxCand) {
-        sCs[pos] = v;
-        sCj[pos] = j;
+  // issue cursor: key group ig, column block icb, and the group's descriptor
+  int64_t ig = 0;
+  int icb = 0;
+  auto rsrc_of = [&](int64_t gi) {
+    const int64_t left = (n - 8 * gi) * KB;
+    const uint32_t bytes = left <= 0 ? 0u : (uint32_t)(left < 8 * KB ? left : 8 * KB);
+    return range_rsrc(wbase + gi * 8 * KB, bytes);
+  };
+  __amdgpu_buffer_rsrc_t rs = rsrc_of(0);
+  auto issue = [&](u32x4* v) {
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) {
+#pragma unroll
+      for (int e = 0; e < LPS; ++e)
+        v[k * LPS + e] = __builtin_amdgcn_raw_buffer_load_b128(rs, lane_off + 16 * e,
+                                                               icb * 64 * (int)sizeof(T), kLoadNonTemporal);
+      if (++icb == NB) {
+        icb = 0;
+        ++ig;
+        rs = rsrc_of(ig);
       }
     }
-  }
-  __syncthreads();
+  };
 
-  // 3. one wave merges them
-  if (wave == 0) {
-    const int nc = min(sNc, kMaxCand);
-    L.init();
-    for (int i = lane; i < nc; i += 64) L.insert(sCs[i], sCj[i]);
-    wave_merge(L, K, ms, mj, cnt);
-    write_sorted<KM>(idx + bhr * K, sel + bhr * K, K, ms, mj, cnt);
+  // compute cursor
+  int64_t cg = 0;
+  int ccb = 0;
+  float acc = 0.f;
+  TopList<KM> L;
+  L.init();
+  auto consume = [&](const u32x4* v, int64_t step0) {
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) {
+      if (step0 + k < nsteps) {
+        acc = dot_block(v + k * LPS, sq + ccb * 64 + sub * 8, acc);
+        if (++ccb == NB) {
+          // sum over the key's 8 lanes (quad swaps, then the other quad)
+          acc += dpp<kDppXor1>(acc);
+          acc += dpp<kDppXor2>(acc);
+          acc += dpp<kDppHalfMirror>(acc);
+          const int64_t key = 8 * cg + kl;
+          // one of the key's 8 lanes inserts it, rotating with the group
+          if (key < n && sub == (int)(cg & 7)) {
+            const float sv = acc * scale;
+            if (__builtin_isfinite(sv)) L.insert(sv, (int)(lo + key));
+          }
+          acc = 0.f;
+          ccb = 0;
+          ++cg;
+        }
+      }
+    }
+  };
+
+  // two register batches alternate: batch b + 1 is in flight while batch b is
+  // consumed; the loop body issues unconditionally so the waits stay exact
+  u32x4 va[kScanBatch * LPS], vb[kScanBatch * LPS];
+  issue(va);
+  int64_t bt = 0;
+  for (; bt + 2 < nbatch; bt += 2) {
+    issue(vb);
+    consume(va, bt * kScanBatch);
+    issue(va);
+    consume(vb, (bt + 1) * kScanBatch);
+  }
+  if (bt + 1 < nbatch) {
+    issue(vb);
+    consume(va, bt * kScanBatch);
+    consume(vb, (bt + 1) * kScanBatch);
+  } else {
+    consume(va, bt * kScanBatch);
+  }
+
+  float ms;
+  int mj, cnt;
+  wave_merge(L, K, ms, mj, cnt);
+  if (lane < K) {
+    const int64_t o = (row * lists + list) * K + lane;
+    cs[o] = lane < cnt ? ms : -INFINITY;
+    cj[o] = lane < cnt ? mj : -1;
   }
 }
 
@@ -425,23 +380,16 @@ hipError_t launch_topk_k(const Shape& s, const float* scores, int32_t* idx, floa
 }
 
 template <typename T, int KM>
-hipError_t launch_decode_k(const Shape& s, const void* lq, const void* lk, int32_t* idx, float* sel, void* ws,
-                           hipStream_t st) {
-  const ScanPlan plan = scan_plan(s.nKV);
+hipError_t launch_scan_k(const Shape& s, const void* lq, const void* lk, void* ws, hipStream_t st) {
+  const DecodePlan plan = decode_plan(s);
   const int64_t rows = (int64_t)s.B * s.Hr;
-  float* cs = reinterpret_cast<float*>(ws);
-  int* cj = reinterpret_cast<int*>(reinterpret_cast<char*>(ws) +
-                                   align256(sizeof(float) * rows * plan.slices * s.topk));
+  float* cs = decode_list_scores(s, ws);
+  int* cj = decode_list_chunks(s, ws);
   const size_t smem = (size_t)s.D * sizeof(T);
-  hipLaunchKernelGGL((decode_scan_kernel<T, KM>), dim3((unsigned)(rows * plan.slices)), dim3(kScanThreads), smem,
-                     st, (const T*)lq, (const T*)lk, cs, cj, s.nKV, s.D, s.score_scale, s.topk, plan.per,
-                     plan.slices);
+  hipLaunchKernelGGL((decode_scan_kernel<T, KM>), dim3((unsigned)(rows * plan.wgs)), dim3(kScanThreads), smem, st,
+                     (const T*)lq, (const T*)lk, cs, cj, s.nKV, s.D, s.score_scale, s.topk, plan.pw, plan.lists,
+                     plan.wgs);
   note_launch("decode_scan_kernel", st);
-  const hipError_t e = take_launch_error();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(decode_merge_kernel<KM>, dim3((unsigned)rows), dim3(kMergeThreads), 0, st, cs, cj, idx, sel, s.topk,
-                     plan.slices);
-  note_launch("decode_merge_kernel", st);
   return take_launch_error();
 }
 
@@ -459,22 +407,41 @@ hipError_t launch_topk(const Shape& s, const float* scores, int32_t* idx, float*
   return launch_topk_k<32>(s, scores, idx, sel, stream);
 }
 
-size_t decode_workspace(const Shape& s) {
-  const ScanPlan plan = scan_plan(s.nKV);
-  const size_t n = (size_t)s.B * s.Hr * plan.slices * s.topk;
-  return align256(n * sizeof(float)) + align256(n * sizeof(int));
+DecodePlan decode_plan(const Shape& s) {
+  // about 512 scan workgroups in all (two per CU), every wave one contiguous
+  // range of at least 64 keys
+  const int64_t rows = (int64_t)s.B * s.Hr;
+  int64_t wgs = 512 / rows;
+  if (wgs < 1) wgs = 1;
+  int64_t pw = (s.nKV + wgs * kScanWaves - 1) / (wgs * kScanWaves);
+  if (pw < 64) pw = 64;
+  pw = (pw + 7) & ~int64_t(7);
+  DecodePlan p;
+  p.pw = pw;
+  p.lists = (s.nKV + pw - 1) / pw;
+  p.wgs = (p.lists + kScanWaves - 1) / kScanWaves;
+  return p;
 }
 
-hipError_t launch_decode_select(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx, float* sel,
-                                void* ws, hipStream_t stream) {
+size_t decode_workspace(const Shape& s) {
+  const size_t n = (size_t)s.B * s.Hr * decode_plan(s).lists * s.topk;
+  return align256(n * sizeof(float)) + align256(n * sizeof(int));
+}
+float* decode_list_scores(const Shape&, void* ws) { return reinterpret_cast<float*>(ws); }
+int* decode_list_chunks(const Shape& s, void* ws) {
+  const size_t n = (size_t)s.B * s.Hr * decode_plan(s).lists * s.topk;
+  return reinterpret_cast<int*>(reinterpret_cast<char*>(ws) + align256(n * sizeof(float)));
+}
+
+hipError_t launch_decode_scan(const Shape& s, const void* lmk_q, const void* lmk_k, void* ws, hipStream_t stream) {
   if (s.bf16) {
-    if (s.topk <= 8) return launch_decode_k<__bf16, 8>(s, lmk_q, lmk_k, idx, sel, ws, stream);
-    if (s.topk <= 16) return launch_decode_k<__bf16, 16>(s, lmk_q, lmk_k, idx, sel, ws, stream);
-    return launch_decode_k<__bf16, 32>(s, lmk_q, lmk_k, idx, sel, ws, stream);
+    if (s.topk <= 8) return launch_scan_k<__bf16, 8>(s, lmk_q, lmk_k, ws, stream);
+    if (s.topk <= 16) return launch_scan_k<__bf16, 16>(s, lmk_q, lmk_k, ws, stream);
+    return launch_scan_k<__bf16, 32>(s, lmk_q, lmk_k, ws, stream);
   }
-  if (s.topk <= 8) return launch_decode_k<float, 8>(s, lmk_q, lmk_k, idx, sel, ws, stream);
-  if (s.topk <= 16) return launch_decode_k<float, 16>(s, lmk_q, lmk_k, idx, sel, ws, stream);
-  return launch_decode_k<float, 32>(s, lmk_q, lmk_k, idx, sel, ws, stream);
+  if (s.topk <= 8) return launch_scan_k<float, 8>(s, lmk_q, lmk_k, ws, stream);
+  if (s.topk <= 16) return launch_scan_k<float, 16>(s, lmk_q, lmk_k, ws, stream);
+  return launch_scan_k<float, 32>(s, lmk_q, lmk_k, ws, stream);
 }
 
 size_t fused_workspace(const Shape&) { return 0; }

@@ -2,14 +2,18 @@
 
     python -m paper_2410_01651_amd.profiling stats   --csv DIR/run_kernel_stats.csv --cmd "..." --out profiles/X.md
     python -m paper_2410_01651_amd.profiling traffic --fetch DIR1/run_counter_collection.csv \
-        --write DIR2/run_counter_collection.csv --copy-bytes N --cmd "..." --out profiles/hbm_traffic.json
+        --write DIR2/run_counter_collection.csv --copy-bytes N --cmd "..." --out profiles/hbm_traffic.json \
+        [--tag WORKLOAD --append]
 
 `traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
 launch for every GCA kernel, scaled by what the same counters read for a plain
 device copy of N bytes in the same run (the copy kernel is the dispatch whose
 name contains "copy").  The result records a hash of the kernel sources, so a
 reader (bench.py) can tell when the kernels have changed since the counters
-were taken.
+were taken.  `--tag` suffixes the kernel names with "@WORKLOAD" (a kernel that
+runs in two workloads, such as the cross attention at 64K training and at 16M
+decode, is then kept apart) and `--append` adds the result to an existing file
+taken from the same sources.
 """
 
 import argparse
@@ -36,7 +40,7 @@ def source_hash() -> str:
 
 def short_name(kernel: str) -> str:
     for key in ("xattn_fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel", "chunk_scores_kernel", "topk_kernel",
-                "fused_select_kernel", "decode_scan_kernel", "decode_merge_kernel", "weights_kernel",
+                "fused_select_kernel", "decode_scan_kernel", "decode_merge_kernel", "xattn_decode_kernel", "weights_kernel",
                 "fill_zero_kernel", "csr_count_kernel", "csr_scan_kernel", "csr_fill_kernel", "csr_sort_kernel",
                 "dsel_kernel", "dlmk_q_kernel", "dlmk_k_kernel"):
         if key in kernel:
@@ -87,7 +91,7 @@ def _per_kernel(counter_csv: str, counter: str):
     return vals
 
 
-def traffic(fetch_csv: str, write_csv: str, copy_bytes: int, cmd: str) -> dict:
+def traffic(fetch_csv: str, write_csv: str, copy_bytes: int, cmd: str, tag: str = "") -> dict:
     f = _per_kernel(fetch_csv, "FETCH_SIZE")
     w = _per_kernel(write_csv, "WRITE_SIZE")
     if "copy" not in f or "copy" not in w:
@@ -99,13 +103,13 @@ def traffic(fetch_csv: str, write_csv: str, copy_bytes: int, cmd: str) -> dict:
     for k in sorted(set(f) & set(w)):
         if k == "copy":
             continue
-        kernels[k] = {
+        kernels[k + ("@" + tag if tag else "")] = {
             "fetch_bytes_per_launch": statistics.median(f[k]) * 1024.0 * f_scale,
             "write_bytes_per_launch": statistics.median(w[k]) * 1024.0 * w_scale,
             "dispatches": len(f[k]),
         }
     return {"source_sha256": source_hash(), "copy_bytes": copy_bytes,
-            "fetch_scale": f_scale, "write_scale": w_scale, "command": cmd, "kernels": kernels}
+            "fetch_scale": f_scale, "write_scale": w_scale, "command": [cmd], "kernels": kernels}
 
 
 def main():
@@ -122,6 +126,8 @@ def main():
     b.add_argument("--copy-bytes", type=int, required=True)
     b.add_argument("--cmd", required=True)
     b.add_argument("--out", required=True)
+    b.add_argument("--tag", default="")
+    b.add_argument("--append", action="store_true")
     args = ap.parse_args()
     if args.what == "stats":
         text = stats_md(args.csv, args.cmd)
@@ -131,7 +137,15 @@ def main():
             text += "\n" + trace_md(trace, args.cmd)
         open(args.out, "w").write(text)
     else:
-        data = traffic(args.fetch, args.write, args.copy_bytes, args.cmd)
+        data = traffic(args.fetch, args.write, args.copy_bytes, args.cmd, args.tag)
+        if args.append:
+            old = json.load(open(args.out))
+            if old.get("source_sha256") != data["source_sha256"]:
+                raise SystemExit(f"{args.out} was taken from other kernel sources")
+            old["command"] = list(old["command"]) + data["command"]
+            old["kernels"].update(data["kernels"])
+            old.setdefault("scales", {})[args.tag or "-"] = [data["fetch_scale"], data["write_scale"]]
+            data = old
         json.dump(data, open(args.out, "w"), indent=1)
     print(args.out)
 

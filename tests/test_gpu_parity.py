@@ -124,6 +124,13 @@ SWEEP = [
     ("decode_16m_bf16", dict(H=4, n_chunks=3000, device_kv=False), False),
     ("decode_16m_bf16", dict(H=2, n_chunks=500, topk=32, dtype="fp32", device_kv=False), True),
     ("decode_16m_bf16", dict(H=2, Hr=2, D=64, n_chunks=5, topk=8, device_kv=False), False),
+    # decode scan ranges: a ragged last key group, 16 and 1 column blocks per key,
+    # fp32 with 3 blocks per key, several retrieval rows
+    ("decode_16m_bf16", dict(H=2, n_chunks=20001, device_kv=False), False),
+    ("decode_16m_bf16", dict(H=2, D=1024, n_chunks=1001, topk=5, device_kv=False), True),
+    ("decode_16m_bf16", dict(H=2, Hr=2, D=64, n_chunks=777, device_kv=False), False),
+    ("decode_16m_bf16", dict(H=1, D=192, n_chunks=999, topk=3, dtype="fp32", device_kv=False), False),
+    ("decode_16m_bf16", dict(B=3, H=2, n_chunks=4000, topk=16, device_kv=False), False),
 ]
 
 
@@ -248,3 +255,39 @@ def test_xattn_only_entry_points(dev):
     dq, dk, dv, dw = og.xattn_bwd(x["q"], x["k"], x["v"], idx_ref, w_ref, x["dout"], w.S, w.attn_scale)
     for key, ref in (("dq", dq), ("dk", dk), ("dv", dv), ("dsel", og.dsel_from_dw(w_ref, dw))):
         assert max_abs_rel(host64(g[key]), ref) <= 1e-4, key
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_decode_xattn_only_entry_point(dev, dtype):
+    """gca_grouped_xattn_fwd in decode mode with an index set chosen by the caller:
+    pads between valid slots, an out-of-range index (a pad), and a row with no
+    valid slot at all."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w = get_workload("decode_16m_bf16", B=2, H=2, Hr=2, D=64, n_chunks=30, topk=6, dtype=dtype, planted=0,
+                     device_kv=False)
+    inp = gi.draw_tokens(w)
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    k = w.topk
+    idx = np.full((2, 2, 1, k), -1, np.int32)
+    sel = np.full((2, 2, 1, k), -np.inf, np.float32)
+    rng = np.random.default_rng(11)
+    for b, hr, slots in ((0, 0, [0, 2, 5]), (0, 1, [1, 2, 3, 4]), (1, 0, [3])):
+        for s, j in zip(slots, sorted(rng.choice(w.n_chunks, size=len(slots), replace=False))):
+            idx[b, hr, 0, s] = j
+            sel[b, hr, 0, s] = rng.standard_normal()
+    idx[0, 1, 0, 3] = 1000            # out of range -> pad
+    # row (1, 1) keeps no valid slot
+    ti, ts = torch.from_numpy(idx).to(dev), torch.from_numpy(sel).to(dev)
+    out, lse, wt = gca.grouped_xattn_fwd(p, t["q"], t["k"], t["v"], ti, ts)
+    x = decode_all(w, inp)
+    idx_ref = np.where(idx >= w.n_chunks, -1, idx)
+    sel_ref = np.where(idx >= w.n_chunks, -np.inf, sel).astype(np.float64)
+    w_ref = og.fusion_weights(sel_ref)
+    o_ref, l_ref = og.xattn_fwd(x["q"], x["k"], x["v"], idx_ref, w_ref, w.S, w.attn_scale, mode="decode")
+    tol = TOL[dtype]
+    assert max_abs_rel(host64(out), o_ref) <= tol
+    assert max_abs_rel(host64(lse), l_ref) <= tol
+    assert max_abs_rel(host64(wt), w_ref) <= 1e-5
+    assert not np.any(host64(out)[1, 1])          # the empty row's output is zero
