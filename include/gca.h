@@ -169,13 +169,14 @@ gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_
                        int32_t* idx, float* sel, float* lse, float* w, void* workspace,
                        size_t ws_bytes, hipStream_t stream);
 
-/* Profiling aid (outside the method).  While armed, every kernel that libgca
- * launches from the calling thread is followed by hipEventRecord(events[i], stream)
- * for i = 0, 1, ... up to `capacity`, so a caller can time each kernel on the
- * stream it runs on.  The events are created and owned by the caller.
- * gca_profile_arm(NULL, 0) disarms; arming resets the count.  gca_profile_count()
- * is the number of events recorded since arming and gca_profile_name(i) the
- * kernel that preceded events[i] (NULL if out of range). */
+/* Profiling aid (outside the method).  While armed, the i-th kernel that libgca
+ * launches from the calling thread (i = 0, 1, ... while 2 (i + 1) <= capacity,
+ * capacity <= 4096) is dispatched with events[2 i] and events[2 i + 1] as its
+ * start and stop events (hipExtLaunchKernel), so a caller can time each kernel
+ * alone without adding work to the stream.  The events are created and owned
+ * by the caller.  gca_profile_arm(NULL, 0) disarms; arming resets the count.
+ * gca_profile_count() is the number of kernels timed since arming and
+ * gca_profile_name(i) the name of kernel i (NULL if out of range). */
 void gca_profile_arm(hipEvent_t* events, int capacity);
 int gca_profile_count(void);
 const char* gca_profile_name(int i);

@@ -113,14 +113,18 @@ gca_status check_ws(void* ws, size_t have, size_t need) {
 namespace gca {
 thread_local hipError_t g_launch_error = hipSuccess;
 
-void note_launch(const char* kernel, hipStream_t stream) {
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess && g_launch_error == hipSuccess) g_launch_error = e;
+bool profile_slot(const char* kernel, hipEvent_t* start, hipEvent_t* stop) {
   ProfileHook& h = g_profile;
-  if (!h.events || h.count >= h.capacity) return;
-  if (h.count < 4096) h.names[h.count] = kernel;
-  (void)hipEventRecord(h.events[h.count], stream);
+  if (!h.events || 2 * (h.count + 1) > h.capacity) return false;
+  h.names[h.count] = kernel;
+  *start = h.events[2 * h.count];
+  *stop = h.events[2 * h.count + 1];
   ++h.count;
+  return true;
+}
+
+void note_launch_error(hipError_t e) {
+  if (e != hipSuccess && g_launch_error == hipSuccess) g_launch_error = e;
 }
 
 hipError_t take_launch_error() {

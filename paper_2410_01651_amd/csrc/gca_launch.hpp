@@ -3,9 +3,13 @@
 // launch; shapes have been validated by the caller.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
+
+#include <tuple>
+#include <utility>
 
 namespace gca {
 
@@ -62,11 +66,37 @@ hipError_t launch_xattn_bwd(const Shape& s, const void* q, const void* k, const 
                             const void* lmk_k, float* dlmk_q, float* dlmk_k, void* ws,
                             hipStream_t stream);
 
-// Called right after every kernel launch: keeps the launch's error (the first
-// one of a sequence) and records the armed profiling event, if any.
-void note_launch(const char* kernel, hipStream_t stream);
+// The per-kernel timing hook (gca_profile_arm): the next pair of the caller's
+// events for `kernel`, or false when the hook is disarmed or full.
+bool profile_slot(const char* kernel, hipEvent_t* start, hipEvent_t* stop);
+// Keeps a launch's error (the first one of a sequence).
+void note_launch_error(hipError_t e);
 // The first launch error since the last call (hipSuccess if none); clears it.
 hipError_t take_launch_error();
+
+template <typename Tup, size_t... I>
+inline void kernel_arg_ptrs(Tup& t, void** p, std::index_sequence<I...>) {
+  ((p[I] = static_cast<void*>(&std::get<I>(t))), ...);
+}
+
+// Every kernel is launched through here.  The arguments are converted to the
+// kernel's parameter types; while the timing hook is armed the dispatch itself
+// carries a start and a stop event (hipExtLaunchKernel), so timing a kernel adds
+// no packets to the stream and measures the kernel alone.
+template <typename... KArgs, typename... Args>
+inline void launch_kernel(const char* name, void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t smem,
+                          hipStream_t stream, Args... args) {
+  static_assert(sizeof...(KArgs) == sizeof...(Args), "kernel argument count");
+  std::tuple<KArgs...> a{static_cast<KArgs>(args)...};
+  void* ptrs[sizeof...(KArgs)];
+  kernel_arg_ptrs(a, ptrs, std::index_sequence_for<KArgs...>{});
+  hipEvent_t start = nullptr, stop = nullptr;
+  const void* f = reinterpret_cast<const void*>(kernel);
+  if (profile_slot(name, &start, &stop))
+    note_launch_error(hipExtLaunchKernel(f, grid, block, ptrs, smem, stream, start, stop, 0));
+  else
+    note_launch_error(hipLaunchKernel(f, grid, block, ptrs, smem, stream));
+}
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 inline int64_t round8(int64_t n) { return (n + 7) & ~int64_t(7); }

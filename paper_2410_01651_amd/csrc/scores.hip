@@ -9,7 +9,7 @@
 //   lexicographic (score desc, chunk asc) reduction.  The chosen chunks are
 //   then written in ascending chunk order.
 // decode scan: one landmark query against every past landmark key.  The keys
-//   are streamed once, coalesced, by ~512 workgroups whose waves each own a
+//   are streamed once, coalesced, by ~256 workgroups whose waves each own a
 //   contiguous range; 8 lanes share one key row and reduce the dot product
 //   with three cross-lane steps.  Each wave leaves its range's best k in the
 //   workspace; the decode attention kernel merges them (xattn_decode.hip).
@@ -353,9 +353,8 @@ hipError_t launch_fused_k(const Shape& s, const void* lq, const void* lk, int32_
                           hipStream_t st) {
   const int64_t ntq = (s.nQ + 63) / 64;
   const int64_t BHr = (int64_t)s.B * s.Hr;
-  hipLaunchKernelGGL((fused_select_kernel<T, KM>), dim3((unsigned)(BHr * ntq)), dim3(256), 0, st, (const T*)lq,
-                     (const T*)lk, idx, sel, s.nQ, s.nKV, s.D, s.score_scale, s.topk, ntq);
-  note_launch("fused_select_kernel", st);
+  launch_kernel("fused_select_kernel", fused_select_kernel<T, KM>, dim3((unsigned)(BHr * ntq)), dim3(256), 0, st,
+                (const T*)lq, (const T*)lk, idx, sel, s.nQ, s.nKV, s.D, s.score_scale, s.topk, ntq);
   return take_launch_error();
 }
 
@@ -363,19 +362,16 @@ template <typename T>
 hipError_t launch_scores_t(const Shape& s, const void* lq, const void* lk, float* scores, hipStream_t st) {
   const int64_t ntq = (s.nQ + 63) / 64, ntj = (s.nKV + 63) / 64;
   const int64_t nwork = (int64_t)s.B * s.Hr * ntq * ntj;
-  hipLaunchKernelGGL(chunk_scores_kernel<T>, dim3((unsigned)round8(nwork)), dim3(256), 0, st,
-                     (const T*)lq, (const T*)lk, scores, s.nQ, s.nKV, s.D, s.score_scale, s.causal, ntq,
-                     ntj, nwork);
-  note_launch("chunk_scores_kernel", st);
+  launch_kernel("chunk_scores_kernel", chunk_scores_kernel<T>, dim3((unsigned)round8(nwork)), dim3(256), 0, st,
+                (const T*)lq, (const T*)lk, scores, s.nQ, s.nKV, s.D, s.score_scale, s.causal, ntq, ntj, nwork);
   return take_launch_error();
 }
 
 template <int KM>
 hipError_t launch_topk_k(const Shape& s, const float* scores, int32_t* idx, float* sel, hipStream_t st) {
   const int64_t rows = (int64_t)s.B * s.Hr * s.nQ;
-  hipLaunchKernelGGL(topk_kernel<KM>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, scores, idx, sel,
-                     rows, s.nQ, s.nKV, s.topk, s.causal);
-  note_launch("topk_kernel", st);
+  launch_kernel("topk_kernel", topk_kernel<KM>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, scores, idx, sel,
+                rows, s.nQ, s.nKV, s.topk, s.causal);
   return take_launch_error();
 }
 
@@ -386,10 +382,9 @@ hipError_t launch_scan_k(const Shape& s, const void* lq, const void* lk, void* w
   float* cs = decode_list_scores(s, ws);
   int* cj = decode_list_chunks(s, ws);
   const size_t smem = (size_t)s.D * sizeof(T);
-  hipLaunchKernelGGL((decode_scan_kernel<T, KM>), dim3((unsigned)(rows * plan.wgs)), dim3(kScanThreads), smem, st,
-                     (const T*)lq, (const T*)lk, cs, cj, s.nKV, s.D, s.score_scale, s.topk, plan.pw, plan.lists,
-                     plan.wgs);
-  note_launch("decode_scan_kernel", st);
+  launch_kernel("decode_scan_kernel", decode_scan_kernel<T, KM>, dim3((unsigned)(rows * plan.wgs)),
+                dim3(kScanThreads), smem, st, (const T*)lq, (const T*)lk, cs, cj, s.nKV, s.D, s.score_scale, s.topk,
+                plan.pw, plan.lists, plan.wgs);
   return take_launch_error();
 }
 
@@ -408,10 +403,10 @@ hipError_t launch_topk(const Shape& s, const float* scores, int32_t* idx, float*
 }
 
 DecodePlan decode_plan(const Shape& s) {
-  // about 512 scan workgroups in all (two per CU), every wave one contiguous
+  // about 256 scan workgroups in all (one per CU), every wave one contiguous
   // range of at least 64 keys
   const int64_t rows = (int64_t)s.B * s.Hr;
-  int64_t wgs = 512 / rows;
+  int64_t wgs = 256 / rows;
   if (wgs < 1) wgs = 1;
   int64_t pw = (s.nKV + wgs * kScanWaves - 1) / (wgs * kScanWaves);
   if (pw < 64) pw = 64;
@@ -434,14 +429,20 @@ int* decode_list_chunks(const Shape& s, void* ws) {
 }
 
 hipError_t launch_decode_scan(const Shape& s, const void* lmk_q, const void* lmk_k, void* ws, hipStream_t stream) {
-  if (s.bf16) {
-    if (s.topk <= 8) return launch_scan_k<__bf16, 8>(s, lmk_q, lmk_k, ws, stream);
-    if (s.topk <= 16) return launch_scan_k<__bf16, 16>(s, lmk_q, lmk_k, ws, stream);
-    return launch_scan_k<__bf16, 32>(s, lmk_q, lmk_k, ws, stream);
-  }
-  if (s.topk <= 8) return launch_scan_k<float, 8>(s, lmk_q, lmk_k, ws, stream);
-  if (s.topk <= 16) return launch_scan_k<float, 16>(s, lmk_q, lmk_k, ws, stream);
-  return launch_scan_k<float, 32>(s, lmk_q, lmk_k, ws, stream);
+  // A lane sees at most ceil(pw / 64) keys of its wave's range (one key of every
+  // eighth group of 8), so a list of min(k, that) entries keeps all it needs.
+  const int64_t per_lane = (decode_plan(s).pw + 63) / 64;
+  const int64_t need = per_lane < s.topk ? per_lane : s.topk;
+  auto run = [&](auto tag) {
+    using T = decltype(tag);
+    if (need <= 1) return launch_scan_k<T, 1>(s, lmk_q, lmk_k, ws, stream);
+    if (need <= 2) return launch_scan_k<T, 2>(s, lmk_q, lmk_k, ws, stream);
+    if (need <= 4) return launch_scan_k<T, 4>(s, lmk_q, lmk_k, ws, stream);
+    if (need <= 8) return launch_scan_k<T, 8>(s, lmk_q, lmk_k, ws, stream);
+    if (need <= 16) return launch_scan_k<T, 16>(s, lmk_q, lmk_k, ws, stream);
+    return launch_scan_k<T, 32>(s, lmk_q, lmk_k, ws, stream);
+  };
+  return s.bf16 ? run(__bf16{}) : run(float{});
 }
 
 size_t fused_workspace(const Shape&) { return 0; }

@@ -885,42 +885,34 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
   const int64_t BHr = (int64_t)s.B * s.Hr, BH = (int64_t)s.B * s.H;
   const int64_t nent = BHr * s.nQ * s.topk;
   Ws& w = p.ws;
-  hipLaunchKernelGGL(weights_kernel, dim3(blocks_for(nent, 256)), dim3(256), 0, st, p.idx, p.sel, w.w,
-                     BHr * s.nQ, s.topk, s.nKV);
-  note_launch("weights_kernel", st);
+  launch_kernel("weights_kernel", weights_kernel, dim3(blocks_for(nent, 256)), dim3(256), 0, st, p.idx, p.sel, w.w,
+                BHr * s.nQ, s.topk, s.nKV);
   const unsigned zblocks = std::min(blocks_for(BHr * s.nKV, 256), 4096u);
-  hipLaunchKernelGGL(fill_zero_kernel, dim3(zblocks), dim3(256), 0, st, w.counts, BHr * s.nKV);
-  note_launch("fill_zero_kernel", st);
-  hipLaunchKernelGGL(csr_count_kernel, dim3(blocks_for(nent, 256)), dim3(256), 0, st, p.idx, w.counts, BHr, s.nQ,
-                     s.topk, s.nKV, s.causal);
-  note_launch("csr_count_kernel", st);
-  hipLaunchKernelGGL(csr_scan_kernel, dim3((unsigned)BHr), dim3(1024), 0, st, w.counts, w.offs, w.cursor, s.nKV);
-  note_launch("csr_scan_kernel", st);
-  hipLaunchKernelGGL(csr_fill_kernel, dim3(blocks_for(nent, 256)), dim3(256), 0, st, p.idx, w.cursor, w.unsorted,
-                     BHr, s.nQ, s.topk, s.nKV, s.causal);
-  note_launch("csr_fill_kernel", st);
-  hipLaunchKernelGGL(csr_sort_kernel, dim3(blocks_for(BHr * s.nKV, 4)), dim3(256), 0, st, w.offs, w.unsorted,
-                     w.sorted, BHr, s.nQ, s.topk, s.nKV);
-  note_launch("csr_sort_kernel", st);
+  launch_kernel("fill_zero_kernel", fill_zero_kernel, dim3(zblocks), dim3(256), 0, st, w.counts, BHr * s.nKV);
+  launch_kernel("csr_count_kernel", csr_count_kernel, dim3(blocks_for(nent, 256)), dim3(256), 0, st, p.idx, w.counts,
+                BHr, s.nQ, s.topk, s.nKV, s.causal);
+  launch_kernel("csr_scan_kernel", csr_scan_kernel, dim3((unsigned)BHr), dim3(1024), 0, st, w.counts, w.offs,
+                w.cursor, s.nKV);
+  launch_kernel("csr_fill_kernel", csr_fill_kernel, dim3(blocks_for(nent, 256)), dim3(256), 0, st, p.idx, w.cursor,
+                w.unsorted, BHr, s.nQ, s.topk, s.nKV, s.causal);
+  launch_kernel("csr_sort_kernel", csr_sort_kernel, dim3(blocks_for(BHr * s.nKV, 4)), dim3(256), 0, st, w.offs,
+                w.unsorted, w.sorted, BHr, s.nQ, s.topk, s.nKV);
   const int64_t nq_work = BH * s.nQ, nk_work = BH * s.nKV;
   // persistent: two workgroups per CU, two chunk streams each
   const int64_t dq_wgs = std::min<int64_t>(512, round8((nq_work + 1) / 2));
-  hipLaunchKernelGGL(bwd_dq_kernel<T>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
-  note_launch("bwd_dq_kernel", st);
-  hipLaunchKernelGGL(bwd_dkdv_kernel<T>, dim3((unsigned)round8(nk_work)), dim3(kThreads), 0, st, p, nk_work);
-  note_launch("bwd_dkdv_kernel", st);
-  hipLaunchKernelGGL(dsel_kernel, dim3((unsigned)(BHr * s.nQ)), dim3(64), 0, st, w.w, w.dwp, dsel, s.nQ, s.H, s.Hr,
-                     s.topk, s.causal);
-  note_launch("dsel_kernel", st);
+  launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
+  launch_kernel("bwd_dkdv_kernel", bwd_dkdv_kernel<T>, dim3((unsigned)round8(nk_work)), dim3(kThreads), 0, st, p,
+                nk_work);
+  launch_kernel("dsel_kernel", dsel_kernel, dim3((unsigned)(BHr * s.nQ)), dim3(64), 0, st, w.w, w.dwp, dsel, s.nQ,
+                s.H, s.Hr, s.topk, s.causal);
   if (dlmk_q) {
-    hipLaunchKernelGGL(dlmk_q_kernel<T>, dim3((unsigned)(BHr * s.nQ)), dim3(256), 0, st, (const T*)lmk_k, p.idx,
-                       dsel, dlmk_q, s.nQ, s.nKV, s.D, s.topk, s.score_scale, gather_shape(s.D, sizeof(T)));
-    note_launch("dlmk_q_kernel", st);
+    launch_kernel("dlmk_q_kernel", dlmk_q_kernel<T>, dim3((unsigned)(BHr * s.nQ)), dim3(256), 0, st, (const T*)lmk_k,
+                  p.idx, dsel, dlmk_q, s.nQ, s.nKV, s.D, s.topk, s.score_scale, gather_shape(s.D, sizeof(T)));
   }
   if (dlmk_k) {
-    hipLaunchKernelGGL(dlmk_k_kernel<T>, dim3((unsigned)(BHr * s.nKV)), dim3(256), 0, st, (const T*)lmk_q, w.offs,
-                       w.sorted, dsel, dlmk_k, s.nQ, s.nKV, s.D, s.topk, s.score_scale, gather_shape(s.D, sizeof(T)));
-    note_launch("dlmk_k_kernel", st);
+    launch_kernel("dlmk_k_kernel", dlmk_k_kernel<T>, dim3((unsigned)(BHr * s.nKV)), dim3(256), 0, st, (const T*)lmk_q,
+                  w.offs, w.sorted, dsel, dlmk_k, s.nQ, s.nKV, s.D, s.topk, s.score_scale,
+                  gather_shape(s.D, sizeof(T)));
   }
   return take_launch_error();
 }

@@ -294,15 +294,14 @@ hipError_t launch_dec_t(const Shape& s, const DecParams& p, hipStream_t st) {
   const dim3 grid((unsigned)((int64_t)s.B * s.H)), block(kDecThreads);
   if (p.ls) {
     if (s.topk <= 8)
-      hipLaunchKernelGGL((xattn_decode_kernel<T, OBO, true, 8>), grid, block, 0, st, p);
+      launch_kernel("xattn_decode_kernel", xattn_decode_kernel<T, OBO, true, 8>, grid, block, 0, st, p);
     else if (s.topk <= 16)
-      hipLaunchKernelGGL((xattn_decode_kernel<T, OBO, true, 16>), grid, block, 0, st, p);
+      launch_kernel("xattn_decode_kernel", xattn_decode_kernel<T, OBO, true, 16>, grid, block, 0, st, p);
     else
-      hipLaunchKernelGGL((xattn_decode_kernel<T, OBO, true, 32>), grid, block, 0, st, p);
+      launch_kernel("xattn_decode_kernel", xattn_decode_kernel<T, OBO, true, 32>, grid, block, 0, st, p);
   } else {
-    hipLaunchKernelGGL((xattn_decode_kernel<T, OBO, false, 8>), grid, block, 0, st, p);
+    launch_kernel("xattn_decode_kernel", xattn_decode_kernel<T, OBO, false, 8>, grid, block, 0, st, p);
   }
-  note_launch("xattn_decode_kernel", st);
   return take_launch_error();
 }
 

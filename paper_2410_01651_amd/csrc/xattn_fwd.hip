@@ -371,21 +371,17 @@ hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const 
   const dim3 grid((unsigned)(wgs < target ? round8(wgs) : target)), block(kThreads);
   if (s.bf16) {
     if (s.off_by_one) {
-      hipLaunchKernelGGL((xattn_fwd_kernel<__bf16, true>), grid, block, 0, stream, p);
-      note_launch("xattn_fwd_kernel", stream);
+      launch_kernel("xattn_fwd_kernel", xattn_fwd_kernel<__bf16, true>, grid, block, 0, stream, p);
     }
     else {
-      hipLaunchKernelGGL((xattn_fwd_kernel<__bf16, false>), grid, block, 0, stream, p);
-      note_launch("xattn_fwd_kernel", stream);
+      launch_kernel("xattn_fwd_kernel", xattn_fwd_kernel<__bf16, false>, grid, block, 0, stream, p);
     }
   } else {
     if (s.off_by_one) {
-      hipLaunchKernelGGL((xattn_fwd_kernel<float, true>), grid, block, 0, stream, p);
-      note_launch("xattn_fwd_kernel", stream);
+      launch_kernel("xattn_fwd_kernel", xattn_fwd_kernel<float, true>, grid, block, 0, stream, p);
     }
     else {
-      hipLaunchKernelGGL((xattn_fwd_kernel<float, false>), grid, block, 0, stream, p);
-      note_launch("xattn_fwd_kernel", stream);
+      launch_kernel("xattn_fwd_kernel", xattn_fwd_kernel<float, false>, grid, block, 0, stream, p);
     }
   }
   return take_launch_error();

@@ -190,3 +190,28 @@ def test_decode_16m(dev):
     assert max_abs_rel(host64(f["lse"][0]), l_ref) <= TOL[w.dtype]
     del t
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("n_chunks,topk", [(150_000, 8), (600_000, 16), (1_100_000, 32)])
+def test_decode_long_scan_ranges(dev, n_chunks, topk):
+    """Decode scans whose waves see 3, 10 and 17 keys per lane (lane lists of 4, 16
+    and 32 entries): one head, D = 64, the planted chunk retrieved, indices exact,
+    output against the oracle over the gathered chunks."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w = get_workload("decode_16m_bf16", H=1, n_chunks=n_chunks, topk=topk)
+    inp, _ = margins.checked_inputs(w, tokens=False)
+    t = {"lmk_q": to_dev(w.dtype, inp["lmk_q"], dev), "lmk_k": to_dev(w.dtype, inp["lmk_k"], dev)}
+    t.update(gi.device_kv(w, dev))
+    t.update(gi.device_tensors(w, ("q",), dev))
+    f = gca.forward(problem_for(w), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    torch.cuda.synchronize()
+    ri, rs, _ = _oracle_rows(w, inp, [0])
+    np.testing.assert_array_equal(f["idx"][0, 0].cpu().numpy(), ri)
+    assert int(gi.plant_positions(w)[0]) in list(ri[0])
+    assert max_abs_rel(host64(f["sel"][0, 0]), rs) <= TOL[w.dtype]
+    o_ref, l_ref = _oracle_chunk(w, t, 0, 0, ri[0], rs[0])
+    assert max_abs_rel(host64(f["out"][0]), o_ref) <= TOL[w.dtype]
+    assert max_abs_rel(host64(f["lse"][0]), l_ref) <= TOL[w.dtype]
+    del t
+    torch.cuda.empty_cache()
