@@ -145,7 +145,7 @@ __device__ __forceinline__ float dot_block(const u32x4* v, const float* q, float
 // descriptor per key group, whose range check zeroes the lanes past the end of
 // the wave's range with no memory access, and run one batch of 8 column blocks
 // ahead of the arithmetic.
-template <typename T, int KM>
+template <typename T, int KM, bool KEEP_ALL>
 __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __restrict__ lq,
                                                                    const T* __restrict__ lk, float* __restrict__ cs,
                                                                    int* __restrict__ cj, int64_t nC, int D,
@@ -204,6 +204,14 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
   float acc = 0.f;
   TopList<KM> L;
   L.init();
+  // KEEP_ALL (a lane sees at most KM keys): lane (kl, sub) keeps the raw score
+  // of key 8 (8 m + sub) + kl of its range in sc[m], ranked only at the end
+  float sc[KEEP_ALL ? KM : 1];
+  float mine = -INFINITY;
+  if constexpr (KEEP_ALL) {
+#pragma unroll
+    for (int m = 0; m < KM; ++m) sc[m] = -INFINITY;
+  }
   auto consume = [&](const u32x4* v, int64_t step0) {
 #pragma unroll
     for (int k = 0; k < kScanBatch; ++k) {
@@ -214,11 +222,21 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
           acc += dpp<kDppXor1>(acc);
           acc += dpp<kDppXor2>(acc);
           acc += dpp<kDppHalfMirror>(acc);
-          const int64_t key = 8 * cg + kl;
-          // one of the key's 8 lanes inserts it, rotating with the group
-          if (key < n && sub == (int)(cg & 7)) {
-            const float sv = acc * scale;
-            if (__builtin_isfinite(sv)) L.insert(sv, (int)(lo + key));
+          if constexpr (KEEP_ALL) {
+            if (sub == (int)(cg & 7)) mine = acc;
+            if ((cg & 7) == 7 || cg + 1 == ngroups) {
+#pragma unroll
+              for (int m = 0; m < KM; ++m)
+                if (m == (int)(cg >> 3)) sc[m] = mine;
+              mine = -INFINITY;
+            }
+          } else {
+            const int64_t key = 8 * cg + kl;
+            // one of the key's 8 lanes inserts it, rotating with the group
+            if (key < n && sub == (int)(cg & 7)) {
+              const float sv = acc * scale;
+              if (__builtin_isfinite(sv)) L.insert(sv, (int)(lo + key));
+            }
           }
           acc = 0.f;
           ccb = 0;
@@ -247,6 +265,14 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
     consume(va, bt * kScanBatch);
   }
 
+  if constexpr (KEEP_ALL) {
+#pragma unroll
+    for (int m = 0; m < KM; ++m) {
+      const int64_t key = 8 * (8 * m + sub) + kl;
+      const float sv = sc[m] * scale;
+      if (key < n && __builtin_isfinite(sv)) L.insert(sv, (int)(lo + key));
+    }
+  }
   float ms;
   int mj, cnt;
   wave_merge(L, K, ms, mj, cnt);
@@ -375,14 +401,14 @@ hipError_t launch_topk_k(const Shape& s, const float* scores, int32_t* idx, floa
   return take_launch_error();
 }
 
-template <typename T, int KM>
+template <typename T, int KM, bool KEEP_ALL>
 hipError_t launch_scan_k(const Shape& s, const void* lq, const void* lk, void* ws, hipStream_t st) {
   const DecodePlan plan = decode_plan(s);
   const int64_t rows = (int64_t)s.B * s.Hr;
   float* cs = decode_list_scores(s, ws);
   int* cj = decode_list_chunks(s, ws);
   const size_t smem = (size_t)s.D * sizeof(T);
-  launch_kernel("decode_scan_kernel", decode_scan_kernel<T, KM>, dim3((unsigned)(rows * plan.wgs)),
+  launch_kernel("decode_scan_kernel", decode_scan_kernel<T, KM, KEEP_ALL>, dim3((unsigned)(rows * plan.wgs)),
                 dim3(kScanThreads), smem, st, (const T*)lq, (const T*)lk, cs, cj, s.nKV, s.D, s.score_scale, s.topk,
                 plan.pw, plan.lists, plan.wgs);
   return take_launch_error();
@@ -430,17 +456,22 @@ int* decode_list_chunks(const Shape& s, void* ws) {
 
 hipError_t launch_decode_scan(const Shape& s, const void* lmk_q, const void* lmk_k, void* ws, hipStream_t stream) {
   // A lane sees at most ceil(pw / 64) keys of its wave's range (one key of every
-  // eighth group of 8), so a list of min(k, that) entries keeps all it needs.
+  // eighth group of 8).  Up to k of them it keeps every raw score and ranks them
+  // at the end; beyond, it keeps a running best-k list.
   const int64_t per_lane = (decode_plan(s).pw + 63) / 64;
-  const int64_t need = per_lane < s.topk ? per_lane : s.topk;
   auto run = [&](auto tag) {
     using T = decltype(tag);
-    if (need <= 1) return launch_scan_k<T, 1>(s, lmk_q, lmk_k, ws, stream);
-    if (need <= 2) return launch_scan_k<T, 2>(s, lmk_q, lmk_k, ws, stream);
-    if (need <= 4) return launch_scan_k<T, 4>(s, lmk_q, lmk_k, ws, stream);
-    if (need <= 8) return launch_scan_k<T, 8>(s, lmk_q, lmk_k, ws, stream);
-    if (need <= 16) return launch_scan_k<T, 16>(s, lmk_q, lmk_k, ws, stream);
-    return launch_scan_k<T, 32>(s, lmk_q, lmk_k, ws, stream);
+    if (per_lane <= s.topk) {
+      if (per_lane <= 1) return launch_scan_k<T, 1, true>(s, lmk_q, lmk_k, ws, stream);
+      if (per_lane <= 2) return launch_scan_k<T, 2, true>(s, lmk_q, lmk_k, ws, stream);
+      if (per_lane <= 4) return launch_scan_k<T, 4, true>(s, lmk_q, lmk_k, ws, stream);
+      if (per_lane <= 8) return launch_scan_k<T, 8, true>(s, lmk_q, lmk_k, ws, stream);
+      if (per_lane <= 16) return launch_scan_k<T, 16, true>(s, lmk_q, lmk_k, ws, stream);
+      return launch_scan_k<T, 32, true>(s, lmk_q, lmk_k, ws, stream);
+    }
+    if (s.topk <= 8) return launch_scan_k<T, 8, false>(s, lmk_q, lmk_k, ws, stream);
+    if (s.topk <= 16) return launch_scan_k<T, 16, false>(s, lmk_q, lmk_k, ws, stream);
+    return launch_scan_k<T, 32, false>(s, lmk_q, lmk_k, ws, stream);
   };
   return s.bf16 ? run(__bf16{}) : run(float{});
 }

@@ -192,11 +192,12 @@ def test_decode_16m(dev):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("n_chunks,topk", [(150_000, 8), (600_000, 16), (1_100_000, 32)])
+@pytest.mark.parametrize("n_chunks,topk", [(150_000, 8), (600_000, 16), (1_100_000, 32), (300_000, 4)])
 def test_decode_long_scan_ranges(dev, n_chunks, topk):
-    """Decode scans whose waves see 3, 10 and 17 keys per lane (lane lists of 4, 16
-    and 32 entries): one head, D = 64, the planted chunk retrieved, indices exact,
-    output against the oracle over the gathered chunks."""
+    """Decode scans whose lanes see 3, 10 and 17 keys (all kept, in 4, 16 and 32
+    registers) and 5 keys with k = 4 (a running best-4 list per lane): one head,
+    D = 64, the planted chunk retrieved, indices exact, output against the oracle
+    over the gathered chunks."""
     import torch
     from paper_2410_01651_amd import gca
     w = get_workload("decode_16m_bf16", H=1, n_chunks=n_chunks, topk=topk)
