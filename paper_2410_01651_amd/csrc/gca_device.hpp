@@ -490,7 +490,6 @@ __device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
   return umax64((uint64_t)l0 | ((uint64_t)h0 << 32), (uint64_t)l1 | ((uint64_t)h1 << 32));
 }
 
-__device__ __forceinline__ uint64_t umin64(uint64_t a, uint64_t b) { return a < b ? a : b; }
 // x of lane l ^ 4 (within each 32-lane half): ds_swizzle in bit-mask mode,
 // lane l reads lane ((l & 31) ^ 4).
 __device__ __forceinline__ uint32_t swz_xor4(uint32_t x) {
@@ -529,21 +528,42 @@ __device__ __forceinline__ uint64_t wave_sort_desc(uint64_t k) {
         else if (j == 4) b = (uint64_t)swz_xor4((uint32_t)k) | ((uint64_t)swz_xor4((uint32_t)(k >> 32)) << 32);
         else b = dpp64<kDppRor8>(k);  // j == 8: rotating a 16-lane row by 8 pairs l with l ^ 8
       }
-      k = keep_max ? umax64(a, b) : umin64(a, b);
+      k = ((a > b) == keep_max) ? a : b;  // the larger key where the lane keeps the max
     }
   }
   return k;
 }
 
-// The wave's best k (k <= 64) when every lane holds at most one candidate
-// (empty lanes pass -inf / kNoChunk), in wave_merge's form.
-__device__ __forceinline__ void wave_top_one(float s, int j, int k, float& my_s, int& my_j, int& count) {
+// Keys sorted largest first across the wave (lane r: r-th) in wave_merge's form:
+// lane r < count holds the r-th best of the first k.
+__device__ __forceinline__ void sorted_keys_top(uint64_t key, int k, float& my_s, int& my_j, int& count) {
   const int lane = threadIdx.x & 63;
-  const uint64_t key = wave_sort_desc(pack_key(s, j));
   const bool real = key_chunk(key) != kNoChunk;
   count = __popcll(__ballot(real && lane < k));
   my_s = lane < count ? key_score(key) : -INFINITY;
   my_j = lane < count ? key_chunk(key) : kNoChunk;
+}
+
+// The wave's best k (k <= 64) when every lane holds at most one candidate
+// (empty lanes pass -inf / kNoChunk), in wave_merge's form.
+__device__ __forceinline__ void wave_top_one(float s, int j, int k, float& my_s, int& my_j, int& count) {
+  sorted_keys_top(wave_sort_desc(pack_key(s, j)), k, my_s, my_j, count);
+}
+
+// The wave's best k (k <= 32) of two candidates per lane: both columns sorted,
+// then the best 32 of each (column 1's moved to lanes 32-63) sorted together.
+__device__ __forceinline__ void wave_top_two(uint64_t a, uint64_t b, int k, float& my_s, int& my_j, int& count) {
+  const int lane = threadIdx.x & 63;
+  a = wave_sort_desc(a);
+  b = wave_sort_desc(b);
+  // lane l >= 32 takes b of lane l - 32: the permlane swap hands every lane both
+  // keys of its pair (l, l ^ 32); the one that is not its own is the partner's
+  uint32_t l0, l1, h0, h1;
+  pair32((uint32_t)b, l0, l1);
+  pair32((uint32_t)(b >> 32), h0, h1);
+  const uint64_t r0 = (uint64_t)l0 | ((uint64_t)h0 << 32), r1 = (uint64_t)l1 | ((uint64_t)h1 << 32);
+  const uint64_t other = r0 != b ? r0 : r1;
+  sorted_keys_top(wave_sort_desc(lane < 32 ? a : other), k, my_s, my_j, count);
 }
 
 // Merge the 64 lanes' lists into the wave's best k (k <= 64).  Lane r < *count
@@ -623,22 +643,37 @@ __device__ void merge_lists(const float* __restrict__ ls, const int* __restrict_
   const int64_t l_lo = wave * share, l_hi = l_lo + share < lists ? l_lo + share : lists;
   TopList<KM> L;
   L.init();
-  // 1. the share's list maxima, four loads per lane in flight
-  for (int64_t l0 = l_lo; l0 < l_hi; l0 += 256) {
-    float v[4];
-    int j[4];
+  // 1. the best k of the share's list maxima
+  if (share <= 128 && K <= 32) {
+    uint64_t c[2];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int64_t l = l0 + 64 * u + lane;
-      const int64_t lc = l < l_hi ? l : l_lo;
-      v[u] = rs[lc * K];
-      j[u] = l < l_hi ? rj[lc * K] : -1;
+    for (int u = 0; u < 2; ++u) {
+      const int64_t l = l_lo + 64 * u + lane;
+      const bool ok = l < l_hi;
+      const int64_t lc = ok ? l : 0;
+      const float v = rs[lc * K];
+      const int j = rj[lc * K];
+      c[u] = pack_key(ok && j >= 0 ? v : -INFINITY, ok && j >= 0 ? j : kNoChunk);
     }
+    wave_top_two(c[0], c[1], K, ms, mj, cnt);
+  } else {
+    // four loads per lane in flight, running lists
+    for (int64_t l0 = l_lo; l0 < l_hi; l0 += 256) {
+      float v[4];
+      int j[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (j[u] >= 0) L.insert(v[u], j[u]);
+      for (int u = 0; u < 4; ++u) {
+        const int64_t l = l0 + 64 * u + lane;
+        const int64_t lc = l < l_hi ? l : l_lo;
+        v[u] = rs[lc * K];
+        j[u] = l < l_hi ? rj[lc * K] : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (j[u] >= 0) L.insert(v[u], j[u]);
+    }
+    wave_merge(L, K, ms, mj, cnt);
   }
-  wave_merge(L, K, ms, mj, cnt);
   // 2. the k entries of each list they head (entry e: list e / K, rank e % K)
   const int ne = cnt * K;
   if (K * K <= 64) {

@@ -95,9 +95,11 @@ __global__ __launch_bounds__(kDecThreads) void xattn_decode_kernel(DecParams p) 
     if (wave == 0) {
       const bool valid = lane < cnt;
       const int rank = rank_by_chunk(mj, cnt);  // slots in ascending chunk order
-      const float mx = max64(valid ? ms : -INFINITY);
+      // the list is best first: lane 0 holds the maximum, and the valid lanes
+      // (< cnt <= 32) all sit in the lower half
+      const float mx = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(ms)));
       const float e = valid ? expf(ms - mx) : 0.f;
-      const float sum = sum64(e);
+      const float sum = sum32(e);
       const float wv = valid ? e / sum : 0.f;
       if (valid) {
         sSlot[rank] = rank;
@@ -226,26 +228,35 @@ __global__ __launch_bounds__(kDecThreads) void xattn_decode_kernel(DecParams p) 
     }
   };
 
+  // Each round: copy the pair's slots, then compute the first as soon as its
+  // tiles are in (the second slot's copies still in flight).  Only the tile
+  // copies are outstanding while they are waited for.
+  constexpr int kSlotLoads = 2 * TileCopy<T, 2>::kN;  // one wave's copies for one slot
   f32x16 o0 = zero16(), o1 = zero16();
   for (int r0 = 0; r0 < n; r0 += kPerRound) {
     if (r0 > 0) block_barrier();  // the last round's tiles have been read
+    wait_vmem<0>();
+    const int i0 = r0 + pair * SP;
 #pragma unroll
     for (int t = 0; t < SP; ++t) {
-      const int i = r0 + pair * SP + t;
-      if (i < n) {
-        int j = sJc[i];
+      if (i0 + t < n) {
+        int j = sJc[i0 + t];
         j = min(max(j, 0), (int)p.nKV - 1);  // valid chunks only; never copy outside the slice
         T* dst = ring + (pair * SP + t) * (2 * TILE);
         cp.issue(gk + kvb + (int64_t)j * TILE, dst);
         cp.issue(gv + kvb + (int64_t)j * TILE, dst + TILE);
       }
     }
-    wait_vmem<0>();
+    if (SP == 2 && i0 + 1 < n)
+      wait_vmem<kSlotLoads>();
+    else
+      wait_vmem<0>();
     block_barrier();
-#pragma unroll
-    for (int t = 0; t < SP; ++t) {
-      const int i = r0 + pair * SP + t;
-      if (i < n) compute(t, sSlot[i], sWc[i], o0, o1);
+    if (i0 < n) compute(0, sSlot[i0], sWc[i0], o0, o1);
+    if constexpr (SP == 2) {
+      wait_vmem<0>();
+      block_barrier();
+      if (i0 + 1 < n) compute(1, sSlot[i0 + 1], sWc[i0 + 1], o0, o1);
     }
   }
 
