@@ -160,8 +160,9 @@ gca_status gca_grouped_xattn_bwd(const gca_problem* p, const void* q, const void
  * are required (the backward needs them), lse and w may be NULL.  In CAUSAL mode
  * the score matrix is written to the workspace and then selected, or, for long
  * sequences or with GCA_FLAG_FUSED_TOPK, scored and selected in one pass without
- * it.  In DECODE mode the past landmark keys are scanned in parallel slices whose
- * candidates are then merged.
+ * it.  In DECODE mode the past landmark keys are scanned in parallel ranges that
+ * each leave their best k in the workspace; the attention kernel merges them
+ * into idx/sel (the exact top-k) before attending.
  * Workspace: gca_workspace_size(p, GCA_OP_FORWARD) bytes, 256-byte aligned.
  */
 gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_k,

@@ -40,7 +40,7 @@ def source_hash() -> str:
 
 def short_name(kernel: str) -> str:
     for key in ("xattn_fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel", "chunk_scores_kernel", "topk_kernel",
-                "fused_select_kernel", "decode_scan_kernel", "decode_merge_kernel", "xattn_decode_kernel", "weights_kernel",
+                "fused_select_kernel", "decode_scan_kernel", "xattn_decode_kernel", "weights_kernel",
                 "fill_zero_kernel", "csr_count_kernel", "csr_scan_kernel", "csr_fill_kernel", "csr_sort_kernel",
                 "dsel_kernel", "dlmk_q_kernel", "dlmk_k_kernel"):
         if key in kernel:
