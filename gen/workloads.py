@@ -30,6 +30,7 @@ class Workload:
     margin: float = 1e-3   # k-th vs (k+1)-th landmark score gap enforced
     whole_reseed: bool = False   # redraw every input until all margins hold
     device_kv: bool = False      # K/V cache drawn on the device (too large for host)
+    gumbel_seed: int = -1        # >= 0: Gumbel top-k selection with this generator seed
     notes: str = field(default="", compare=False)
 
     @property

@@ -27,6 +27,9 @@ Readings where the paper is silent or ambiguous (all configurable):
   all-zero output row (chunks 0 and 1 in causal mode);
 * the per-chunk softmax is the plain softmax of Algorithm 1 by default;
   ``off_by_one=True`` gives Eq. 3's softmax-off-by-one (denominator 1 + sum);
+* Gumbel top-k (Training & Inference, an option): noise from a counter-based
+  generator (gumbel_noise) is added to the scores for the selection only; sel,
+  the weights and everything after use the raw scores;
 * ``lse`` is the log of each (row, slot) softmax denominator, -inf for pads;
 * one retrieval head shared by all heads (Hr = 1, as Eq. 1 yields one score per
   chunk pair) or one per head (Hr = H).
@@ -36,6 +39,8 @@ q/dout [B,H,nQ*S,d], k/v [B,H,nC*S,d]; all inputs are taken as fp64.
 """
 
 import numpy as np
+
+from .philox import philox4x32_10
 
 NEG_INF = -np.inf
 
@@ -84,15 +89,34 @@ def scores(lmk_q, lmk_k, score_scale, mode="causal", rows=None):
     return out
 
 
-def topk_row(r_row, k):
+def gumbel_noise(seed, bhr, t, j):
+    """Gumbel noise g = -ln(-ln u) of candidate chunk j for retrieval row t of
+    (batch, retrieval head) bhr = b * Hr + hr (Gumbel top-k sampling, Training &
+    Inference).  u is uniform in (0, 1) from the Philox4x32-10 generator: key =
+    the 64-bit seed (low word, high word), counter = (j div 4, t, bhr, 0), output
+    word j mod 4, whose top 24 bits x give u = (x + 1/2) / 2^24.  Broadcasts over
+    array arguments."""
+    j = np.asarray(j, dtype=np.int64)
+    words = philox4x32_10(j >> 2, t, bhr, 0, seed & 0xFFFFFFFF, (seed >> 32) & 0xFFFFFFFF)
+    shape = np.broadcast_shapes(np.shape(words[0]), j.shape)
+    sel = np.broadcast_to(j & 3, shape)
+    x = np.select([sel == 0, sel == 1, sel == 2, sel == 3], [np.broadcast_to(w, shape) for w in words])
+    u = ((x >> np.uint64(8)).astype(np.float64) + 0.5) / 2.0 ** 24
+    return -np.log(-np.log(u))
+
+
+def topk_row(r_row, k, noise_row=None):
     """Top-k of one score row (Eq. 1): indices ascending, ties to the lower index.
 
-    Only finite entries are candidates.  Returns (idx[k] int32 padded with -1,
+    Only finite entries are candidates.  With ``noise_row`` (Gumbel top-k) the
+    candidates are ranked by score + noise, and sel still reports the raw score:
+    the noise only decides membership.  Returns (idx[k] int32 padded with -1,
     sel[k] fp64 padded with -inf).
     """
     r_row = _f64(r_row)
     cand = np.nonzero(np.isfinite(r_row))[0]
-    order = cand[np.lexsort((cand, -r_row[cand]))]       # score desc, then j asc
+    key = r_row[cand] if noise_row is None else r_row[cand] + _f64(noise_row)[cand]
+    order = cand[np.lexsort((cand, -key))]               # (noisy) score desc, then j asc
     chosen = np.sort(order[:k])
     idx = np.full(k, -1, dtype=np.int32)
     sel = np.full(k, NEG_INF)
@@ -101,15 +125,20 @@ def topk_row(r_row, k):
     return idx, sel
 
 
-def topk(r, k):
-    """Row-wise top-k over a [B, Hr, nRows, nC] score array."""
-    B, Hr, n, _ = r.shape
+def topk(r, k, gumbel_seed=None, rows=None):
+    """Row-wise top-k over a [B, Hr, nRows, nC] score array.  ``rows`` are the
+    landmark rows the array holds (default 0..nRows-1); with ``gumbel_seed`` the
+    selection is Gumbel top-k (noise from gumbel_noise)."""
+    B, Hr, n, nC = r.shape
+    rows = np.arange(n) if rows is None else np.asarray(rows)
     idx = np.full((B, Hr, n, k), -1, dtype=np.int32)
     sel = np.full((B, Hr, n, k), NEG_INF)
+    cols = np.arange(nC)
     for b in range(B):
         for hr in range(Hr):
-            for t in range(n):
-                idx[b, hr, t], sel[b, hr, t] = topk_row(r[b, hr, t], k)
+            for i in range(n):
+                noise = None if gumbel_seed is None else gumbel_noise(gumbel_seed, b * Hr + hr, int(rows[i]), cols)
+                idx[b, hr, i], sel[b, hr, i] = topk_row(r[b, hr, i], k, noise)
     return idx, sel
 
 
@@ -282,11 +311,11 @@ def landmark_grads(dsel, idx, lmk_q, lmk_k, score_scale):
 def forward(p, lmk_q, lmk_k, q, k, v):
     """Scores -> top-k -> weights -> grouped cross attention (Eq. 1-3).
 
-    ``p`` is a mapping with S, topk, score_scale, attn_scale, mode and
-    off_by_one.  Returns a dict with scores, idx, sel, w, out and lse.
+    ``p`` is a mapping with S, topk, score_scale, attn_scale, mode, off_by_one
+    and optionally gumbel_seed (Gumbel top-k selection).  Returns a dict with scores, idx, sel, w, out and lse.
     """
     r = scores(lmk_q, lmk_k, p["score_scale"], p["mode"])
-    idx, sel = topk(r, p["topk"])
+    idx, sel = topk(r, p["topk"], p.get("gumbel_seed"))
     w = fusion_weights(sel)
     out, lse = xattn_fwd(q, k, v, idx, w, p["S"], p["attn_scale"], p["mode"],
                          p.get("off_by_one", False))

@@ -4,7 +4,8 @@ The GPU accumulates landmark scores in fp32 while the oracle uses fp64, so a
 row whose k-th and (k+1)-th best scores (Eq. 1) nearly tie could be ranked
 differently by the two.  Inputs used for parity therefore keep a gap of at
 least ``margin`` between the k-th and (k+1)-th score of every row that has
-more than k candidates, measured in fp64 on the exact stored values.
+more than k candidates, measured in fp64 on the exact stored values (for Gumbel
+top-k workloads, between the noisy scores that the selection ranks).
 
 Two ways to restore the gap (the workload says which):
 
@@ -24,19 +25,30 @@ from gen import inputs as gi
 from . import gca
 
 
-def row_gaps(lmk_q64, lmk_k64, score_scale, k, mode, rows=None):
-    """fp64 gap between the k-th and (k+1)-th best score of each row (inf if <= k candidates)."""
+def row_gaps(lmk_q64, lmk_k64, score_scale, k, mode, rows=None, gumbel_seed=None, bhr0=0):
+    """fp64 gap between the k-th and (k+1)-th best score of each row (inf if <= k
+    candidates).  With ``gumbel_seed`` the ranked values are score + Gumbel noise
+    (the selection's key); ``bhr0`` is the (batch, retrieval head) index of the
+    first slice, for the noise counters."""
     r = gca.scores(lmk_q64, lmk_k64, score_scale, mode, rows=rows)
     B, Hr, n, nC = r.shape
+    rows_ = np.arange(n) if rows is None else np.asarray(rows)
     gaps = np.full((B, Hr, n), np.inf)
     for b in range(B):
         for hr in range(Hr):
-            srt = -np.sort(-r[b, hr], axis=1)         # descending, -inf last
+            rb = r[b, hr]
+            if gumbel_seed is not None:
+                rb = rb + gca.gumbel_noise(gumbel_seed, bhr0 + b * Hr + hr, rows_[:, None], np.arange(nC)[None, :])
+            srt = -np.sort(-rb, axis=1)               # descending, -inf last
             if nC > k:
                 kth, nxt = srt[:, k - 1], srt[:, k]
                 ok = np.isfinite(nxt)
                 gaps[b, hr] = np.where(ok, kth - np.where(ok, nxt, 0.0), np.inf)
     return gaps
+
+
+def _seed(w):
+    return w.gumbel_seed if w.gumbel_seed >= 0 else None
 
 
 def _failing_rows(w, lmk_q, lmk_k, block=2048):
@@ -46,7 +58,7 @@ def _failing_rows(w, lmk_q, lmk_k, block=2048):
     bad = []
     for r0 in range(0, nQ, block):
         rows = np.arange(r0, min(nQ, r0 + block))
-        g = row_gaps(q64, k64, w.score_scale, w.topk, w.mode, rows=rows)
+        g = row_gaps(q64, k64, w.score_scale, w.topk, w.mode, rows=rows, gumbel_seed=_seed(w))
         for b, hr, i in zip(*np.nonzero(g < w.margin)):
             bad.append((int(b), int(hr), int(rows[i])))
     return bad
@@ -63,7 +75,7 @@ def enforce(w, lmk_q, lmk_k, max_attempts=1000):
             gi.redraw_lmk_q_row(w, lmk_q, lmk_k, b, hr, t, attempt)
             g = row_gaps(gi.decode(w, lmk_q[b:b + 1, hr:hr + 1]),
                          gi.decode(w, lmk_k[b:b + 1, hr:hr + 1]),
-                         w.score_scale, w.topk, w.mode, rows=[t])
+                         w.score_scale, w.topk, w.mode, rows=[t], gumbel_seed=_seed(w), bhr0=b * w.Hr + hr)
             if g[0, 0, 0] >= w.margin:
                 break
         else:
