@@ -66,6 +66,14 @@ typedef enum { GCA_CAUSAL = 0, GCA_DECODE = 1 } gca_mode;
 /* Problem flags (gca_problem.flags). */
 #define GCA_FLAG_FUSED_TOPK 1u   /* gca_forward, CAUSAL: score and select in one pass (no score matrix) */
 #define GCA_FLAG_MATERIALIZE 2u  /* gca_forward, CAUSAL: always write the score matrix, then select */
+#define GCA_FLAG_GUMBEL 4u       /* Gumbel top-k selection (Training & Inference, "Gumbel Top-k
+                                  * sampling"): every selection (gca_topk, gca_forward in both
+                                  * modes) ranks score + g, g = -ln(-ln u) with u from the
+                                  * Philox4x32-10 generator (Salmon et al., SC 2011) keyed by
+                                  * gumbel_seed, counter (j / 4, t, b * Hr + hr, 0), word j mod 4,
+                                  * u = (top 24 bits + 1/2) / 2^24 for candidate chunk j of
+                                  * landmark row t (DECODE: t = 0).  sel, w and everything after
+                                  * use the raw scores. */
 
 /* Workspace queries (gca_workspace_size op argument). */
 #define GCA_OP_FORWARD 0
@@ -88,6 +96,7 @@ typedef struct {
   int32_t dtype;        /* gca_dtype of q, k, v, dout, dq, dk, dv, out, lmk_q, lmk_k */
   int32_t mode;         /* gca_mode */
   uint32_t flags;       /* GCA_FLAG_* */
+  uint64_t gumbel_seed; /* generator seed for GCA_FLAG_GUMBEL (ignored otherwise) */
 } gca_problem;
 
 /* Causal relevance scores (Eq. 1):

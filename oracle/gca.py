@@ -125,10 +125,11 @@ def topk_row(r_row, k, noise_row=None):
     return idx, sel
 
 
-def topk(r, k, gumbel_seed=None, rows=None):
+def topk(r, k, gumbel_seed=None, rows=None, bhr0=0):
     """Row-wise top-k over a [B, Hr, nRows, nC] score array.  ``rows`` are the
     landmark rows the array holds (default 0..nRows-1); with ``gumbel_seed`` the
-    selection is Gumbel top-k (noise from gumbel_noise)."""
+    selection is Gumbel top-k (noise from gumbel_noise), the array's first
+    (batch, retrieval head) slice being slice ``bhr0`` of the problem."""
     B, Hr, n, nC = r.shape
     rows = np.arange(n) if rows is None else np.asarray(rows)
     idx = np.full((B, Hr, n, k), -1, dtype=np.int32)
@@ -137,7 +138,8 @@ def topk(r, k, gumbel_seed=None, rows=None):
     for b in range(B):
         for hr in range(Hr):
             for i in range(n):
-                noise = None if gumbel_seed is None else gumbel_noise(gumbel_seed, b * Hr + hr, int(rows[i]), cols)
+                noise = None if gumbel_seed is None else gumbel_noise(gumbel_seed, bhr0 + b * Hr + hr,
+                                                                      int(rows[i]), cols)
                 idx[b, hr, i], sel[b, hr, i] = topk_row(r[b, hr, i], k, noise)
     return idx, sel
 

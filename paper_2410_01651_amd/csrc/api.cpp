@@ -3,6 +3,7 @@
 #include "gca.h"
 
 #include <cmath>
+#include <cstddef>
 #include <cstdint>
 #include <string>
 
@@ -32,6 +33,11 @@ gca_status from_hip(hipError_t e, const char* what) {
 
 constexpr int64_t kMaxGrid = 2147483647;  // largest 1-D grid we launch
 
+// the layout the Python binding mirrors
+static_assert(sizeof(gca_problem) == 72 && offsetof(gca_problem, n_chunks) == 16 &&
+                  offsetof(gca_problem, flags) == 56 && offsetof(gca_problem, gumbel_seed) == 64,
+              "gca_problem layout");
+
 gca_status check_problem(const gca_problem* p, gca::Shape& s) {
   if (!p) return fail(GCA_ERR_INVALID, "problem pointer is NULL");
   if (p->B < 1 || p->H < 1) return fail(GCA_ERR_INVALID, "B and H must be >= 1");
@@ -50,7 +56,8 @@ gca_status check_problem(const gca_problem* p, gca::Shape& s) {
   if (p->off_by_one != 0 && p->off_by_one != 1) return fail(GCA_ERR_INVALID, "off_by_one must be 0 or 1");
   if (!std::isfinite(p->score_scale) || !std::isfinite(p->attn_scale))
     return fail(GCA_ERR_INVALID, "scales must be finite");
-  if (p->flags & ~(GCA_FLAG_FUSED_TOPK | GCA_FLAG_MATERIALIZE)) return fail(GCA_ERR_INVALID, "unknown flag bits");
+  if (p->flags & ~(GCA_FLAG_FUSED_TOPK | GCA_FLAG_MATERIALIZE | GCA_FLAG_GUMBEL))
+    return fail(GCA_ERR_INVALID, "unknown flag bits");
   if ((p->flags & GCA_FLAG_FUSED_TOPK) && (p->flags & GCA_FLAG_MATERIALIZE))
     return fail(GCA_ERR_INVALID, "GCA_FLAG_FUSED_TOPK and GCA_FLAG_MATERIALIZE are exclusive");
   s.B = p->B;
@@ -65,6 +72,8 @@ gca_status check_problem(const gca_problem* p, gca::Shape& s) {
   s.off_by_one = p->off_by_one;
   s.score_scale = p->score_scale;
   s.attn_scale = p->attn_scale;
+  s.gumbel = (p->flags & GCA_FLAG_GUMBEL) ? 1 : 0;
+  s.gumbel_seed = p->gumbel_seed;
   const int64_t BH = (int64_t)s.B * s.H;
   if (BH > kMaxGrid / s.nQ || BH > kMaxGrid / s.nKV || (int64_t)s.B * s.Hr * s.nQ > kMaxGrid / s.topk)
     return fail(GCA_ERR_UNSUPPORTED, "problem too large for one launch");
@@ -275,7 +284,7 @@ gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_
     if (e != hipSuccess) return from_hip(e, "gca_forward (decode scan)");
     return from_hip(gca::launch_xattn_decode(s, gca::decode_list_scores(s, workspace),
                                              gca::decode_list_chunks(s, workspace), q, k, v, idx, sel, out, lse,
-                                             w, stream),
+                                             w, lmk_q, lmk_k, stream),
                     "gca_forward (decode attention)");
   } else if (fused_path(p, s)) {
     e = gca::launch_fused_select(s, lmk_q, lmk_k, idx, sel, workspace, stream);

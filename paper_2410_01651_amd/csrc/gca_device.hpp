@@ -409,6 +409,78 @@ struct Geo {
 
 // ---------------------------------------------------- top-k selection ----
 
+// ------------------------------------------------------- Gumbel noise ----
+//
+// Gumbel top-k retrieval adds g = -ln(-ln u) to every candidate's score before
+// the selection (and only there).  u comes from the Philox4x32-10 counter-based
+// generator (Salmon et al., SC 2011): key = the 64-bit seed, counter = (j / 4,
+// t, b * Hr + hr, 0) for candidate chunk j of landmark row t, output word j mod
+// 4, whose top 24 bits x give u = (x + 1/2) / 2^24 (exact in fp32).
+__device__ __forceinline__ uint32_t philox_word(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                                uint32_t k1, int word) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+    const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    c0 = hi1 ^ c1 ^ k0;
+    c1 = lo1;
+    c2 = hi0 ^ c3 ^ k1;
+    c3 = lo0;
+  }
+  return word == 0 ? c0 : word == 1 ? c1 : word == 2 ? c2 : c3;
+}
+
+// g for candidate chunk j of landmark row t in (batch, retrieval head) slice bhr.
+// The logarithms are v_log_f32 (base 2) scaled by ln 2.
+__device__ __forceinline__ float gumbel_noise(uint64_t seed, uint32_t bhr, uint32_t t, uint32_t j) {
+  const uint32_t x = philox_word(j >> 2, t, bhr, 0u, (uint32_t)seed, (uint32_t)(seed >> 32), (int)(j & 3));
+  const float u = ((float)(x >> 8) + 0.5f) * 5.9604644775390625e-8f;  // 2^-24
+  const float e = -kLn2 * __builtin_amdgcn_logf(u);                   // -ln u > 0
+  return -kLn2 * __builtin_amdgcn_logf(e);
+}
+
+// The four values of candidates 4 j4 .. 4 j4 + 3 (one generator call).
+__device__ __forceinline__ f32x4 gumbel_noise4(uint64_t seed, uint32_t bhr, uint32_t t, uint32_t j4) {
+  uint32_t c0 = j4, c1 = t, c2 = bhr, c3 = 0u, k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+    const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    c0 = hi1 ^ c1 ^ k0;
+    c1 = lo1;
+    c2 = hi0 ^ c3 ^ k1;
+    c3 = lo0;
+  }
+  const uint32_t x[4] = {c0, c1, c2, c3};
+  f32x4 g;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float u = ((float)(x[w] >> 8) + 0.5f) * 5.9604644775390625e-8f;
+    g[w] = -kLn2 * __builtin_amdgcn_logf(-kLn2 * __builtin_amdgcn_logf(u));
+  }
+  return g;
+}
+
+// fp32 dot product of two D-element rows (D a multiple of 8).
+template <typename T>
+__device__ __forceinline__ float dot_rows(const T* __restrict__ a, const T* __restrict__ b, int D) {
+  float acc = 0.f;
+  for (int x = 0; x < D; x += 8) {
+    const Frag<T> fa = load_frag(a + x), fb = load_frag(b + x);
+#pragma unroll
+    for (int m = 0; m < 8; ++m) acc = fmaf(frag_elem(fa, m), frag_elem(fb, m), acc);
+  }
+  return acc;
+}
+
 // Ordering of retrieval candidates: higher score first, ties to lower chunk index.
 __device__ __forceinline__ bool better(float s, int j, float s2, int j2) {
   return s > s2 || (s == s2 && j < j2);

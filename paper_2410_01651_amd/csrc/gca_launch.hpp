@@ -21,6 +21,8 @@ struct Shape {
   int bf16;        // element type of tensors: 1 bf16, 0 fp32
   int off_by_one;
   float score_scale, attn_scale;
+  int gumbel;            // 1: Gumbel top-k selection
+  uint64_t gumbel_seed;  // its generator seed
 };
 
 // Eq. 1 scores, written as a [B,Hr,nQ,nKV] fp32 matrix.
@@ -45,9 +47,11 @@ hipError_t launch_decode_scan(const Shape& s, const void* lmk_q, const void* lmk
 // Decode attention (Eq. 2-3 for the one query chunk of every (batch, head)).
 // With lists (list_s != null) it first merges them into the row's top-k and
 // writes idx/sel; without, idx/sel are its inputs.
+// With Gumbel top-k the lists rank noisy scores and the chosen chunks' raw
+// scores are recomputed from lmk_q / lmk_k (unused otherwise).
 hipError_t launch_xattn_decode(const Shape& s, const float* list_s, const int* list_j, const void* q,
                                const void* k, const void* v, int32_t* idx, float* sel, void* out, float* lse,
-                               float* w, hipStream_t stream);
+                               float* w, const void* lmk_q, const void* lmk_k, hipStream_t stream);
 // Causal: scores and top-k in one pass, no score matrix.
 size_t fused_workspace(const Shape& s);
 hipError_t launch_fused_select(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx,

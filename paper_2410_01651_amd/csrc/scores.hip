@@ -16,6 +16,8 @@
 #include "gca_device.hpp"
 #include "gca_launch.hpp"
 
+#include <type_traits>
+
 namespace gca {
 namespace {
 
@@ -75,10 +77,12 @@ __device__ __forceinline__ void write_sorted(int32_t* idx, float* sel, int K, fl
   }
 }
 
-template <int KM>
+// GUMBEL: candidates are ranked by score + Gumbel noise; sel reports the raw
+// score of each chosen chunk (read back from the matrix).
+template <int KM, bool GUMBEL>
 __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ scores, int32_t* __restrict__ idx,
                                                    float* __restrict__ sel, int64_t rows, int64_t nQ,
-                                                   int64_t nC, int K, int causal) {
+                                                   int64_t nC, int K, int causal, uint64_t seed) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= rows) return;
@@ -88,12 +92,14 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ sco
   TopList<KM> L;
   L.init();
   for (int64_t j = lane; j < lim; j += 64) {
-    const float v = sr[j];
+    float v = sr[j];
+    if constexpr (GUMBEL) v += gumbel_noise(seed, (uint32_t)(row / nQ), (uint32_t)t, (uint32_t)j);
     if (__builtin_isfinite(v)) L.insert(v, (int)j);
   }
   float ms;
   int mj, cnt;
   wave_merge(L, K, ms, mj, cnt);
+  if constexpr (GUMBEL) ms = lane < cnt ? sr[mj] : -INFINITY;
   write_sorted<KM>(idx + row * K, sel + row * K, K, ms, mj, cnt);
 }
 
@@ -145,12 +151,14 @@ __device__ __forceinline__ float dot_block(const u32x4* v, const float* q, float
 // descriptor per key group, whose range check zeroes the lanes past the end of
 // the wave's range with no memory access, and run one batch of 8 column blocks
 // ahead of the arithmetic.
-template <typename T, int KM, bool KEEP_ALL>
+// GUMBEL: the lists rank (and hold) score + Gumbel noise; the decode attention
+// recomputes the chosen chunks' raw scores.
+template <typename T, int KM, bool KEEP_ALL, bool GUMBEL>
 __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __restrict__ lq,
                                                                    const T* __restrict__ lk, float* __restrict__ cs,
                                                                    int* __restrict__ cj, int64_t nC, int D,
                                                                    float scale, int K, int64_t pw, int64_t lists,
-                                                                   int64_t wgs) {
+                                                                   int64_t wgs, uint64_t seed) {
   constexpr int LPS = (int)sizeof(T) / 2;  // 16-byte records per lane per column block
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   T* sq = reinterpret_cast<T*>(smem);
@@ -234,7 +242,8 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
             const int64_t key = 8 * cg + kl;
             // one of the key's 8 lanes inserts it, rotating with the group
             if (key < n && sub == (int)(cg & 7)) {
-              const float sv = acc * scale;
+              float sv = acc * scale;
+              if constexpr (GUMBEL) sv += gumbel_noise(seed, (uint32_t)row, 0u, (uint32_t)(lo + key));
               if (__builtin_isfinite(sv)) L.insert(sv, (int)(lo + key));
             }
           }
@@ -269,7 +278,10 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
 #pragma unroll
     for (int m = 0; m < KM; ++m) {
       const int64_t key = 8 * (8 * m + sub) + kl;
-      const float sv = sc[m] * scale;
+      float sv = sc[m] * scale;
+      if constexpr (GUMBEL) {
+        if (key < n) sv += gumbel_noise(seed, (uint32_t)row, 0u, (uint32_t)(lo + key));
+      }
       if (key < n && __builtin_isfinite(sv)) L.insert(sv, (int)(lo + key));
     }
   }
@@ -290,11 +302,14 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
 // matrix cores into LDS, and 4 threads per row fold the tile into their
 // running best-KM lists.  No score matrix is written.  Row blocks are issued
 // longest first (block tq has tq+1 tiles) so the triangular work balances.
-template <typename T, int KM>
+// GUMBEL: the lists rank score + Gumbel noise (each thread then takes 16
+// consecutive columns, four generator calls per tile) and the chosen chunks'
+// raw scores are recomputed from the landmark rows for sel.
+template <typename T, int KM, bool GUMBEL>
 __global__ __launch_bounds__(256) void fused_select_kernel(const T* __restrict__ lq, const T* __restrict__ lk,
                                                            int32_t* __restrict__ idx, float* __restrict__ sel,
                                                            int64_t nQ, int64_t nC, int D, float scale, int K,
-                                                           int64_t ntq) {
+                                                           int64_t ntq, uint64_t seed) {
   __shared__ float sT[64][65];
   __shared__ float sRs[64][32];
   __shared__ int sRj[64][32];
@@ -331,11 +346,24 @@ __global__ __launch_bounds__(256) void fused_select_kernel(const T* __restrict__
       sT[tl][jl] = (any && t < nQ && j < nC && j < t) ? acc[i] * scale : -INFINITY;
     }
     __syncthreads();
+    if constexpr (GUMBEL) {
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const int c = u + 4 * m;
-      const float v = sT[r][c];
-      if (__builtin_isfinite(v)) L.insert(v, (int)(j0 + c));
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int c0 = 16 * u + 4 * q4;
+        const f32x4 g = gumbel_noise4(seed, (uint32_t)bhr, (uint32_t)(t0 + r), (uint32_t)((j0 + c0) >> 2));
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const float v = sT[r][c0 + m] + g[m];
+          if (__builtin_isfinite(v)) L.insert(v, (int)(j0 + c0 + m));
+        }
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < 16; ++m) {
+        const int c = u + 4 * m;
+        const float v = sT[r][c];
+        if (__builtin_isfinite(v)) L.insert(v, (int)(j0 + c));
+      }
     }
     __syncthreads();
   }
@@ -365,7 +393,10 @@ __global__ __launch_bounds__(256) void fused_select_kernel(const T* __restrict__
         int rank = 0;
         for (int e2 = 0; e2 < n; ++e2) rank += sRj[r][e2] < je ? 1 : 0;
         io[rank] = je;
-        so[rank] = sRs[r][e];
+        if constexpr (GUMBEL)
+          so[rank] = scale * dot_rows(lq + (bhr * nQ + t) * D, lk + (bhr * nC + je) * D, D);
+        else
+          so[rank] = sRs[r][e];
       } else {
         io[e] = -1;
         so[e] = -INFINITY;
@@ -374,13 +405,14 @@ __global__ __launch_bounds__(256) void fused_select_kernel(const T* __restrict__
   }
 }
 
-template <typename T, int KM>
+template <typename T, int KM, bool GUMBEL>
 hipError_t launch_fused_k(const Shape& s, const void* lq, const void* lk, int32_t* idx, float* sel,
                           hipStream_t st) {
   const int64_t ntq = (s.nQ + 63) / 64;
   const int64_t BHr = (int64_t)s.B * s.Hr;
-  launch_kernel("fused_select_kernel", fused_select_kernel<T, KM>, dim3((unsigned)(BHr * ntq)), dim3(256), 0, st,
-                (const T*)lq, (const T*)lk, idx, sel, s.nQ, s.nKV, s.D, s.score_scale, s.topk, ntq);
+  launch_kernel("fused_select_kernel", fused_select_kernel<T, KM, GUMBEL>, dim3((unsigned)(BHr * ntq)), dim3(256),
+                0, st, (const T*)lq, (const T*)lk, idx, sel, s.nQ, s.nKV, s.D, s.score_scale, s.topk, ntq,
+                s.gumbel_seed);
   return take_launch_error();
 }
 
@@ -393,24 +425,24 @@ hipError_t launch_scores_t(const Shape& s, const void* lq, const void* lk, float
   return take_launch_error();
 }
 
-template <int KM>
+template <int KM, bool GUMBEL>
 hipError_t launch_topk_k(const Shape& s, const float* scores, int32_t* idx, float* sel, hipStream_t st) {
   const int64_t rows = (int64_t)s.B * s.Hr * s.nQ;
-  launch_kernel("topk_kernel", topk_kernel<KM>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, scores, idx, sel,
-                rows, s.nQ, s.nKV, s.topk, s.causal);
+  launch_kernel("topk_kernel", topk_kernel<KM, GUMBEL>, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, scores,
+                idx, sel, rows, s.nQ, s.nKV, s.topk, s.causal, s.gumbel_seed);
   return take_launch_error();
 }
 
-template <typename T, int KM, bool KEEP_ALL>
+template <typename T, int KM, bool KEEP_ALL, bool GUMBEL>
 hipError_t launch_scan_k(const Shape& s, const void* lq, const void* lk, void* ws, hipStream_t st) {
   const DecodePlan plan = decode_plan(s);
   const int64_t rows = (int64_t)s.B * s.Hr;
   float* cs = decode_list_scores(s, ws);
   int* cj = decode_list_chunks(s, ws);
   const size_t smem = (size_t)s.D * sizeof(T);
-  launch_kernel("decode_scan_kernel", decode_scan_kernel<T, KM, KEEP_ALL>, dim3((unsigned)(rows * plan.wgs)),
+  launch_kernel("decode_scan_kernel", decode_scan_kernel<T, KM, KEEP_ALL, GUMBEL>, dim3((unsigned)(rows * plan.wgs)),
                 dim3(kScanThreads), smem, st, (const T*)lq, (const T*)lk, cs, cj, s.nKV, s.D, s.score_scale, s.topk,
-                plan.pw, plan.lists, plan.wgs);
+                plan.pw, plan.lists, plan.wgs, s.gumbel_seed);
   return take_launch_error();
 }
 
@@ -423,9 +455,13 @@ hipError_t launch_chunk_scores(const Shape& s, const void* lmk_q, const void* lm
 }
 
 hipError_t launch_topk(const Shape& s, const float* scores, int32_t* idx, float* sel, hipStream_t stream) {
-  if (s.topk <= 8) return launch_topk_k<8>(s, scores, idx, sel, stream);
-  if (s.topk <= 16) return launch_topk_k<16>(s, scores, idx, sel, stream);
-  return launch_topk_k<32>(s, scores, idx, sel, stream);
+  auto run = [&](auto gumbel) {
+    constexpr bool G = decltype(gumbel)::value;
+    if (s.topk <= 8) return launch_topk_k<8, G>(s, scores, idx, sel, stream);
+    if (s.topk <= 16) return launch_topk_k<16, G>(s, scores, idx, sel, stream);
+    return launch_topk_k<32, G>(s, scores, idx, sel, stream);
+  };
+  return s.gumbel ? run(std::true_type{}) : run(std::false_type{});
 }
 
 DecodePlan decode_plan(const Shape& s) {
@@ -459,21 +495,23 @@ hipError_t launch_decode_scan(const Shape& s, const void* lmk_q, const void* lmk
   // eighth group of 8).  Up to k of them it keeps every raw score and ranks them
   // at the end; beyond, it keeps a running best-k list.
   const int64_t per_lane = (decode_plan(s).pw + 63) / 64;
-  auto run = [&](auto tag) {
+  auto run = [&](auto tag, auto gumbel) {
     using T = decltype(tag);
+    constexpr bool G = decltype(gumbel)::value;
     if (per_lane <= s.topk) {
-      if (per_lane <= 1) return launch_scan_k<T, 1, true>(s, lmk_q, lmk_k, ws, stream);
-      if (per_lane <= 2) return launch_scan_k<T, 2, true>(s, lmk_q, lmk_k, ws, stream);
-      if (per_lane <= 4) return launch_scan_k<T, 4, true>(s, lmk_q, lmk_k, ws, stream);
-      if (per_lane <= 8) return launch_scan_k<T, 8, true>(s, lmk_q, lmk_k, ws, stream);
-      if (per_lane <= 16) return launch_scan_k<T, 16, true>(s, lmk_q, lmk_k, ws, stream);
-      return launch_scan_k<T, 32, true>(s, lmk_q, lmk_k, ws, stream);
+      if (per_lane <= 1) return launch_scan_k<T, 1, true, G>(s, lmk_q, lmk_k, ws, stream);
+      if (per_lane <= 2) return launch_scan_k<T, 2, true, G>(s, lmk_q, lmk_k, ws, stream);
+      if (per_lane <= 4) return launch_scan_k<T, 4, true, G>(s, lmk_q, lmk_k, ws, stream);
+      if (per_lane <= 8) return launch_scan_k<T, 8, true, G>(s, lmk_q, lmk_k, ws, stream);
+      if (per_lane <= 16) return launch_scan_k<T, 16, true, G>(s, lmk_q, lmk_k, ws, stream);
+      return launch_scan_k<T, 32, true, G>(s, lmk_q, lmk_k, ws, stream);
     }
-    if (s.topk <= 8) return launch_scan_k<T, 8, false>(s, lmk_q, lmk_k, ws, stream);
-    if (s.topk <= 16) return launch_scan_k<T, 16, false>(s, lmk_q, lmk_k, ws, stream);
-    return launch_scan_k<T, 32, false>(s, lmk_q, lmk_k, ws, stream);
+    if (s.topk <= 8) return launch_scan_k<T, 8, false, G>(s, lmk_q, lmk_k, ws, stream);
+    if (s.topk <= 16) return launch_scan_k<T, 16, false, G>(s, lmk_q, lmk_k, ws, stream);
+    return launch_scan_k<T, 32, false, G>(s, lmk_q, lmk_k, ws, stream);
   };
-  return s.bf16 ? run(__bf16{}) : run(float{});
+  if (s.bf16) return s.gumbel ? run(__bf16{}, std::true_type{}) : run(__bf16{}, std::false_type{});
+  return s.gumbel ? run(float{}, std::true_type{}) : run(float{}, std::false_type{});
 }
 
 size_t fused_workspace(const Shape&) { return 0; }
@@ -481,14 +519,15 @@ size_t fused_workspace(const Shape&) { return 0; }
 hipError_t launch_fused_select(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx, float* sel,
                                void* ws, hipStream_t stream) {
   (void)ws;
-  if (s.bf16) {
-    if (s.topk <= 8) return launch_fused_k<__bf16, 8>(s, lmk_q, lmk_k, idx, sel, stream);
-    if (s.topk <= 16) return launch_fused_k<__bf16, 16>(s, lmk_q, lmk_k, idx, sel, stream);
-    return launch_fused_k<__bf16, 32>(s, lmk_q, lmk_k, idx, sel, stream);
-  }
-  if (s.topk <= 8) return launch_fused_k<float, 8>(s, lmk_q, lmk_k, idx, sel, stream);
-  if (s.topk <= 16) return launch_fused_k<float, 16>(s, lmk_q, lmk_k, idx, sel, stream);
-  return launch_fused_k<float, 32>(s, lmk_q, lmk_k, idx, sel, stream);
+  auto run = [&](auto tag, auto gumbel) {
+    using T = decltype(tag);
+    constexpr bool G = decltype(gumbel)::value;
+    if (s.topk <= 8) return launch_fused_k<T, 8, G>(s, lmk_q, lmk_k, idx, sel, stream);
+    if (s.topk <= 16) return launch_fused_k<T, 16, G>(s, lmk_q, lmk_k, idx, sel, stream);
+    return launch_fused_k<T, 32, G>(s, lmk_q, lmk_k, idx, sel, stream);
+  };
+  if (s.bf16) return s.gumbel ? run(__bf16{}, std::true_type{}) : run(__bf16{}, std::false_type{});
+  return s.gumbel ? run(float{}, std::true_type{}) : run(float{}, std::false_type{});
 }
 
 }  // namespace gca

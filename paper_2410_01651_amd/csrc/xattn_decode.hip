@@ -46,6 +46,13 @@ struct DecParams {
   int H, Hr, topk;
   int64_t nKV;
   float attn_scale;
+  // Gumbel top-k: the lists rank noisy scores, so the chosen chunks' raw scores
+  // are recomputed from the landmark rows
+  int gumbel;
+  const void* lmk_q;
+  const void* lmk_k;
+  int D;
+  float score_scale;
 };
 
 template <typename T, bool OBO, bool MERGE, int KM>
@@ -95,9 +102,17 @@ __global__ __launch_bounds__(kDecThreads) void xattn_decode_kernel(DecParams p) 
     if (wave == 0) {
       const bool valid = lane < cnt;
       const int rank = rank_by_chunk(mj, cnt);  // slots in ascending chunk order
-      // the list is best first: lane 0 holds the maximum, and the valid lanes
-      // (< cnt <= 32) all sit in the lower half
-      const float mx = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(ms)));
+      float mx;
+      if (p.gumbel) {
+        const T* lq = reinterpret_cast<const T*>(p.lmk_q) + row * p.D;
+        const T* lk = reinterpret_cast<const T*>(p.lmk_k) + (row * p.nKV + (valid ? mj : 0)) * p.D;
+        ms = valid ? p.score_scale * dot_rows(lq, lk, p.D) : -INFINITY;
+        mx = max64(ms);
+      } else {
+        // the list is best first: lane 0 holds the maximum
+        mx = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(ms)));
+      }
+      // the valid lanes (< cnt <= 32) all sit in the lower half
       const float e = valid ? expf(ms - mx) : 0.f;
       const float sum = sum32(e);
       const float wv = valid ? e / sum : 0.f;
@@ -320,7 +335,7 @@ hipError_t launch_dec_t(const Shape& s, const DecParams& p, hipStream_t st) {
 
 hipError_t launch_xattn_decode(const Shape& s, const float* list_s, const int* list_j, const void* q,
                                const void* k, const void* v, int32_t* idx, float* sel, void* out, float* lse,
-                               float* w, hipStream_t stream) {
+                               float* w, const void* lmk_q, const void* lmk_k, hipStream_t stream) {
   DecParams p;
   p.ls = list_s;
   p.lj = list_j;
@@ -333,6 +348,11 @@ hipError_t launch_xattn_decode(const Shape& s, const float* list_s, const int* l
   p.H = s.H; p.Hr = s.Hr; p.topk = s.topk;
   p.nKV = s.nKV;
   p.attn_scale = s.attn_scale;
+  p.gumbel = list_s != nullptr && s.gumbel;
+  p.lmk_q = lmk_q;
+  p.lmk_k = lmk_k;
+  p.D = s.D;
+  p.score_scale = s.score_scale;
   if (s.bf16)
     return s.off_by_one ? launch_dec_t<__bf16, true>(s, p, stream) : launch_dec_t<__bf16, false>(s, p, stream);
   return s.off_by_one ? launch_dec_t<float, true>(s, p, stream) : launch_dec_t<float, false>(s, p, stream);

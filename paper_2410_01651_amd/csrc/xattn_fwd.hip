@@ -356,7 +356,7 @@ hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const 
                             const int32_t* idx, const float* sel, void* out, float* lse, float* w,
                             hipStream_t stream) {
   if (!s.causal) return launch_xattn_decode(s, nullptr, nullptr, q, k, v, const_cast<int32_t*>(idx),
-                                            const_cast<float*>(sel), out, lse, w, stream);
+                                            const_cast<float*>(sel), out, lse, w, nullptr, nullptr, stream);
   FwdParams p;
   p.q = q; p.k = k; p.v = v; p.idx = idx; p.sel = sel;
   p.out = out; p.lse = lse; p.w = w;

@@ -31,7 +31,7 @@ EXPORTS = (
 GCA_OK, GCA_ERR_INVALID, GCA_ERR_UNSUPPORTED, GCA_ERR_WORKSPACE, GCA_ERR_HIP = range(5)
 GCA_FP32, GCA_BF16 = 0, 1
 GCA_CAUSAL, GCA_DECODE = 0, 1
-FLAG_FUSED_TOPK, FLAG_MATERIALIZE = 1, 2
+FLAG_FUSED_TOPK, FLAG_MATERIALIZE, FLAG_GUMBEL = 1, 2, 4
 OP_FORWARD, OP_BACKWARD = 0, 1
 
 
@@ -53,6 +53,7 @@ class Problem(ctypes.Structure):
         ("dtype", ctypes.c_int32),
         ("mode", ctypes.c_int32),
         ("flags", ctypes.c_uint32),
+        ("gumbel_seed", ctypes.c_uint64),
     ]
 
     @property
@@ -113,9 +114,12 @@ def _check(status: int) -> None:
 
 
 def problem(B, H, n_chunks, topk, D=None, Hr=1, d=64, S=64, score_scale=None, attn_scale=None,
-            off_by_one=False, dtype="bf16", mode="causal", flags=0) -> Problem:
-    """Build a ``gca_problem``; D defaults to H*d, scales to 1/sqrt(D) and 1/sqrt(d)."""
+            off_by_one=False, dtype="bf16", mode="causal", flags=0, gumbel_seed=None) -> Problem:
+    """Build a ``gca_problem``; D defaults to H*d, scales to 1/sqrt(D) and 1/sqrt(d).
+    A ``gumbel_seed`` turns on Gumbel top-k selection (GCA_FLAG_GUMBEL)."""
     D = H * d if D is None else D
+    if gumbel_seed is not None:
+        flags |= FLAG_GUMBEL
     return Problem(
         B=B, H=H, d=d, S=S, n_chunks=n_chunks, topk=topk, Hr=Hr, D=D,
         score_scale=1.0 / math.sqrt(D) if score_scale is None else score_scale,
@@ -124,6 +128,7 @@ def problem(B, H, n_chunks, topk, D=None, Hr=1, d=64, S=64, score_scale=None, at
         dtype={"fp32": GCA_FP32, "bf16": GCA_BF16}[dtype] if isinstance(dtype, str) else dtype,
         mode={"causal": GCA_CAUSAL, "decode": GCA_DECODE}[mode] if isinstance(mode, str) else mode,
         flags=flags,
+        gumbel_seed=0 if gumbel_seed is None else int(gumbel_seed),
     )
 
 

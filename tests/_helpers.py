@@ -48,15 +48,19 @@ def max_abs_rel(x, ref):
     return float(diff / scale) if scale > 0 else float(diff)
 
 
+def _gumbel(w):
+    return w.gumbel_seed if w.gumbel_seed >= 0 else None
+
+
 def oracle_params(w, off_by_one=False):
     return dict(S=w.S, topk=w.topk, score_scale=w.score_scale, attn_scale=w.attn_scale,
-                mode=w.mode, off_by_one=off_by_one)
+                mode=w.mode, off_by_one=off_by_one, gumbel_seed=_gumbel(w))
 
 
 def problem_for(w, off_by_one=False, flags=0):
     from paper_2410_01651_amd import gca
     return gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode,
-                       off_by_one=off_by_one, flags=flags)
+                       off_by_one=off_by_one, flags=flags, gumbel_seed=_gumbel(w))
 
 
 def upload(w, inp, dev):

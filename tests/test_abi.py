@@ -37,9 +37,11 @@ def test_exports_every_declared_symbol(gca):
 
 
 def test_problem_struct_layout(gca):
-    assert ctypes.sizeof(gca.Problem) == 64
+    # the layout api.cpp asserts for gca_problem
+    assert ctypes.sizeof(gca.Problem) == 72
     assert gca.Problem.n_chunks.offset == 16
     assert gca.Problem.flags.offset == 56
+    assert gca.Problem.gumbel_seed.offset == 64
 
 
 def test_status_strings(gca):

@@ -291,3 +291,45 @@ def test_decode_xattn_only_entry_point(dev, dtype):
     assert max_abs_rel(host64(lse), l_ref) <= tol
     assert max_abs_rel(host64(wt), w_ref) <= 1e-5
     assert not np.any(host64(out)[1, 1])          # the empty row's output is zero
+
+
+GUMBEL = [
+    # name, overrides, problem flags: every selection path with Gumbel top-k
+    ("train_16k_bf16", dict(B=2, H=2, n_chunks=70, topk=5, gumbel_seed=11), "materialize"),
+    ("train_16k_bf16", dict(B=1, H=2, n_chunks=300, topk=8, gumbel_seed=12, dtype="fp32"), "fused"),
+    ("planted_1m_bf16", dict(H=2, n_chunks=500, topk=8, gumbel_seed=13), "fused"),
+    ("decode_16m_bf16", dict(H=2, n_chunks=3001, topk=8, gumbel_seed=14, device_kv=False), None),
+    ("decode_16m_bf16", dict(H=1, D=64, n_chunks=40000, topk=4, gumbel_seed=15, device_kv=False), None),
+]
+
+
+@pytest.mark.parametrize("name,kw,path", GUMBEL)
+def test_gumbel_forward(dev, name, kw, path):
+    """Gumbel top-k selection: the noisy ranking reproduces the oracle's indices
+    exactly (margins enforced on the noisy scores) while sel, w and the outputs
+    use the raw scores."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case(name, **kw)
+    t = upload(w, inp, dev)
+    flags = {"materialize": gca.FLAG_MATERIALIZE, "fused": gca.FLAG_FUSED_TOPK, None: 0}[path]
+    f = gca.forward(problem_for(w, flags=flags), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    ref = _check_forward(w, inp, f)
+    plain = og.topk(ref["scores"], w.topk)[0]
+    assert not np.array_equal(plain, ref["idx"]), "the noise changed no selection"
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_gumbel_topk_entry_point(dev, dtype):
+    """gca_topk with Gumbel selection over a score matrix: exact indices, and sel
+    holds the raw matrix entries."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w, inp = _case("train_16k_bf16", B=1, H=2, n_chunks=200, topk=8, dtype=dtype, gumbel_seed=21)
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    sc = gca.chunk_scores(p, t["lmk_q"], t["lmk_k"])
+    idx, sel = gca.topk(p, sc)
+    r = sc.double().cpu().numpy()
+    ri, rs = og.topk(r, w.topk, gumbel_seed=w.gumbel_seed)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ri)
+    np.testing.assert_array_equal(sel.cpu().numpy(), rs.astype(np.float32))

@@ -40,7 +40,8 @@ def _oracle_rows(w, inp, rows, b=0, hr=0):
     lq = gi.decode(w, inp["lmk_q"][b:b + 1, hr:hr + 1])
     lk = gi.decode(w, inp["lmk_k"][b:b + 1, hr:hr + 1])
     r = og.scores(lq, lk, w.score_scale, w.mode, rows=rows)
-    idx, sel = og.topk(r, w.topk)
+    seed = w.gumbel_seed if w.gumbel_seed >= 0 else None
+    idx, sel = og.topk(r, w.topk, seed, rows=rows, bhr0=b * w.Hr + hr)
     return idx[0, 0], sel[0, 0], og.fusion_weights(sel)[0, 0]
 
 
@@ -192,15 +193,16 @@ def test_decode_16m(dev):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("n_chunks,topk", [(150_000, 8), (600_000, 16), (1_100_000, 32), (300_000, 4)])
-def test_decode_long_scan_ranges(dev, n_chunks, topk):
+@pytest.mark.parametrize("n_chunks,topk,gumbel", [(150_000, 8, -1), (600_000, 16, -1), (1_100_000, 32, -1),
+                                                  (300_000, 4, -1), (300_000, 4, 31), (150_000, 8, 32)])
+def test_decode_long_scan_ranges(dev, n_chunks, topk, gumbel):
     """Decode scans whose lanes see 3, 10 and 17 keys (all kept, in 4, 16 and 32
-    registers) and 5 keys with k = 4 (a running best-4 list per lane): one head,
-    D = 64, the planted chunk retrieved, indices exact, output against the oracle
-    over the gathered chunks."""
+    registers) and 5 keys with k = 4 (a running best-4 list per lane), the last
+    two also with Gumbel top-k: one head, D = 64, the planted chunk retrieved,
+    indices exact, output against the oracle over the gathered chunks."""
     import torch
     from paper_2410_01651_amd import gca
-    w = get_workload("decode_16m_bf16", H=1, n_chunks=n_chunks, topk=topk)
+    w = get_workload("decode_16m_bf16", H=1, n_chunks=n_chunks, topk=topk, gumbel_seed=gumbel)
     inp, _ = margins.checked_inputs(w, tokens=False)
     t = {"lmk_q": to_dev(w.dtype, inp["lmk_q"], dev), "lmk_k": to_dev(w.dtype, inp["lmk_k"], dev)}
     t.update(gi.device_kv(w, dev))
