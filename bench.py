@@ -184,10 +184,10 @@ def bench_train(args, dev, gca):
     wsf, _ = gca.workspace(p, gca.OP_FORWARD, dev)
     wsb, _ = gca.workspace(p, gca.OP_BACKWARD, dev)
 
-    def step():
-        gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"], out=fo["out"], idx=fo["idx"],
+    def step(pp=p):
+        gca.forward(pp, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"], out=fo["out"], idx=fo["idx"],
                     sel=fo["sel"], lse=fo["lse"], w=fo["w"], ws=wsf)
-        gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], fo["idx"], fo["sel"], fo["lse"], t["dout"],
+        gca.grouped_xattn_bwd(pp, t["q"], t["k"], t["v"], fo["idx"], fo["sel"], fo["lse"], t["dout"],
                               t["lmk_q"], t["lmk_k"], ws=wsb, grads=grads)
 
     stream = torch.cuda.current_stream()
@@ -206,8 +206,17 @@ def bench_train(args, dev, gca):
     # the same K steps again with every kernel's dispatch carrying start/stop events
     prof_ms, per = kernel_times(step, args.steps, stream, gca)
     print(f"[bench] profiled {args.steps} steps: {prof_ms / args.steps:.3f} ms/step", file=sys.stderr, flush=True)
-
     idx_host = fo["idx"].cpu().numpy()
+    # the Gumbel top-k variant of the same step (noise in the selection only)
+    pg = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, gumbel_seed=1)
+    step(pg)
+    g_ms = timed(lambda: step(pg), args.steps, stream) / args.steps
+    _, g_per = kernel_times(lambda: step(pg), args.steps, stream, gca)
+    gumbel = {"value": w.B * w.Lq / (g_ms * 1e-3), "unit": "tokens/s", "ms_per_step": g_ms,
+              "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()
+                          if k in ("chunk_scores_kernel", "topk_kernel")}}
+    print(f"[bench] gumbel top-k {args.steps} steps: {g_ms:.3f} ms/step", file=sys.stderr, flush=True)
+
     units = valid_units(idx_host, w)
     fpu = flops_per_unit()
     kern = {}
@@ -230,6 +239,7 @@ def bench_train(args, dev, gca):
     algo_fl = units * S * (fpu["xattn_fwd_kernel"] + 5 * 2 * S * DH)
     return {
         "w": w, "t": t, "tokens": tokens, "ms_step": ms_step, "profiled_ms_step": prof_ms / args.steps,
+        "gumbel": gumbel,
         "kernels": kern, "roofline": roof,
         "units": units, "path_tflops": algo_fl / (ms_step * 1e-3) / 1e12,
     }
@@ -297,8 +307,8 @@ def bench_decode(args, dev, gca):
     ws, _ = gca.workspace(p, gca.OP_FORWARD, dev)
     it = [0]
 
-    def call():
-        gca.forward(p, lmk_q, keys[it[0] % 2], q, kv["k"], kv["v"], out=out, idx=idx, sel=sel, lse=lse, w=wts,
+    def call(pp=p):
+        gca.forward(pp, lmk_q, keys[it[0] % 2], q, kv["k"], kv["v"], out=out, idx=idx, sel=sel, lse=lse, w=wts,
                     ws=ws)
         it[0] += 1
 
@@ -311,6 +321,11 @@ def bench_decode(args, dev, gca):
     prof_ms, per = kernel_times(call, steps, stream, gca)
     planted = int(gi.plant_positions(w)[0])
     found = planted in idx.cpu().numpy().ravel().tolist()
+    # the Gumbel top-k variant of the same call
+    pg = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, gumbel_seed=1)
+    call(pg)
+    g_ms = timed(lambda: call(pg), steps, stream) / steps
+    _, g_per = kernel_times(lambda: call(pg), steps, stream, gca)
     key_bytes = w.n_chunks * w.Dl * 2
     kv_bytes = 2 * w.topk * w.H * S * DH * 2
     io_bytes = 2 * w.H * S * DH * 2 + w.Dl * 2
@@ -333,6 +348,8 @@ def bench_decode(args, dev, gca):
                      "traffic": measured_traffic("decode_scan_kernel@decode_16m"),
                      "algorithmic_bytes_per_launch": key_bytes, "avg_launch_ms": scan_ms},
         "kernels": kern,
+        "gumbel_topk": {"value": total_bytes / (g_ms * 1e-3) / 1e9, "unit": "GB/s", "ms_per_call": g_ms,
+                        "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()}},
     }
 
 
@@ -395,6 +412,7 @@ def main():
                    "global_batch": w.B, "seq_len": w.Lq, "parallelism": "none (1 GPU)"},
         "roofline": tr["roofline"],
         "path_algorithmic_tflops": tr["path_tflops"],
+        "gumbel_topk": tr["gumbel"],
         "kernels": tr["kernels"],
     }
     if not args.no_cpu_baseline:

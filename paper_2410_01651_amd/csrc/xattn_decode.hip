@@ -104,9 +104,23 @@ __global__ __launch_bounds__(kDecThreads) void xattn_decode_kernel(DecParams p) 
       const int rank = rank_by_chunk(mj, cnt);  // slots in ascending chunk order
       float mx;
       if (p.gumbel) {
+        // raw scores of the chosen chunks: 8 lanes per chunk, each one eighth of
+        // the D columns, summed over the 8 lanes
         const T* lq = reinterpret_cast<const T*>(p.lmk_q) + row * p.D;
-        const T* lk = reinterpret_cast<const T*>(p.lmk_k) + (row * p.nKV + (valid ? mj : 0)) * p.D;
-        ms = valid ? p.score_scale * dot_rows(lq, lk, p.D) : -INFINITY;
+        const int part = p.D / 8, sub = lane & 7;
+        float raw = -INFINITY;
+        for (int e0 = 0; e0 < cnt; e0 += 8) {
+          const int e = e0 + (lane >> 3);
+          const int je = __shfl(mj, e < cnt ? e : 0);
+          const T* lk = reinterpret_cast<const T*>(p.lmk_k) + (row * p.nKV + (e < cnt ? je : 0)) * p.D;
+          float acc = dot_rows(lq + sub * part, lk + sub * part, part);
+          acc += dpp<kDppXor1>(acc);
+          acc += dpp<kDppXor2>(acc);
+          acc += dpp<kDppHalfMirror>(acc);
+          const float mine = __shfl(acc, 8 * ((lane - e0) & 7));  // chunk `lane` of this group of 8
+          if (lane >= e0 && lane < e0 + 8) raw = p.score_scale * mine;
+        }
+        ms = valid ? raw : -INFINITY;
         mx = max64(ms);
       } else {
         // the list is best first: lane 0 holds the maximum
