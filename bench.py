@@ -353,6 +353,54 @@ def bench_decode(args, dev, gca):
     }
 
 
+def bench_decode_host_kv(args, dev, gca):
+    """Decode with the past chunks' K/V offloaded to pinned host memory (landmarks,
+    q and outputs in HBM): the decode attention gathers the k retrieved chunks over
+    the host link.  1M past tokens (16,384 chunks, 2 x 1.07 GB of host K/V)."""
+    import torch
+    from gen import get_workload, inputs as gi
+
+    w = get_workload("decode_16m_bf16", n_chunks=16384)
+    lq, lk = landmarks(w)
+    lmk_q, lmk_k = upload(w, lq, dev), upload(w, lk, dev)
+    kv = gi.device_kv(w, dev)
+    host = {n: torch.empty(kv[n].shape, dtype=kv[n].dtype, pin_memory=True) for n in ("k", "v")}
+    for n in ("k", "v"):
+        host[n].copy_(kv[n])
+    q = gi.device_tensors(w, ("q",), dev)["q"]
+    sh = gca.shapes(gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, mode=w.mode))
+    out = torch.empty(sh.q, dtype=torch.bfloat16, device=dev)
+    idx = torch.empty(sh.rows, dtype=torch.int32, device=dev)
+    sel = torch.empty(sh.rows, dtype=torch.float32, device=dev)
+    lse = torch.empty(sh.lse, dtype=torch.float32, device=dev)
+    wts = torch.empty(sh.rows, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    res = {}
+    for where, flags, k, v in (("device", 0, kv["k"], kv["v"]), ("host", gca.FLAG_HOST_KV, host["k"], host["v"])):
+        p = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, flags=flags)
+        ws, _ = gca.workspace(p, gca.OP_FORWARD, dev)
+
+        def call():
+            gca.forward(p, lmk_q, lmk_k, q, k, v, out=out, idx=idx, sel=sel, lse=lse, w=wts, ws=ws)
+
+        for _ in range(5):
+            call()
+        ms = timed(call, args.decode_steps, stream) / args.decode_steps
+        _, per = kernel_times(call, args.decode_steps, stream, gca)
+        res[where] = {"ms_per_call": ms, "kernels": {n: {"avg_ms": sum(d) / len(d)} for n, d in per.items()}}
+    gathered = 2 * w.topk * w.H * S * DH * 2      # K and V tiles of the retrieved chunks, every head
+    att_host = res["host"]["kernels"]["xattn_decode_kernel"]["avg_ms"]
+    att_dev = res["device"]["kernels"]["xattn_decode_kernel"]["avg_ms"]
+    del kv, host
+    torch.cuda.empty_cache()
+    return {"config": {"workload": "decode with host-resident K/V: B=1 H=8 d=64, 1,048,576 past tokens "
+                                   "(16,384 chunks), S=64, top-8, D=512, bf16; K/V in pinned host memory"},
+            "ms_per_call": res["host"]["ms_per_call"], "ms_per_call_device_kv": res["device"]["ms_per_call"],
+            "host_link_bytes_per_call": gathered,
+            "host_link_GBps": gathered / ((att_host - att_dev) * 1e-3) / 1e9 if att_host > att_dev else None,
+            "kernels": res["host"]["kernels"], "kernels_device_kv": res["device"]["kernels"]}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -361,6 +409,7 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-host-kv", action="store_true", help="skip the decode leg with host-resident K/V")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="first run one plain device copy of this many MiB (a known-size reference for "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -391,7 +440,10 @@ def main():
         del src, dst
 
     if args.only == "decode":
-        print(json.dumps({"decode_scan": bench_decode(args, dev, gca)}), flush=True)
+        line = {"decode_scan": bench_decode(args, dev, gca)}
+        if not args.no_host_kv:
+            line["decode_host_kv"] = bench_decode_host_kv(args, dev, gca)
+        print(json.dumps(line), flush=True)
         return
     if args.only == "train":
         args.no_decode = True
@@ -423,6 +475,9 @@ def main():
     if not args.no_decode:
         print("[bench] decode scan at 16M context", file=sys.stderr, flush=True)
         line["decode_scan"] = bench_decode(args, dev, gca)
+        if not args.no_host_kv:
+            print("[bench] decode with host-resident K/V at 1M context", file=sys.stderr, flush=True)
+            line["decode_host_kv"] = bench_decode_host_kv(args, dev, gca)
     print(json.dumps(line), flush=True)
 
 

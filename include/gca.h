@@ -66,6 +66,14 @@ typedef enum { GCA_CAUSAL = 0, GCA_DECODE = 1 } gca_mode;
 /* Problem flags (gca_problem.flags). */
 #define GCA_FLAG_FUSED_TOPK 1u   /* gca_forward, CAUSAL: score and select in one pass (no score matrix) */
 #define GCA_FLAG_MATERIALIZE 2u  /* gca_forward, CAUSAL: always write the score matrix, then select */
+#define GCA_FLAG_HOST_KV 8u      /* DECODE: k and v are pinned host allocations (hipHostMalloc),
+                                  * the past chunks offloaded to CPU memory (Training &
+                                  * Inference, "Memory Offloading"); landmarks, q and every
+                                  * output stay in device memory.  The decode attention reads
+                                  * the k retrieved chunks straight from host memory over the
+                                  * host link (their device mapping, hipHostGetDevicePointer).
+                                  * GCA_ERR_INVALID if k or v has no device mapping, or in
+                                  * CAUSAL mode. */
 #define GCA_FLAG_GUMBEL 4u       /* Gumbel top-k selection (Training & Inference, "Gumbel Top-k
                                   * sampling"): every selection (gca_topk, gca_forward in both
                                   * modes) ranks score + g, g = -ln(-ln u) with u from the

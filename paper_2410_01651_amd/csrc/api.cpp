@@ -56,8 +56,10 @@ gca_status check_problem(const gca_problem* p, gca::Shape& s) {
   if (p->off_by_one != 0 && p->off_by_one != 1) return fail(GCA_ERR_INVALID, "off_by_one must be 0 or 1");
   if (!std::isfinite(p->score_scale) || !std::isfinite(p->attn_scale))
     return fail(GCA_ERR_INVALID, "scales must be finite");
-  if (p->flags & ~(GCA_FLAG_FUSED_TOPK | GCA_FLAG_MATERIALIZE | GCA_FLAG_GUMBEL))
+  if (p->flags & ~(GCA_FLAG_FUSED_TOPK | GCA_FLAG_MATERIALIZE | GCA_FLAG_GUMBEL | GCA_FLAG_HOST_KV))
     return fail(GCA_ERR_INVALID, "unknown flag bits");
+  if ((p->flags & GCA_FLAG_HOST_KV) && p->mode != GCA_DECODE)
+    return fail(GCA_ERR_INVALID, "GCA_FLAG_HOST_KV is for DECODE mode");
   if ((p->flags & GCA_FLAG_FUSED_TOPK) && (p->flags & GCA_FLAG_MATERIALIZE))
     return fail(GCA_ERR_INVALID, "GCA_FLAG_FUSED_TOPK and GCA_FLAG_MATERIALIZE are exclusive");
   s.B = p->B;
@@ -77,6 +79,21 @@ gca_status check_problem(const gca_problem* p, gca::Shape& s) {
   const int64_t BH = (int64_t)s.B * s.H;
   if (BH > kMaxGrid / s.nQ || BH > kMaxGrid / s.nKV || (int64_t)s.B * s.Hr * s.nQ > kMaxGrid / s.topk)
     return fail(GCA_ERR_UNSUPPORTED, "problem too large for one launch");
+  return GCA_OK;
+}
+
+// With GCA_FLAG_HOST_KV, k and v are pinned host allocations: the kernels use
+// their device mapping.
+gca_status device_view(const gca_problem* p, const void*& ptr, const char* name) {
+  if (!(p->flags & GCA_FLAG_HOST_KV) || !ptr) return GCA_OK;
+  void* dev = nullptr;
+  const hipError_t e = hipHostGetDevicePointer(&dev, const_cast<void*>(ptr), 0);
+  if (e != hipSuccess || !dev) {
+    (void)hipGetLastError();
+    return fail(GCA_ERR_INVALID, std::string(name) + " is not pinned host memory with a device mapping "
+                                                      "(GCA_FLAG_HOST_KV needs hipHostMalloc allocations)");
+  }
+  ptr = dev;
   return GCA_OK;
 }
 
@@ -220,6 +237,8 @@ gca_status gca_grouped_xattn_fwd(const gca_problem* p, const void* q, const void
   GCA_TRY(check_ptr(out, "out", true, 16));
   GCA_TRY(check_ptr(lse, "lse", false, 4));
   GCA_TRY(check_ptr(w, "w", false, 4));
+  GCA_TRY(device_view(p, k, "k"));
+  GCA_TRY(device_view(p, v, "v"));
   (void)hipGetLastError();
   (void)gca::take_launch_error();
   return from_hip(gca::launch_xattn_fwd(s, q, k, v, idx, sel, out, lse, w, stream), "gca_grouped_xattn_fwd");
@@ -251,6 +270,8 @@ gca_status gca_grouped_xattn_bwd(const gca_problem* p, const void* q, const void
   GCA_TRY(check_ptr(lmk_q, "lmk_q", dlmk_k != nullptr, 16));
   GCA_TRY(check_ptr(lmk_k, "lmk_k", dlmk_q != nullptr, 16));
   GCA_TRY(check_ws(workspace, ws_bytes, gca::bwd_workspace(s)));
+  GCA_TRY(device_view(p, k, "k"));
+  GCA_TRY(device_view(p, v, "v"));
   (void)hipGetLastError();
   (void)gca::take_launch_error();
   return from_hip(gca::launch_xattn_bwd(s, q, k, v, idx, sel, lse, dout, dq, dk, dv, dsel, lmk_q, lmk_k, dlmk_q,
@@ -274,6 +295,8 @@ gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_
   GCA_TRY(check_ptr(lse, "lse", false, 4));
   GCA_TRY(check_ptr(w, "w", false, 4));
   GCA_TRY(check_ws(workspace, ws_bytes, forward_ws(p, s)));
+  GCA_TRY(device_view(p, k, "k"));
+  GCA_TRY(device_view(p, v, "v"));
   (void)hipGetLastError();
   (void)gca::take_launch_error();
   hipError_t e;

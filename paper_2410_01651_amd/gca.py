@@ -31,7 +31,7 @@ EXPORTS = (
 GCA_OK, GCA_ERR_INVALID, GCA_ERR_UNSUPPORTED, GCA_ERR_WORKSPACE, GCA_ERR_HIP = range(5)
 GCA_FP32, GCA_BF16 = 0, 1
 GCA_CAUSAL, GCA_DECODE = 0, 1
-FLAG_FUSED_TOPK, FLAG_MATERIALIZE, FLAG_GUMBEL = 1, 2, 4
+FLAG_FUSED_TOPK, FLAG_MATERIALIZE, FLAG_GUMBEL, FLAG_HOST_KV = 1, 2, 4, 8
 OP_FORWARD, OP_BACKWARD = 0, 1
 
 
@@ -144,11 +144,11 @@ def _elem_dtype(p: Problem):
     return torch.bfloat16 if p.dtype == GCA_BF16 else torch.float32
 
 
-def _ptr(t, name, dtype=None, shape=None):
+def _ptr(t, name, dtype=None, shape=None, host_ok=False):
     if t is None:
         return None
-    if not t.is_cuda:
-        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_cuda and not (host_ok and t.is_pinned()):
+        raise ValueError(f"{name} must be a device tensor" + (" or a pinned host tensor" if host_ok else ""))
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype != dtype:
@@ -156,6 +156,10 @@ def _ptr(t, name, dtype=None, shape=None):
     if shape is not None and tuple(t.shape) != tuple(shape):
         raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _host_kv(p: Problem) -> bool:
+    return bool(p.flags & FLAG_HOST_KV)
 
 
 def _stream(stream):
@@ -234,7 +238,8 @@ def grouped_xattn_fwd(p: Problem, q, k, v, idx, sel, out=None, lse=None, w=None,
     if w is None and want_w:
         w = torch.empty(sh.rows, dtype=torch.float32, device=dev)
     _check(lib().gca_grouped_xattn_fwd(
-        ctypes.byref(p), _ptr(q, "q", dt, sh.q), _ptr(k, "k", dt, sh.kv), _ptr(v, "v", dt, sh.kv),
+        ctypes.byref(p), _ptr(q, "q", dt, sh.q),
+        _ptr(k, "k", dt, sh.kv, _host_kv(p)), _ptr(v, "v", dt, sh.kv, _host_kv(p)),
         _ptr(idx, "idx", torch.int32, sh.rows), _ptr(sel, "sel", torch.float32, sh.rows),
         _ptr(out, "out", dt, sh.q), _ptr(lse, "lse", torch.float32, sh.lse),
         _ptr(w, "w", torch.float32, sh.rows), _stream(stream)))
@@ -260,7 +265,8 @@ def grouped_xattn_bwd(p: Problem, q, k, v, idx, sel, lse, dout, lmk_q=None, lmk_
     else:
         nbytes = ws.numel()
     _check(lib().gca_grouped_xattn_bwd(
-        ctypes.byref(p), _ptr(q, "q", dt, sh.q), _ptr(k, "k", dt, sh.kv), _ptr(v, "v", dt, sh.kv),
+        ctypes.byref(p), _ptr(q, "q", dt, sh.q),
+        _ptr(k, "k", dt, sh.kv, _host_kv(p)), _ptr(v, "v", dt, sh.kv, _host_kv(p)),
         _ptr(idx, "idx", torch.int32, sh.rows), _ptr(sel, "sel", torch.float32, sh.rows),
         _ptr(lse, "lse", torch.float32, sh.lse), _ptr(dout, "dout", dt, sh.q),
         _ptr(g["dq"], "dq", dt, sh.q), _ptr(g["dk"], "dk", dt, sh.kv), _ptr(g["dv"], "dv", dt, sh.kv),
@@ -295,7 +301,8 @@ def forward(p: Problem, lmk_q, lmk_k, q, k, v, out=None, idx=None, sel=None, lse
         nbytes = ws.numel()
     _check(lib().gca_forward(
         ctypes.byref(p), _ptr(lmk_q, "lmk_q", dt, sh.lmk_q), _ptr(lmk_k, "lmk_k", dt, sh.lmk_k),
-        _ptr(q, "q", dt, sh.q), _ptr(k, "k", dt, sh.kv), _ptr(v, "v", dt, sh.kv),
+        _ptr(q, "q", dt, sh.q),
+        _ptr(k, "k", dt, sh.kv, _host_kv(p)), _ptr(v, "v", dt, sh.kv, _host_kv(p)),
         _ptr(out, "out", dt, sh.q), _ptr(idx, "idx", torch.int32, sh.rows),
         _ptr(sel, "sel", torch.float32, sh.rows), _ptr(lse, "lse", torch.float32, sh.lse),
         _ptr(w, "w", torch.float32, sh.rows), _ptr(ws, "workspace"), ctypes.c_size_t(nbytes),

@@ -86,7 +86,7 @@ def _fwd_call(gca, p, **override):
     ("d", 32, "UNSUPPORTED"), ("S", 128, "UNSUPPORTED"), ("topk", 0, "INVALID"),
     ("topk", 33, "UNSUPPORTED"), ("Hr", 3, "INVALID"), ("D", 96, "UNSUPPORTED"), ("D", 0, "INVALID"),
     ("n_chunks", 0, "INVALID"), ("B", 0, "INVALID"), ("dtype", 5, "INVALID"), ("mode", 2, "INVALID"),
-    ("off_by_one", 2, "INVALID"), ("flags", 3, "INVALID"), ("flags", 8, "INVALID"),
+    ("off_by_one", 2, "INVALID"), ("flags", 3, "INVALID"), ("flags", 8, "INVALID"), ("flags", 16, "INVALID"),
     ("attn_scale", math.inf, "INVALID"),
 ])
 def test_invalid_problem_rejected(gca, field, value, status):
@@ -142,3 +142,15 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(g, "_lib", None)
     with pytest.raises(RuntimeError, match="not built"):
         g.lib()
+
+
+def test_host_kv_rules(gca):
+    """Host-resident K/V is a DECODE option, and k/v must be pinned host memory
+    with a device mapping (an arbitrary address is rejected before any launch)."""
+    causal = gca.problem(1, 2, 64, 8, flags=gca.FLAG_HOST_KV)
+    st, msg = _fwd_call(gca, causal)
+    assert st == gca.GCA_ERR_INVALID and "DECODE" in msg
+    dec = gca.problem(1, 2, 64, 8, mode="decode", flags=gca.FLAG_HOST_KV)
+    ws = ctypes.c_void_p(1 << 24)
+    st, msg = _fwd_call(gca, dec, ws=ws, nbytes=gca.workspace_size(dec, gca.OP_FORWARD))
+    assert st == gca.GCA_ERR_INVALID and "pinned host memory" in msg

@@ -333,3 +333,30 @@ def test_gumbel_topk_entry_point(dev, dtype):
     ri, rs = og.topk(r, w.topk, gumbel_seed=w.gumbel_seed)
     np.testing.assert_array_equal(idx.cpu().numpy(), ri)
     np.testing.assert_array_equal(sel.cpu().numpy(), rs.astype(np.float32))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_decode_host_kv(dev, dtype):
+    """Decode with the K/V cache in pinned host memory (GCA_FLAG_HOST_KV): the
+    attention gathers the retrieved chunks over the host link and gives exactly
+    what the device-resident cache gives; the oracle agrees; unpinned host
+    tensors are refused."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w, inp = _case("decode_16m_bf16", H=2, n_chunks=3000, topk=8, dtype=dtype, device_kv=False)
+    t = upload(w, inp, dev)
+    kh = torch.empty(t["k"].shape, dtype=t["k"].dtype, pin_memory=True)
+    vh = torch.empty(t["v"].shape, dtype=t["v"].dtype, pin_memory=True)
+    kh.copy_(t["k"].cpu())
+    vh.copy_(t["v"].cpu())
+    f_dev = gca.forward(problem_for(w), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    ph = problem_for(w, flags=gca.FLAG_HOST_KV)
+    f_host = gca.forward(ph, t["lmk_q"], t["lmk_k"], t["q"], kh, vh)
+    torch.cuda.synchronize()
+    for key in ("idx", "sel", "w", "out", "lse"):
+        assert torch.equal(f_dev[key], f_host[key]), key
+    _check_forward(w, inp, f_host)
+    out, lse, wt = gca.grouped_xattn_fwd(ph, t["q"], kh, vh, f_host["idx"], f_host["sel"])
+    assert torch.equal(out, f_dev["out"]) and torch.equal(lse, f_dev["lse"])
+    with pytest.raises(ValueError):
+        gca.forward(ph, t["lmk_q"], t["lmk_k"], t["q"], t["k"].cpu(), t["v"].cpu())
