@@ -360,3 +360,29 @@ def test_decode_host_kv(dev, dtype):
     assert torch.equal(out, f_dev["out"]) and torch.equal(lse, f_dev["lse"])
     with pytest.raises(ValueError):
         gca.forward(ph, t["lmk_q"], t["lmk_k"], t["q"], t["k"].cpu(), t["v"].cpu())
+
+
+def test_selection_reused_by_layers(dev):
+    """One selection (gca_topk) serves several layers of a group: each layer runs
+    gca_grouped_xattn_fwd / _bwd with its own q, k, v on the same idx / sel."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w, inp = _case("train_16k_bf16", B=1, H=2, n_chunks=40, topk=4)
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    idx, sel = gca.topk(p, gca.chunk_scores(p, t["lmk_q"], t["lmk_k"]))
+    x = decode_all(w, inp)
+    ref = og.forward(oracle_params(w), x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"])
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref["idx"])
+    for layer in range(1, 3):
+        lw = get_workload("train_16k_bf16", B=1, H=2, n_chunks=40, topk=4, seed=100 + layer)
+        tok = gi.draw_tokens(lw, with_dout=True)
+        tt = upload(lw, tok, dev)
+        out, lse, wt = gca.grouped_xattn_fwd(p, tt["q"], tt["k"], tt["v"], idx, sel)
+        y = decode_all(lw, tok)
+        o_ref, l_ref = og.xattn_fwd(y["q"], y["k"], y["v"], ref["idx"], ref["w"], w.S, w.attn_scale)
+        assert max_abs_rel(host64(out), o_ref) <= TOL[w.dtype], layer
+        g = gca.grouped_xattn_bwd(p, tt["q"], tt["k"], tt["v"], idx, sel, lse, tt["dout"], landmark_grads=False)
+        dq, dk, dv, _ = og.xattn_bwd(y["q"], y["k"], y["v"], ref["idx"], ref["w"], y["dout"], w.S, w.attn_scale)
+        for key, r in (("dq", dq), ("dk", dk), ("dv", dv)):
+            assert max_abs_rel(host64(g[key]), r) <= TOL[w.dtype], (layer, key)
