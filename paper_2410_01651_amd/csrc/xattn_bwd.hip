@@ -29,8 +29,8 @@ constexpr int kThreads = 256;  // two pairs of waves
 
 struct Ws {
   float* w;        // [B*Hr, nQ, K] fusion weights
-  float* Dbuf;     // [B*H, Lq, K]  D_s per query token
-  float* Lbuf;     // [B*H, Lq, K]  log2 of 1 / (w_s exp(-lse)): log2(e) lse - log2(w_s)
+  float* Dbuf;     // [B*H, K, Lq]  D_s per query token (slot-major: one slot's tokens contiguous)
+  float* Lbuf;     // [B*H, K, Lq]  log2 of 1 / (w_s exp(-lse)): log2(e) lse - log2(w_s)
   float* dwp;      // [B*H, nQ, K, 2] dw partials per head and query half
   int* counts;     // [B*Hr, nKV]
   int* cursor;     // [B*Hr, nKV]
@@ -268,6 +268,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_
     if (lane == 0) sN[pair][buf] = __popcll(mask);
   };
   auto tok_of = [&](const Geo& g) -> int64_t { return ((g.b * p.H + g.h) * p.nQ + g.c) * kS; };
+  const int64_t lq_len = p.nQ * kS;  // query tokens per (batch, head)
 
   // ---- prologue
   Frag<T> qf[4], df[4];  // the current chunk's Q and dO rows of this lane's query
@@ -332,7 +333,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_
   }
 
   f32x16 g0a = zero16(), g1a = zero16();  // dQ^T, d rows 0-31 / 32-63
-  auto run = [&](int slot, int u, float lse_q, int64_t tok0, int64_t t) __device__ {
+  // cbase: element of (this slice, slot 0, this chunk's first token) in Dbuf / Lbuf
+  auto run = [&](int slot, int u, float lse_q, int64_t cbase, int64_t t) __device__ {
     const uint32_t co = (uint32_t)slot * 2 * kTileB;
     const int s = __builtin_amdgcn_readlane(ls, u);
     const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lw), u));
@@ -389,8 +391,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_
     }
     // D_s and the shifted lse of this (query, slot) for the key-stationary pass
     if (hh == 0) {
-      p.ws.Dbuf[(tok0 + qi) * K + s] = Dq;
-      p.ws.Lbuf[(tok0 + qi) * K + s] = lse_q * kLog2e - __builtin_amdgcn_logf(ws);
+      p.ws.Dbuf[cbase + s * lq_len + qi] = Dq;
+      p.ws.Lbuf[cbase + s * lq_len + qi] = lse_q * kLog2e - __builtin_amdgcn_logf(ws);
     }
     // this wave's 32 queries' share of dw[t, s]
     const float dsum = sum32(Dq);
@@ -402,6 +404,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_
     const int buf = (int)(ci & 1);
     const int n = live ? sN[pair][buf] : 0;
     const int64_t tok0 = tok_of(g0);
+    const int64_t cbase = (g0.b * p.H + g0.h) * K * lq_len + g0.c * kS;
     const int64_t tglob = (g0.b * p.H + g0.h) * p.nQ + (p.causal ? g0.c - 1 : 0);  // dw row (b, h, t)
     const int64_t tok_n = tok_of(g1);
     for (int u = 0; u < K; ++u) {
@@ -432,7 +435,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_
         lse_next = p.lse[(tok_n + qi) * K + sSlot[pair][buf ^ 1][0]];
       }
       if (comp) {
-        run(cs, u, lse_q, tok0, tglob);
+        run(cs, u, lse_q, cbase, tglob);
         cs ^= 1;
       }
       // the next chunk's Q and dO rows arrive with the copies of its first item
@@ -523,7 +526,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
   const float* Db = p.ws.Dbuf + bh * p.nQ * kS * K;
 
   const TileCopy<T, 4> cp(wave, lane);
-  const uint32_t col_off = (uint32_t)(lane * K * sizeof(float));
+  const uint32_t col_off = (uint32_t)(lane * sizeof(float));
+  const int64_t lq_len = p.nQ * kS;
   auto issue = [&](int slot, int u) __device__ {
     const int cs = sE[u];  // (query chunk << 5) | slot
     const int64_t c = cs >> 5;
@@ -532,8 +536,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
     cp.issue(qb + c * TILE, dst);
     cp.issue(ob + c * TILE, dst + TILE);
     float* cols = reinterpret_cast<float*>(dst + 2 * TILE);
-    if (wave == 0) dma_column_s(Lb + c * kS * K + s, col_off, cols);
-    else if (wave == 1) dma_column_s(Db + c * kS * K + s, col_off, cols + kS);
+    if (wave == 0) dma_column_s(Lb + s * lq_len + c * kS, col_off, cols);
+    else if (wave == 1) dma_column_s(Db + s * lq_len + c * kS, col_off, cols + kS);
   };
 
   f32x16 dv0 = zero16(), dv1 = zero16(), dk0 = zero16(), dk1 = zero16();

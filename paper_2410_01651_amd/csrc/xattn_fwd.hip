@@ -70,6 +70,11 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   __shared__ int sJc[2][2][32];
   __shared__ float sWc[2][2][32];
   __shared__ int sN[2][2];
+  // per wave, the log-sum-exp of its 32 tokens x k slots (k <= 8), stored to
+  // HBM in one contiguous run at the end of the chunk instead of k scattered
+  // 4-byte writes per token
+  constexpr int kStageK = 8;
+  __shared__ float sLse[4][32][kStageK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
@@ -248,7 +253,13 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
     for (int i = 1; i < 16; ++i) sum += st0[i] + st1[i];
     sum = sum_xor32(sum);
     if (OBO) sum += __builtin_amdgcn_exp2f(-mx);
-    if (p.lse && hh == 0) p.lse[(tok0 + qi) * K + s] = (mx + __builtin_amdgcn_logf(sum)) * kLn2;
+    if (p.lse && hh == 0) {
+      const float lv = (mx + __builtin_amdgcn_logf(sum)) * kLn2;
+      if (K <= kStageK)
+        sLse[wave][l32][s] = lv;
+      else
+        p.lse[(tok0 + qi) * K + s] = lv;
+    }
     const int coef_bits = __builtin_amdgcn_readlane(__float_as_int(lw), u);
     const float coef = __int_as_float(coef_bits) * __builtin_amdgcn_rcpf(sum);
     Frag<T> pf[4];
@@ -323,7 +334,15 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
         store4(orow + 8 * gq + 4 * hh, o0[4 * gq], o0[4 * gq + 1], o0[4 * gq + 2], o0[4 * gq + 3]);
         store4(orow + 32 + 8 * gq + 4 * hh, o1[4 * gq], o1[4 * gq + 1], o1[4 * gq + 2], o1[4 * gq + 3]);
       }
-      if (p.lse && n < K && hh == 0) {
+      if (p.lse && K <= kStageK) {
+        // this wave's tokens are one contiguous run of 32 k entries; slots
+        // without a chunk read -inf
+        const int64_t base = (tok0 + 32 * half) * K;
+        for (int e = lane; e < 32 * K; e += 64) {
+          const int tk = e / K, sl = e - tk * K;
+          p.lse[base + e] = sJ[pair][buf][sl] < 0 ? -INFINITY : sLse[wave][tk][sl];
+        }
+      } else if (p.lse && n < K && hh == 0) {
         float* lse = p.lse + (tok0 + qi) * K;
         for (int s = 0; s < K; ++s)
           if (sJ[pair][buf][s] < 0) lse[s] = -INFINITY;

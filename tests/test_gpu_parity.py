@@ -338,9 +338,9 @@ def test_gumbel_topk_entry_point(dev, dtype):
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 def test_decode_host_kv(dev, dtype):
     """Decode with the K/V cache in pinned host memory (GCA_FLAG_HOST_KV): the
-    attention gathers the retrieved chunks over the host link and gives exactly
-    what the device-resident cache gives; the oracle agrees; unpinned host
-    tensors are refused."""
+    attention (and its backward) reads the retrieved chunks over the host link and
+    gives exactly what the device-resident cache gives; the oracle agrees;
+    unpinned host tensors are refused."""
     import torch
     from paper_2410_01651_amd import gca
     w, inp = _case("decode_16m_bf16", H=2, n_chunks=3000, topk=8, dtype=dtype, device_kv=False)
@@ -358,6 +358,13 @@ def test_decode_host_kv(dev, dtype):
     _check_forward(w, inp, f_host)
     out, lse, wt = gca.grouped_xattn_fwd(ph, t["q"], kh, vh, f_host["idx"], f_host["sel"])
     assert torch.equal(out, f_dev["out"]) and torch.equal(lse, f_dev["lse"])
+    dout = torch.randn(t["q"].shape, device=dev).to(t["q"].dtype)
+    g_dev = gca.grouped_xattn_bwd(problem_for(w), t["q"], t["k"], t["v"], f_dev["idx"], f_dev["sel"], f_dev["lse"],
+                                  dout, t["lmk_q"], t["lmk_k"])
+    g_host = gca.grouped_xattn_bwd(ph, t["q"], kh, vh, f_dev["idx"], f_dev["sel"], f_dev["lse"], dout,
+                                   t["lmk_q"], t["lmk_k"])
+    for key in ("dq", "dk", "dv", "dsel", "dlmk_q", "dlmk_k"):
+        assert torch.equal(g_dev[key], g_host[key]), key
     with pytest.raises(ValueError):
         gca.forward(ph, t["lmk_q"], t["lmk_k"], t["q"], t["k"].cpu(), t["v"].cpu())
 
