@@ -86,8 +86,14 @@ gca_status check_problem(const gca_problem* p, gca::Shape& s) {
 // their device mapping.
 gca_status device_view(const gca_problem* p, const void*& ptr, const char* name) {
   if (!(p->flags & GCA_FLAG_HOST_KV) || !ptr) return GCA_OK;
+  // both: the runtime knows the allocation as pinned host memory, and it has a
+  // device mapping
+  hipPointerAttribute_t attr{};
   void* dev = nullptr;
-  const hipError_t e = hipHostGetDevicePointer(&dev, const_cast<void*>(ptr), 0);
+  const hipError_t ea = hipPointerGetAttributes(&attr, ptr);
+  const hipError_t e = ea == hipSuccess && attr.type == hipMemoryTypeHost
+                           ? hipHostGetDevicePointer(&dev, const_cast<void*>(ptr), 0)
+                           : hipErrorInvalidValue;
   if (e != hipSuccess || !dev) {
     (void)hipGetLastError();
     return fail(GCA_ERR_INVALID, std::string(name) + " is not pinned host memory with a device mapping "

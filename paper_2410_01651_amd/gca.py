@@ -147,8 +147,11 @@ def _elem_dtype(p: Problem):
 def _ptr(t, name, dtype=None, shape=None, host_ok=False):
     if t is None:
         return None
-    if not t.is_cuda and not (host_ok and t.is_pinned()):
-        raise ValueError(f"{name} must be a device tensor" + (" or a pinned host tensor" if host_ok else ""))
+    # a host tensor (GCA_FLAG_HOST_KV) is checked by the library itself: it must
+    # be pinned memory with a device mapping (torch's is_pinned() query costs far
+    # more than the call it would guard)
+    if not t.is_cuda and not host_ok:
+        raise ValueError(f"{name} must be a device tensor")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype != dtype:

@@ -365,7 +365,7 @@ def test_decode_host_kv(dev, dtype):
                                    t["lmk_q"], t["lmk_k"])
     for key in ("dq", "dk", "dv", "dsel", "dlmk_q", "dlmk_k"):
         assert torch.equal(g_dev[key], g_host[key]), key
-    with pytest.raises(ValueError):
+    with pytest.raises(gca.GcaError, match="pinned host memory"):
         gca.forward(ph, t["lmk_q"], t["lmk_k"], t["q"], t["k"].cpu(), t["v"].cpu())
 
 
