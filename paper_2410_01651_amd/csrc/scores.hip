@@ -118,10 +118,9 @@ constexpr int kLoadNonTemporal = 2;  // cache policy: streamed once
 
 // Partial dot product of one lane's 8 elements of a key column block with the
 // query's (both 16 bytes of bf16, or 32 bytes of fp32 as two records).
-__device__ __forceinline__ float dot_block(const u32x4* v, const __bf16* q, float acc) {
+__device__ __forceinline__ float dot_block(const u32x4* v, const bf16x8 b, float acc) {
   typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
   const bf16x8 a = __builtin_bit_cast(bf16x8, v[0]);
-  const bf16x8 b = load_frag(q);
   acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 0, 1), __builtin_shufflevector(b, b, 0, 1),
                                         acc, false);
   acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 2, 3), __builtin_shufflevector(b, b, 2, 3),
@@ -132,8 +131,7 @@ __device__ __forceinline__ float dot_block(const u32x4* v, const __bf16* q, floa
                                         acc, false);
   return acc;
 }
-__device__ __forceinline__ float dot_block(const u32x4* v, const float* q, float acc) {
-  const f32x8 b = load_frag(q);
+__device__ __forceinline__ float dot_block(const u32x4* v, const f32x8 b, float acc) {
   const f32x4 a0 = __builtin_bit_cast(f32x4, v[0]), a1 = __builtin_bit_cast(f32x4, v[1]);
 #pragma unroll
   for (int m = 0; m < 4; ++m) acc = fmaf(a0[m], b.lo[m], acc);
@@ -152,8 +150,11 @@ __device__ __forceinline__ float dot_block(const u32x4* v, const float* q, float
 // the wave's range with no memory access, and run one batch of 8 column blocks
 // ahead of the arithmetic.
 // GUMBEL: the lists rank (and hold) score + Gumbel noise; the decode attention
-// recomputes the chosen chunks' raw scores.
-template <typename T, int KM, bool KEEP_ALL, bool GUMBEL>
+// recomputes the chosen chunks' raw scores.  Q8 (D = 512, eight column blocks
+// per key): every lane keeps its eight query fragments in registers, so there
+// is no staging of the query through LDS and no barrier before the first loads,
+// and a batch of loads is exactly one key group.
+template <typename T, int KM, bool KEEP_ALL, bool GUMBEL, bool Q8>
 __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __restrict__ lq,
                                                                    const T* __restrict__ lk, float* __restrict__ cs,
                                                                    int* __restrict__ cj, int64_t nC, int D,
@@ -166,9 +167,15 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
   const int64_t row = blockIdx.x / wgs, g = blockIdx.x % wgs;
   const int tid = threadIdx.x, lane = tid & 63, sub = lane & 7, kl = lane >> 3;
   const T* q = lq + row * D;  // the one landmark query of this row
-  for (int x = tid * (16 / (int)sizeof(T)); x < D; x += kScanThreads * (16 / (int)sizeof(T)))
-    *reinterpret_cast<u32x4*>(sq + x) = *reinterpret_cast<const u32x4*>(q + x);
-  __syncthreads();
+  Frag<T> qreg[Q8 ? kScanBatch : 1];
+  if constexpr (Q8) {
+#pragma unroll
+    for (int k = 0; k < kScanBatch; ++k) qreg[k] = load_frag(q + 64 * k + sub * 8);
+  } else {
+    for (int x = tid * (16 / (int)sizeof(T)); x < D; x += kScanThreads * (16 / (int)sizeof(T)))
+      *reinterpret_cast<u32x4*>(sq + x) = *reinterpret_cast<const u32x4*>(q + x);
+    __syncthreads();
+  }
 
   const int64_t list = uniform64(g * kScanWaves + (tid >> 6));
   if (list >= lists) return;
@@ -220,36 +227,48 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan_kernel(const T* __re
 #pragma unroll
     for (int m = 0; m < KM; ++m) sc[m] = -INFINITY;
   }
+  // the dot products of key group cg are complete in acc
+  auto finish_group = [&]() {
+    // sum over the key's 8 lanes (quad swaps, then the other quad)
+    acc += dpp<kDppXor1>(acc);
+    acc += dpp<kDppXor2>(acc);
+    acc += dpp<kDppHalfMirror>(acc);
+    if constexpr (KEEP_ALL) {
+      if (sub == (int)(cg & 7)) mine = acc;
+      if ((cg & 7) == 7 || cg + 1 == ngroups) {
+#pragma unroll
+        for (int m = 0; m < KM; ++m)
+          if (m == (int)(cg >> 3)) sc[m] = mine;
+        mine = -INFINITY;
+      }
+    } else {
+      const int64_t key = 8 * cg + kl;
+      // one of the key's 8 lanes inserts it, rotating with the group
+      if (key < n && sub == (int)(cg & 7)) {
+        float sv = acc * scale;
+        if constexpr (GUMBEL) sv += gumbel_noise(seed, (uint32_t)row, 0u, (uint32_t)(lo + key));
+        if (__builtin_isfinite(sv)) L.insert(sv, (int)(lo + key));
+      }
+    }
+    acc = 0.f;
+    ++cg;
+  };
   auto consume = [&](const u32x4* v, int64_t step0) {
+    if constexpr (Q8) {
+      if (step0 < nsteps) {  // one whole group
 #pragma unroll
-    for (int k = 0; k < kScanBatch; ++k) {
-      if (step0 + k < nsteps) {
-        acc = dot_block(v + k * LPS, sq + ccb * 64 + sub * 8, acc);
-        if (++ccb == NB) {
-          // sum over the key's 8 lanes (quad swaps, then the other quad)
-          acc += dpp<kDppXor1>(acc);
-          acc += dpp<kDppXor2>(acc);
-          acc += dpp<kDppHalfMirror>(acc);
-          if constexpr (KEEP_ALL) {
-            if (sub == (int)(cg & 7)) mine = acc;
-            if ((cg & 7) == 7 || cg + 1 == ngroups) {
+        for (int k = 0; k < kScanBatch; ++k) acc = dot_block(v + k * LPS, qreg[k], acc);
+        finish_group();
+      }
+    } else {
 #pragma unroll
-              for (int m = 0; m < KM; ++m)
-                if (m == (int)(cg >> 3)) sc[m] = mine;
-              mine = -INFINITY;
-            }
-          } else {
-            const int64_t key = 8 * cg + kl;
-            // one of the key's 8 lanes inserts it, rotating with the group
-            if (key < n && sub == (int)(cg & 7)) {
-              float sv = acc * scale;
-              if constexpr (GUMBEL) sv += gumbel_noise(seed, (uint32_t)row, 0u, (uint32_t)(lo + key));
-              if (__builtin_isfinite(sv)) L.insert(sv, (int)(lo + key));
-            }
+      for (int k = 0; k < kScanBatch; ++k) {
+        if (step0 + k < nsteps) {
+          acc = dot_block(v + k * LPS, load_frag(sq + ccb * 64 + sub * 8), acc);
+          if (++ccb == NB) {
+            ccb = 0;
+            finish_group();
           }
-          acc = 0.f;
-          ccb = 0;
-          ++cg;
         }
       }
     }
@@ -433,17 +452,23 @@ hipError_t launch_topk_k(const Shape& s, const float* scores, int32_t* idx, floa
   return take_launch_error();
 }
 
-template <typename T, int KM, bool KEEP_ALL, bool GUMBEL>
-hipError_t launch_scan_k(const Shape& s, const void* lq, const void* lk, void* ws, hipStream_t st) {
+template <typename T, int KM, bool KEEP_ALL, bool GUMBEL, bool Q8>
+hipError_t launch_scan_q(const Shape& s, const void* lq, const void* lk, void* ws, hipStream_t st) {
   const DecodePlan plan = decode_plan(s);
   const int64_t rows = (int64_t)s.B * s.Hr;
   float* cs = decode_list_scores(s, ws);
   int* cj = decode_list_chunks(s, ws);
-  const size_t smem = (size_t)s.D * sizeof(T);
-  launch_kernel("decode_scan_kernel", decode_scan_kernel<T, KM, KEEP_ALL, GUMBEL>, dim3((unsigned)(rows * plan.wgs)),
-                dim3(kScanThreads), smem, st, (const T*)lq, (const T*)lk, cs, cj, s.nKV, s.D, s.score_scale, s.topk,
+  const size_t smem = Q8 ? 0 : (size_t)s.D * sizeof(T);
+  launch_kernel("decode_scan_kernel", decode_scan_kernel<T, KM, KEEP_ALL, GUMBEL, Q8>,
+                dim3((unsigned)(rows * plan.wgs)), dim3(kScanThreads), smem, st, (const T*)lq, (const T*)lk, cs, cj, s.nKV, s.D, s.score_scale, s.topk,
                 plan.pw, plan.lists, plan.wgs, s.gumbel_seed);
   return take_launch_error();
+}
+
+template <typename T, int KM, bool KEEP_ALL, bool GUMBEL>
+hipError_t launch_scan_k(const Shape& s, const void* lq, const void* lk, void* ws, hipStream_t st) {
+  if (s.D == 64 * kScanBatch) return launch_scan_q<T, KM, KEEP_ALL, GUMBEL, true>(s, lq, lk, ws, st);
+  return launch_scan_q<T, KM, KEEP_ALL, GUMBEL, false>(s, lq, lk, ws, st);
 }
 
 }  // namespace

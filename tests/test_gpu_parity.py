@@ -131,6 +131,9 @@ SWEEP = [
     ("decode_16m_bf16", dict(H=2, Hr=2, D=64, n_chunks=777, device_kv=False), False),
     ("decode_16m_bf16", dict(H=1, D=192, n_chunks=999, topk=3, dtype="fp32", device_kv=False), False),
     ("decode_16m_bf16", dict(B=3, H=2, n_chunks=4000, topk=16, device_kv=False), False),
+    # D = 512: the query fragments live in registers
+    ("decode_16m_bf16", dict(H=8, n_chunks=3001, device_kv=False), False),
+    ("decode_16m_bf16", dict(H=8, n_chunks=2001, topk=5, dtype="fp32", device_kv=False), True),
 ]
 
 
@@ -300,6 +303,7 @@ GUMBEL = [
     ("planted_1m_bf16", dict(H=2, n_chunks=500, topk=8, gumbel_seed=13), "fused"),
     ("decode_16m_bf16", dict(H=2, n_chunks=3001, topk=8, gumbel_seed=14, device_kv=False), None),
     ("decode_16m_bf16", dict(H=1, D=64, n_chunks=40000, topk=4, gumbel_seed=15, device_kv=False), None),
+    ("decode_16m_bf16", dict(H=8, n_chunks=2500, topk=8, gumbel_seed=16, device_kv=False), None),
 ]
 
 
