@@ -816,10 +816,14 @@ inline GatherShape gather_shape(int D, int elem_bytes) {
 
 // dlmk_q[t] = score_scale * sum_s dsel[t, s] lmk_k[idx[t, s]]
 template <typename T>
+// The row's dsel (as dsel_kernel computes it) is formed here by the first wave
+// and written out, so the backward needs no separate dsel launch when the
+// landmark-query gradient is wanted.
 __global__ __launch_bounds__(256) void dlmk_q_kernel(const T* __restrict__ lk, const int32_t* __restrict__ idx,
-                                                     const float* __restrict__ dsel, float* __restrict__ dlq,
-                                                     int64_t nQ, int64_t nKV, int D, int K, float scale,
-                                                     GatherShape gs) {
+                                                     const float* __restrict__ w, const float* __restrict__ dwp,
+                                                     float* __restrict__ dsel, float* __restrict__ dlq,
+                                                     int64_t nQ, int64_t nKV, int D, int K, int H, int Hr,
+                                                     int causal, float scale, GatherShape gs) {
   constexpr int V = 16 / sizeof(T);
   __shared__ int64_t sRow[32];
   __shared__ float sW[32];
@@ -829,13 +833,30 @@ __global__ __launch_bounds__(256) void dlmk_q_kernel(const T* __restrict__ lk, c
   const int64_t bhr = row / nQ;
   if (threadIdx.x < 64) {
     const int s = threadIdx.x;
+    const int64_t t = row % nQ;
+    const int64_t b = bhr / Hr;
+    const int hr = (int)(bhr % Hr);
+    float dw = 0.f, ws = 0.f;
+    if (s < K) {
+      ws = w[row * K + s];
+      if (t + causal < nQ) {
+        const int h0 = Hr == 1 ? 0 : hr, h1 = Hr == 1 ? H : hr + 1;
+        for (int h = h0; h < h1; ++h) {
+          const float* d2 = dwp + (((b * H + h) * nQ + t) * K + s) * 2;
+          dw += d2[0] + d2[1];
+        }
+      }
+    }
+    const float tot = sum64(ws * dw);
+    const float ds = ws * (dw - tot);
+    if (s < K) dsel[row * K + s] = ds;
     const int j = s < K ? idx[row * K + s] : -1;
     const bool ok = j >= 0 && j < nKV;
     const uint64_t mask = __ballot(ok);
     if (ok) {
       const int rk = __popcll(mask & ((1ull << s) - 1));
       sRow[rk] = bhr * nKV + j;
-      sW[rk] = dsel[row * K + s];
+      sW[rk] = ds;
     }
     if (s == 0) sN = __popcll(mask);
   }
@@ -907,11 +928,14 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
   launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
   launch_kernel("bwd_dkdv_kernel", bwd_dkdv_kernel<T>, dim3((unsigned)round8(nk_work)), dim3(kThreads), 0, st, p,
                 nk_work);
-  launch_kernel("dsel_kernel", dsel_kernel, dim3((unsigned)(BHr * s.nQ)), dim3(64), 0, st, w.w, w.dwp, dsel, s.nQ,
-                s.H, s.Hr, s.topk, s.causal);
   if (dlmk_q) {
+    // dsel is formed inside the landmark-query gradient kernel
     launch_kernel("dlmk_q_kernel", dlmk_q_kernel<T>, dim3((unsigned)(BHr * s.nQ)), dim3(256), 0, st, (const T*)lmk_k,
-                  p.idx, dsel, dlmk_q, s.nQ, s.nKV, s.D, s.topk, s.score_scale, gather_shape(s.D, sizeof(T)));
+                  p.idx, w.w, w.dwp, dsel, dlmk_q, s.nQ, s.nKV, s.D, s.topk, s.H, s.Hr, s.causal, s.score_scale,
+                  gather_shape(s.D, sizeof(T)));
+  } else {
+    launch_kernel("dsel_kernel", dsel_kernel, dim3((unsigned)(BHr * s.nQ)), dim3(64), 0, st, w.w, w.dwp, dsel,
+                  s.nQ, s.H, s.Hr, s.topk, s.causal);
   }
   if (dlmk_k) {
     launch_kernel("dlmk_k_kernel", dlmk_k_kernel<T>, dim3((unsigned)(BHr * s.nKV)), dim3(256), 0, st, (const T*)lmk_q,
