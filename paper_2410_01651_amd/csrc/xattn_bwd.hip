@@ -466,25 +466,27 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_
 
 // ---------------------------------------------- key-stationary dK, dV ----
 
-// One workgroup of four waves per (batch, head, key chunk j); the two wave pairs
-// take alternate retrievers (row t, slot s) of chunk j from a four-slot LDS ring
-// (Q_c and dO_c tiles plus the shifted-lse and D columns of slot s, which the
-// query-stationary pass wrote), each wave owning 32 of chunk j's keys.  With the
-// shifted lse L = log2(e) lse - log2(w_s), exp2(S log2(e) scale - L) is w_s P_s
-// directly.  dK/dV partials of the pairs are summed at the end.
+// One workgroup of two waves per (batch, head, key chunk j), four per CU; the pair
+// takes the retrievers (row t, slot s) of chunk j in list order through a
+// two-slot LDS ring (Q_c and dO_c tiles plus the shifted-lse and D columns of
+// slot s, which the query-stationary pass wrote), each wave owning 32 of chunk
+// j's keys, so a workgroup's barrier couples only its two waves and no partial
+// sums are exchanged.  With the shifted lse L = log2(e) lse - log2(w_s),
+// exp2(S log2(e) scale - L) is w_s P_s directly.
+constexpr int kKvThreads = 128;
 template <typename T>
-__global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int64_t nwork) {
+__global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, int64_t nwork) {
   constexpr int TILE = kS * kD;
   // ring slot: Q_c tile, dO_c tile, shifted-lse column, D column
   constexpr int ENTRY = 2 * TILE + 2 * kS * (int)(sizeof(float) / sizeof(T));
-  __shared__ __attribute__((aligned(16))) T ring[4 * ENTRY];
+  __shared__ __attribute__((aligned(16))) T ring[2 * ENTRY];
   constexpr int NE = 256;  // retrievers staged in LDS per batch
   __shared__ int sE[NE];
 
   const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
   if (wid >= nwork) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
-  const int pair = wave >> 1, half = wave & 1;
+  const int half = wave;
   const int64_t j = wid % p.nKV;
   const int64_t bh = wid / p.nKV;
   const int h = (int)(bh % p.H);
@@ -501,7 +503,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
   T* dk = reinterpret_cast<T*>(p.dk) + key0 * kD;
   T* dv = reinterpret_cast<T*>(p.dv) + key0 * kD;
   if (n == 0) {
-    for (int e = tid; e < kS * kD / 4; e += kThreads) {
+    for (int e = tid; e < kS * kD / 4; e += kKvThreads) {
       store4(dk + 4 * e, 0.f, 0.f, 0.f, 0.f);
       store4(dv + 4 * e, 0.f, 0.f, 0.f, 0.f);
     }
@@ -518,14 +520,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
     kf[kb] = load_frag(krow + 16 * kb + 8 * hh);
     vf[kb] = load_frag(vrow + 16 * kb + 8 * hh);
   }
-  wait_vmem<0>();
 
   const T* qb = reinterpret_cast<const T*>(p.q) + bh * p.nQ * kS * kD;
   const T* ob = reinterpret_cast<const T*>(p.dout) + bh * p.nQ * kS * kD;
   const float* Lb = p.ws.Lbuf + bh * p.nQ * kS * K;
   const float* Db = p.ws.Dbuf + bh * p.nQ * kS * K;
 
-  const TileCopy<T, 4> cp(wave, lane);
+  const TileCopy<T, 2> cp(wave, lane);
   const uint32_t col_off = (uint32_t)(lane * sizeof(float));
   const int64_t lq_len = p.nQ * kS;
   auto issue = [&](int slot, int u) __device__ {
@@ -537,7 +538,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
     cp.issue(ob + c * TILE, dst + TILE);
     float* cols = reinterpret_cast<float*>(dst + 2 * TILE);
     if (wave == 0) dma_column_s(Lb + s * lq_len + c * kS, col_off, cols);
-    else if (wave == 1) dma_column_s(Db + s * lq_len + c * kS, col_off, cols + kS);
+    else dma_column_s(Db + s * lq_len + c * kS, col_off, cols + kS);
   };
 
   f32x16 dv0 = zero16(), dv1 = zero16(), dk0 = zero16(), dk1 = zero16();
@@ -574,7 +575,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
     }
   };
 
-  auto run = [&](int slot, int u) __device__ {
+  auto run = [&](int slot) __device__ {
     const T* sQ = ring + slot * ENTRY;
     const T* sO = sQ + TILE;
     const uint32_t qo = (uint32_t)slot * kEntryB, oo = qo + kTileB;
@@ -645,57 +646,35 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dkdv_kernel(BwdParams p, int6
   };
 
   // the retriever list is staged through LDS in batches, each streamed through
-  // the ring and drained at its end
+  // the ring (one item in flight ahead of the compute) and drained at its end
   for (int b0 = 0; b0 < n; b0 += NE) {
     const int nb = min(NE, n - b0);
     __syncthreads();
-    for (int i = tid; i < nb; i += kThreads) {
+    for (int i = tid; i < nb; i += kKvThreads) {
       const int e = list_g[b0 + i];  // t * K + s
       sE[i] = ((e / K + p.causal) << 5) | (e % K);
     }
     __syncthreads();
-    pair_ring_dyn(nb, pair, issue, run);
+    issue(0, 0);
+    for (int u = 0; u < nb; ++u) {
+      wait_vmem<0>();
+      block_barrier();
+      if (u + 1 < nb) issue((u + 1) & 1, u + 1);
+      run(u & 1);
+    }
   }
 
-  // pair 1 hands its dK^T/dV^T partials to pair 0 through LDS: dV in ring0,
-  // dK in ring1, each [half][tile][register][lane] fp32 (16 KB)
-  float* partv = reinterpret_cast<float*>(ring);
-  float* partk = reinterpret_cast<float*>(ring + ENTRY);
-  __syncthreads();
-  auto slot = [&](int which, int i) {
-    return (which < 2 ? partv : partk) + ((half * 2 + (which & 1)) * 16 + i) * 64 + lane;
-  };
-  if (pair == 1) {
+  // accumulators are transposed: lane holds key kr, d = 32*dt + 8*g + 4*hh + 0..3
+  const float as = p.attn_scale;
+  T* dkr = dk + kr * kD;
+  T* dvr = dv + kr * kD;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      *slot(0, i) = dv0[i];
-      *slot(1, i) = dv1[i];
-      *slot(2, i) = dk0[i];
-      *slot(3, i) = dk1[i];
-    }
-  }
-  __syncthreads();
-  if (pair == 0) {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      dv0[i] += *slot(0, i);
-      dv1[i] += *slot(1, i);
-      dk0[i] += *slot(2, i);
-      dk1[i] += *slot(3, i);
-    }
-    // accumulators are transposed: lane holds key kr, d = 32*dt + 8*g + 4*hh + 0..3
-    const float as = p.attn_scale;
-    T* dkr = dk + kr * kD;
-    T* dvr = dv + kr * kD;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      store4(dvr + 8 * g + 4 * hh, dv0[4 * g], dv0[4 * g + 1], dv0[4 * g + 2], dv0[4 * g + 3]);
-      store4(dvr + 32 + 8 * g + 4 * hh, dv1[4 * g], dv1[4 * g + 1], dv1[4 * g + 2], dv1[4 * g + 3]);
-      store4(dkr + 8 * g + 4 * hh, as * dk0[4 * g], as * dk0[4 * g + 1], as * dk0[4 * g + 2],
-             as * dk0[4 * g + 3]);
-      store4(dkr + 32 + 8 * g + 4 * hh, as * dk1[4 * g], as * dk1[4 * g + 1], as * dk1[4 * g + 2],
-             as * dk1[4 * g + 3]);
-    }
+  for (int g = 0; g < 4; ++g) {
+    store4(dvr + 8 * g + 4 * hh, dv0[4 * g], dv0[4 * g + 1], dv0[4 * g + 2], dv0[4 * g + 3]);
+    store4(dvr + 32 + 8 * g + 4 * hh, dv1[4 * g], dv1[4 * g + 1], dv1[4 * g + 2], dv1[4 * g + 3]);
+    store4(dkr + 8 * g + 4 * hh, as * dk0[4 * g], as * dk0[4 * g + 1], as * dk0[4 * g + 2], as * dk0[4 * g + 3]);
+    store4(dkr + 32 + 8 * g + 4 * hh, as * dk1[4 * g], as * dk1[4 * g + 1], as * dk1[4 * g + 2],
+           as * dk1[4 * g + 3]);
   }
 }
 
@@ -926,7 +905,7 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
   // persistent: two workgroups per CU, two chunk streams each
   const int64_t dq_wgs = std::min<int64_t>(512, round8((nq_work + 1) / 2));
   launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
-  launch_kernel("bwd_dkdv_kernel", bwd_dkdv_kernel<T>, dim3((unsigned)round8(nk_work)), dim3(kThreads), 0, st, p,
+  launch_kernel("bwd_dkdv_kernel", bwd_dkdv_kernel<T>, dim3((unsigned)round8(nk_work)), dim3(kKvThreads), 0, st, p,
                 nk_work);
   if (dlmk_q) {
     // dsel is formed inside the landmark-query gradient kernel
