@@ -25,7 +25,11 @@
 namespace gca {
 namespace {
 
-constexpr int kThreads = 256;  // two pairs of waves
+// query-stationary pass: wave pairs per workgroup (one, so that a round's
+// barrier couples only the two waves sharing a ring), four workgroups per CU
+constexpr int kPairs = 1;
+constexpr int kThreads = 128 * kPairs;
+constexpr int kWgPerCu = 4 / kPairs;
 
 struct Ws {
   float* w;        // [B*Hr, nQ, K] fusion weights
@@ -199,34 +203,35 @@ __global__ __launch_bounds__(256) void csr_sort_kernel(const int* __restrict__ o
 
 // ------------------------------------------------- query-stationary dQ ----
 
-// Persistent workgroups of four waves; each wave pair is a stream of (batch,
-// head, query chunk) items, taking the chunk's retrieved chunks one per round
+// Persistent workgroups of one wave pair, four per CU; each pair is a stream of
+// (batch, head, query chunk) items, taking the chunk's retrieved chunks one per round
 // from its two LDS ring slots (K_j and V_j tiles, copied one round ahead), each
 // wave owning 32 query tokens.  Per retrieved chunk it writes D_s and the
 // shifted log-sum-exp used by the key-stationary pass, and the wave's partial
 // sum of D_s for dw; dQ stays in registers until the chunk ends.  The work order
 // is the forward's (each XCD sweeps consecutive chunks of one slice at a time).
 template <typename T>
-__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p, int64_t nwork) {
+__global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p, int64_t nwork) {
   constexpr int TILE = kS * kD;
-  __shared__ __attribute__((aligned(16))) T ring[4 * 2 * TILE];  // pair p: slots 2p, 2p+1
-  __shared__ int sJ[2][2][32];     // [pair][chunk parity][slot]: chunk index or -1
-  __shared__ int sSlot[2][2][32];  // compacted valid slots: slot, chunk, weight
-  __shared__ int sJc[2][2][32];
-  __shared__ float sWc[2][2][32];
-  __shared__ int sN[2][2];
+  __shared__ __attribute__((aligned(16))) T ring[kPairs * 2 * 2 * TILE];  // pair p: slots 2p, 2p+1
+  __shared__ int sJ[kPairs][2][32];     // [pair][chunk parity][slot]: chunk index or -1
+  __shared__ int sSlot[kPairs][2][32];  // compacted valid slots: slot, chunk, weight
+  __shared__ int sJc[kPairs][2][32];
+  __shared__ float sWc[kPairs][2][32];
+  __shared__ int sN[kPairs][2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
-  const int64_t stride = (int64_t)(gridDim.x >> 3) * 2;
+  const int64_t stride = (int64_t)(gridDim.x >> 3) * kPairs;
   const int xcd = (int)(blockIdx.x & 7);
   const int64_t r_lo = nwork * xcd / 8, r_hi = nwork * (xcd + 1) / 8;
-  const int64_t st_wg = (int64_t)(blockIdx.x >> 3) * 2;
+  const int64_t st_wg = (int64_t)(blockIdx.x >> 3) * kPairs;
   auto stream_len = [&](int64_t st) -> int64_t {
     return r_lo + st < r_hi ? (r_hi - r_lo - st + stride - 1) / stride : 0;
   };
   const int64_t my_n = stream_len(st_wg + pair);
-  const int64_t nch = max(stream_len(st_wg), stream_len(st_wg + 1));
+  int64_t nch = 0;  // all pairs of the workgroup run nch chunks of rounds
+  for (int q = 0; q < kPairs; ++q) nch = max(nch, stream_len(st_wg + q));
   if (nch == 0) return;
   const int64_t c_begin = r_lo + st_wg + pair;
   const int K = p.K;
@@ -902,8 +907,8 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
   launch_kernel("csr_sort_kernel", csr_sort_kernel, dim3(blocks_for(BHr * s.nKV, 4)), dim3(256), 0, st, w.offs,
                 w.unsorted, w.sorted, BHr, s.nQ, s.topk, s.nKV);
   const int64_t nq_work = BH * s.nQ, nk_work = BH * s.nKV;
-  // persistent: two workgroups per CU, two chunk streams each
-  const int64_t dq_wgs = std::min<int64_t>(512, round8((nq_work + 1) / 2));
+  // persistent: kWgPerCu workgroups per CU, kPairs chunk streams each
+  const int64_t dq_wgs = std::min<int64_t>(256 * kWgPerCu, round8((nq_work + kPairs - 1) / kPairs));
   launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
   launch_kernel("bwd_dkdv_kernel", bwd_dkdv_kernel<T>, dim3((unsigned)round8(nk_work)), dim3(kKvThreads), 0, st, p,
                 nk_work);

@@ -1,7 +1,7 @@
 // Grouped cross attention forward (Eq. 2-3 of the method; Algorithm 1 in the
 // appendix is its tiled form).
 //
-// Persistent workgroups of four waves: each pair of waves is a stream of
+// Persistent workgroups of one wave pair, four per CU: each pair is a stream of
 // (batch, head, query chunk) work items, and within a pair each wave owns 32 of
 // the chunk's 64 query tokens and keeps their Q fragments in registers.  A pair
 // takes its chunk's retrieved chunks one per round; their keys and values stream
@@ -27,7 +27,11 @@
 namespace gca {
 namespace {
 
-constexpr int kThreads = 256;  // two pairs of waves
+// wave pairs per workgroup: one, so that a round's barrier couples only the two
+// waves that share a ring; four workgroups per CU
+constexpr int kPairs = 1;
+constexpr int kThreads = 128 * kPairs;
+constexpr int kWgPerCu = 4 / kPairs;
 
 struct FwdParams {
   const void* q;
@@ -62,19 +66,19 @@ __device__ __forceinline__ RowMeta load_row_meta(const FwdParams& p, int64_t row
 }
 
 template <typename T, bool OBO>
-__global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
+__global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams p) {
   constexpr int TILE = kS * kD;
-  __shared__ __attribute__((aligned(16))) T ring[4 * 2 * TILE];  // pair p: slots 2p, 2p+1 (K and V tiles)
-  __shared__ int sJ[2][2][32];     // [pair][chunk parity][slot]: chunk index or -1
-  __shared__ int sSlot[2][2][32];  // compacted lists of the valid slots: slot, chunk, weight
-  __shared__ int sJc[2][2][32];
-  __shared__ float sWc[2][2][32];
-  __shared__ int sN[2][2];
+  __shared__ __attribute__((aligned(16))) T ring[kPairs * 2 * 2 * TILE];  // pair p: slots 2p, 2p+1 (K and V tiles)
+  __shared__ int sJ[kPairs][2][32];     // [pair][chunk parity][slot]: chunk index or -1
+  __shared__ int sSlot[kPairs][2][32];  // compacted lists of the valid slots: slot, chunk, weight
+  __shared__ int sJc[kPairs][2][32];
+  __shared__ float sWc[kPairs][2][32];
+  __shared__ int sN[kPairs][2];
   // per wave, the log-sum-exp of its 32 tokens x k slots (k <= 8), stored to
   // HBM in one contiguous run at the end of the chunk instead of k scattered
   // 4-byte writes per token
   constexpr int kStageK = 8;
-  __shared__ float sLse[4][32][kStageK];
+  __shared__ float sLse[2 * kPairs][32][kStageK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
@@ -85,15 +89,16 @@ __global__ __launch_bounds__(kThreads, 2) void xattn_fwd_kernel(FwdParams p) {
   // an XCD works on a window of consecutive query chunks of one (batch, head)
   // slice, whose retrieved key/value chunks its L2 and the shared last-level cache
   // keep resident across the queries that reuse them.
-  const int64_t stride = (int64_t)(gridDim.x >> 3) * 2;
+  const int64_t stride = (int64_t)(gridDim.x >> 3) * kPairs;
   const int xcd = (int)(blockIdx.x & 7);
   const int64_t r_lo = p.nwork * xcd / 8, r_hi = p.nwork * (xcd + 1) / 8;
-  const int64_t st_wg = (int64_t)(blockIdx.x >> 3) * 2;
+  const int64_t st_wg = (int64_t)(blockIdx.x >> 3) * kPairs;
   auto stream_len = [&](int64_t st) -> int64_t {
     return r_lo + st < r_hi ? (r_hi - r_lo - st + stride - 1) / stride : 0;
   };
   const int64_t my_n = stream_len(st_wg + pair);
-  const int64_t nch = max(stream_len(st_wg), stream_len(st_wg + 1));  // both pairs run nch chunks of rounds
+  int64_t nch = 0;  // all pairs of the workgroup run nch chunks of rounds
+  for (int q = 0; q < kPairs; ++q) nch = max(nch, stream_len(st_wg + q));
   if (nch == 0) return;
   const int64_t c_begin = r_lo + st_wg + pair;
   const int K = p.topk;
@@ -384,9 +389,9 @@ hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const 
   p.nwork = (int64_t)s.B * s.H * s.nQ;
   p.causal = s.causal;
   p.attn_scale = s.attn_scale;
-  // persistent workgroups: two per CU (256 CUs), a multiple of 8 (one share per
-  // XCD), each running two chunk streams
-  const int64_t target = 512, wgs = (p.nwork + 1) / 2;
+  // persistent workgroups: kWgPerCu per CU (256 CUs), a multiple of 8 (one share
+  // per XCD), each running kPairs chunk streams
+  const int64_t target = 256 * kWgPerCu, wgs = (p.nwork + kPairs - 1) / kPairs;
   const dim3 grid((unsigned)(wgs < target ? round8(wgs) : target)), block(kThreads);
   if (s.bf16) {
     if (s.off_by_one) {
