@@ -33,7 +33,7 @@ constexpr int kWgPerCu = 4 / kPairs;
 
 struct Ws {
   float* w;        // [B*Hr, nQ, K] fusion weights
-  float* Dbuf;     // [B*H, K, Lq]  D_s per query token (slot-major: one slot's tokens contiguous)
+  float* Dbuf;     // [B*H, K, Lq]  -D_s per query token (slot-major: one slot's tokens contiguous)
   float* Lbuf;     // [B*H, K, Lq]  log2 of 1 / (w_s exp(-lse)): log2(e) lse - log2(w_s)
   float* dwp;      // [B*H, nQ, K, 2] dw partials per head and query half
   int* counts;     // [B*Hr, nKV]
@@ -396,7 +396,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     }
     // D_s and the shifted lse of this (query, slot) for the key-stationary pass
     if (hh == 0) {
-      p.ws.Dbuf[cbase + s * lq_len + qi] = Dq;
+      p.ws.Dbuf[cbase + s * lq_len + qi] = -Dq;  // negated: it seeds the dP accumulator there
       p.ws.Lbuf[cbase + s * lq_len + qi] = lse_q * kLog2e - __builtin_amdgcn_logf(ws);
     }
     // this wave's 32 queries' share of dw[t, s]
@@ -586,63 +586,63 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
     const uint32_t qo = (uint32_t)slot * kEntryB, oo = qo + kTileB;
     const float* sL = reinterpret_cast<const float*>(sQ + 2 * TILE);
     const float* sD = sL + kS;
-    // S = Q K^T for this wave's keys; queries 0-31 in s0, 32-63 in s1
-    Frag<T> wp[4];
-    {
-      f32x16 s0 = zero16(), s1 = zero16();
+    // accumulator row i of a 32-query tile holds query 32*qt + 8*(i/4) + 4*hh + i%4,
+    // so four consecutive registers take one 16-byte column read.
+    // dP - D = dO V^T + (-D): the accumulators start from the stored -D column
+    f32x16 p0, p1;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        mma32(s0, row_frag(sQ, qo, kb, 0), kf[kb]);
-        mma32(s1, row_frag(sQ, qo, kb, 1), kf[kb]);
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 d0 = *reinterpret_cast<const f32x4*>(sD + 8 * g + 4 * hh);
+      const f32x4 d1 = *reinterpret_cast<const f32x4*>(sD + 32 + 8 * g + 4 * hh);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        p0[4 * g + r] = d0[r];
+        p1[4 * g + r] = d1[r];
       }
-      // w P; accumulator row i holds query 32*qt + 8*(i/4) + 4*hh + i%4
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 l0 = *reinterpret_cast<const f32x4*>(sL + 8 * g + 4 * hh);
-        const f32x4 l1 = *reinterpret_cast<const f32x4*>(sL + 32 + 8 * g + 4 * hh);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          s0[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s0[4 * g + r], sc, -l0[r]));
-          s1[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s1[4 * g + r], sc, -l1[r]));
-        }
-      }
-      frag_from_acc(wp[0], s0, 0, 1.f);
-      frag_from_acc(wp[1], s0, 1, 1.f);
-      frag_from_acc(wp[2], s1, 0, 1.f);
-      frag_from_acc(wp[3], s1, 1, 1.f);
     }
-    // dV^T += dO^T (w P)  (contraction over the 64 queries)
+    // S = Q K^T for this wave's keys (queries 0-31 in s0, 32-63 in s1), and dP
+    f32x16 s0 = zero16(), s1 = zero16();
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      mma32(s0, row_frag(sQ, qo, kb, 0), kf[kb]);
+      mma32(s1, row_frag(sQ, qo, kb, 1), kf[kb]);
+    }
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      mma32(p0, row_frag(sO, oo, kb, 0), vf[kb]);
+      mma32(p1, row_frag(sO, oo, kb, 1), vf[kb]);
+    }
+    // w P (fp32), then dS = w P o (dP - D)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 l0 = *reinterpret_cast<const f32x4*>(sL + 8 * g + 4 * hh);
+      const f32x4 l1 = *reinterpret_cast<const f32x4*>(sL + 32 + 8 * g + 4 * hh);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        s0[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s0[4 * g + r], sc, -l0[r]));
+        s1[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s1[4 * g + r], sc, -l1[r]));
+      }
+    }
+    Frag<T> wp[4], ds[4];
+    frag_from_acc(wp[0], s0, 0, 1.f);
+    frag_from_acc(wp[1], s0, 1, 1.f);
+    frag_from_acc(wp[2], s1, 0, 1.f);
+    frag_from_acc(wp[3], s1, 1, 1.f);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      p0[i] *= s0[i];
+      p1[i] *= s1[i];
+    }
+    frag_from_acc(ds[0], p0, 0, 1.f);
+    frag_from_acc(ds[1], p0, 1, 1.f);
+    frag_from_acc(ds[2], p1, 0, 1.f);
+    frag_from_acc(ds[3], p1, 1, 1.f);
+    // dV^T += dO^T (w P) and dK^T += Q^T dS  (contractions over the 64 queries)
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       mma32(dv0, col_frag(sO, oo, kb, 0), wp[kb]);
       mma32(dv1, col_frag(sO, oo, kb, 1), wp[kb]);
     }
-    // dP = dO V^T, then dS = w P o (dP - D) from the w P fragments
-    Frag<T> ds[4];
-    {
-      f32x16 p0 = zero16(), p1 = zero16();
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        mma32(p0, row_frag(sO, oo, kb, 0), vf[kb]);
-        mma32(p1, row_frag(sO, oo, kb, 1), vf[kb]);
-      }
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 d0 = *reinterpret_cast<const f32x4*>(sD + 8 * g + 4 * hh);
-        const f32x4 d1 = *reinterpret_cast<const f32x4*>(sD + 32 + 8 * g + 4 * hh);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int i = 4 * g + r;  // register i of tile qt lives in wp[2*qt + i/8] entry i%8
-          p0[i] = frag_elem(wp[i >> 3], i & 7) * (p0[i] - d0[r]);
-          p1[i] = frag_elem(wp[2 + (i >> 3)], i & 7) * (p1[i] - d1[r]);
-        }
-      }
-      frag_from_acc(ds[0], p0, 0, 1.f);
-      frag_from_acc(ds[1], p0, 1, 1.f);
-      frag_from_acc(ds[2], p1, 0, 1.f);
-      frag_from_acc(ds[3], p1, 1, 1.f);
-    }
-    // dK^T += Q^T dS
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       mma32(dk0, col_frag(sQ, qo, kb, 0), ds[kb]);
