@@ -685,6 +685,22 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
 
 // -------------------------------------- score and landmark gradients ----
 
+// dw[t, s] of one row: the per-head, per-wave-half partials summed over the
+// group's heads as kDwClasses interleaved classes (head h in class (h - h0) mod
+// kDwClasses), each class summed in head order and the classes added in class
+// order, so that both kernels that form dsel round identically.
+constexpr int kDwClasses = 8;
+__device__ __forceinline__ float dw_class(const float* __restrict__ dwp, int64_t b, int64_t t, int s, int H, int Hr,
+                                          int hr, int64_t nQ, int K, int cls) {
+  const int h0 = Hr == 1 ? 0 : hr, h1 = Hr == 1 ? H : hr + 1;
+  float acc = 0.f;
+  for (int h = h0 + cls; h < h1; h += kDwClasses) {
+    const float* d2 = dwp + (((b * H + h) * nQ + t) * K + s) * 2;
+    acc += d2[0] + d2[1];
+  }
+  return acc;
+}
+
 // dsel[t, s] = w_s (dw_s - sum_s' w_s' dw_s'), dw summed over the group's heads.
 __global__ __launch_bounds__(64) void dsel_kernel(const float* __restrict__ w, const float* __restrict__ dwp,
                                                   float* __restrict__ dsel, int64_t nQ, int H, int Hr, int K,
@@ -699,11 +715,7 @@ __global__ __launch_bounds__(64) void dsel_kernel(const float* __restrict__ w, c
   if (s < K) {
     ws = w[row * K + s];
     if (t + causal < nQ) {
-      const int h0 = Hr == 1 ? 0 : hr, h1 = Hr == 1 ? H : hr + 1;
-      for (int h = h0; h < h1; ++h) {
-        const float* d2 = dwp + (((b * H + h) * nQ + t) * K + s) * 2;
-        dw += d2[0] + d2[1];
-      }
+      for (int c = 0; c < kDwClasses; ++c) dw += dw_class(dwp, b, t, s, H, Hr, hr, nQ, K, c);
     }
   }
   float tot = ws * dw;
@@ -813,23 +825,25 @@ __global__ __launch_bounds__(256) void dlmk_q_kernel(const T* __restrict__ lk, c
   __shared__ float sW[32];
   __shared__ int sN;
   __shared__ float sAcc[256 * 8];
+  __shared__ float sCls[kDwClasses][32];
   const int64_t row = blockIdx.x;
   const int64_t bhr = row / nQ;
+  const int64_t t = row % nQ;
+  const int64_t b = bhr / Hr;
+  const int hr = (int)(bhr % Hr);
+  {
+    // the dw partials of every head are read by all 256 threads at once: thread
+    // (class c, slot s) sums head class c of slot s
+    const int s = threadIdx.x & 31, c = threadIdx.x >> 5;
+    sCls[c][s] = (s < K && t + causal < nQ) ? dw_class(dwp, b, t, s, H, Hr, hr, nQ, K, c) : 0.f;
+  }
+  __syncthreads();
   if (threadIdx.x < 64) {
     const int s = threadIdx.x;
-    const int64_t t = row % nQ;
-    const int64_t b = bhr / Hr;
-    const int hr = (int)(bhr % Hr);
     float dw = 0.f, ws = 0.f;
     if (s < K) {
       ws = w[row * K + s];
-      if (t + causal < nQ) {
-        const int h0 = Hr == 1 ? 0 : hr, h1 = Hr == 1 ? H : hr + 1;
-        for (int h = h0; h < h1; ++h) {
-          const float* d2 = dwp + (((b * H + h) * nQ + t) * K + s) * 2;
-          dw += d2[0] + d2[1];
-        }
-      }
+      for (int c = 0; c < kDwClasses; ++c) dw += sCls[c][s];
     }
     const float tot = sum64(ws * dw);
     const float ds = ws * (dw - tot);
