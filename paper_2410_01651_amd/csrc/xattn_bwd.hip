@@ -210,7 +210,10 @@ __global__ __launch_bounds__(256) void csr_sort_kernel(const int* __restrict__ o
 // shifted log-sum-exp used by the key-stationary pass, and the wave's partial
 // sum of D_s for dw; dQ stays in registers until the chunk ends.  The work order
 // is the forward's (each XCD sweeps consecutive chunks of one slice at a time).
-template <typename T>
+// STAGE (k <= kDqStageK): the per-(token, slot) values are staged in LDS and
+// stored once per chunk.
+constexpr int kDqStageK = 8;
+template <typename T, bool STAGE>
 __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p, int64_t nwork) {
   constexpr int TILE = kS * kD;
   __shared__ __attribute__((aligned(16))) T ring[kPairs * 2 * 2 * TILE];  // pair p: slots 2p, 2p+1
@@ -219,6 +222,12 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
   __shared__ int sJc[kPairs][2][32];
   __shared__ float sWc[kPairs][2][32];
   __shared__ int sN[kPairs][2];
+  // per wave, the (-D, shifted lse) pairs of its 32 tokens x k slots and its dw
+  // partials (k <= 8), stored at the end of the chunk: a store still in flight
+  // holds up the next round's wait for its copies, so none is issued per round
+  constexpr int kStageK = STAGE ? kDqStageK : 1;
+  __shared__ float sDL[2 * kPairs][2][kStageK][32];
+  __shared__ float sDw[2 * kPairs][kStageK];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
@@ -394,14 +403,24 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         mma32(g1a, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), f[kb]);
       }
     }
-    // D_s and the shifted lse of this (query, slot) for the key-stationary pass
+    // D_s (negated: it seeds the dP accumulator there) and the shifted lse of this
+    // (query, slot) for the key-stationary pass
     if (hh == 0) {
-      p.ws.Dbuf[cbase + s * lq_len + qi] = -Dq;  // negated: it seeds the dP accumulator there
-      p.ws.Lbuf[cbase + s * lq_len + qi] = lse_q * kLog2e - __builtin_amdgcn_logf(ws);
+      const float dneg = -Dq, lsh = lse_q * kLog2e - __builtin_amdgcn_logf(ws);
+      if constexpr (STAGE) {
+        sDL[wave][0][s][l32] = dneg;
+        sDL[wave][1][s][l32] = lsh;
+      } else {
+        p.ws.Dbuf[cbase + s * lq_len + qi] = dneg;
+        p.ws.Lbuf[cbase + s * lq_len + qi] = lsh;
+      }
     }
     // this wave's 32 queries' share of dw[t, s]
     const float dsum = sum32(Dq);
-    if (lane == 0) p.ws.dwp[(t * K + s) * 2 + half] = dsum;
+    if (lane == 0) {
+      if constexpr (STAGE) sDw[wave][s] = dsum;
+      else p.ws.dwp[(t * K + s) * 2 + half] = dsum;
+    }
   };
 
   for (int64_t ci = 0; ci < nch; ++ci) {
@@ -459,7 +478,22 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
                as * g1a[4 * g + 3]);
       }
       const bool has_row = !p.causal || g0.c > 0;
-      if (has_row && n < K && lane < K && sJ[pair][buf][lane] < 0) p.ws.dwp[(tglob * K + lane) * 2 + half] = 0.f;
+      if constexpr (STAGE) {
+        // this wave's staged values (its own LDS writes, read back in program
+        // order): per valid slot one contiguous run of 32 tokens
+        for (int e = lane; e < 32 * K; e += 64) {
+          const int sl = e >> 5, q = e & 31;
+          if (sJ[pair][buf][sl] >= 0) {
+            const int64_t o = cbase + sl * lq_len + 32 * half + q;
+            p.ws.Dbuf[o] = sDL[wave][0][sl][q];
+            p.ws.Lbuf[o] = sDL[wave][1][sl][q];
+          }
+        }
+        if (has_row && lane < K)
+          p.ws.dwp[(tglob * K + lane) * 2 + half] = sJ[pair][buf][lane] >= 0 ? sDw[wave][lane] : 0.f;
+      } else if (has_row && n < K && lane < K && sJ[pair][buf][lane] < 0) {
+        p.ws.dwp[(tglob * K + lane) * 2 + half] = 0.f;
+      }
     }
     g0a = zero16();
     g1a = zero16();
@@ -923,7 +957,11 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
   const int64_t nq_work = BH * s.nQ, nk_work = BH * s.nKV;
   // persistent: kWgPerCu workgroups per CU, kPairs chunk streams each
   const int64_t dq_wgs = std::min<int64_t>(256 * kWgPerCu, round8((nq_work + kPairs - 1) / kPairs));
-  launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
+  if (s.topk <= kDqStageK)
+    launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T, true>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
+  else
+    launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T, false>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p,
+                  nq_work);
   launch_kernel("bwd_dkdv_kernel", bwd_dkdv_kernel<T>, dim3((unsigned)round8(nk_work)), dim3(kKvThreads), 0, st, p,
                 nk_work);
   if (dlmk_q) {
