@@ -348,7 +348,10 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
 
   f32x16 g0a = zero16(), g1a = zero16();  // dQ^T, d rows 0-31 / 32-63
   // cbase: element of (this slice, slot 0, this chunk's first token) in Dbuf / Lbuf
-  auto run = [&](int slot, int u, float lse_q, int64_t cbase, int64_t t) __device__ {
+  // pre: this is the chunk's last item and a next chunk follows; its Q and dO rows
+  // are loaded as soon as this item's products have read qf/df, so that the
+  // next chunk's first round does not wait out the whole load
+  auto run = [&](int slot, int u, float lse_q, int64_t cbase, int64_t t, bool pre) __device__ {
     const uint32_t co = (uint32_t)slot * 2 * kTileB;
     const int s = __builtin_amdgcn_readlane(ls, u);
     const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lw), u));
@@ -370,6 +373,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         mma32(p1, lds_frag(sV, 32 + (lane & 31), 16 * kb + 8 * hh), df[kb]);
       }
     }
+    if (pre) load_qdo(g1, qf, df);
     // w P^T (the weight folded into the exponent: wsf = max(ws, 1e-30) keeps the
     // shift finite), D = rowsum(P o dP) for this lane's query, w dS
     const float wsf = fmaxf(ws, 1e-30f);
@@ -459,11 +463,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         lse_next = p.lse[(tok_n + qi) * K + sSlot[pair][buf ^ 1][0]];
       }
       if (comp) {
-        run(cs, u, lse_q, cbase, tglob);
+        run(cs, u, lse_q, cbase, tglob, live_next && u == n - 1);
         cs ^= 1;
       }
-      // the next chunk's Q and dO rows arrive with the copies of its first item
-      if (u == K - 1 && live_next) load_qdo(g1, qf, df);
+      // a chunk without items loads the next chunk's Q and dO rows in its first round
+      if (n == 0 && u == 0 && live_next) load_qdo(g1, qf, df);
     }
 
     // ---- finish the chunk: dQ rows of this wave; zero dw partials of empty slots
