@@ -189,13 +189,16 @@ struct TileCopy {
   uint32_t goff[kN];
   uint32_t lwave;  // this wave's first 1 KiB block of the tile in LDS (scalar)
 
-  __device__ __forceinline__ TileCopy(int wave, int lane) {
+  // row_stride: elements between consecutive source rows (kD: a contiguous tile);
+  // rows: source rows that exist (LDS rows past them repeat the last one)
+  __device__ __forceinline__ TileCopy(int wave, int lane, int row_stride = kD, int rows = kS) {
 #pragma unroll
     for (int ii = 0; ii < kN; ++ii) {
       const int pch = (ii * NW + wave) * 64 + lane;
       const int r = pch / kCPR;
       const int c = (pch % kCPR) ^ Swz<T>::sw(r);
-      goff[ii] = (uint32_t)((r * kD + c * kVec) * sizeof(T));
+      const int rs = r < rows ? r : rows - 1;
+      goff[ii] = (uint32_t)((rs * row_stride + c * kVec) * sizeof(T));
     }
     lwave = __builtin_amdgcn_readfirstlane((uint32_t)(wave * 64 * 16));
   }

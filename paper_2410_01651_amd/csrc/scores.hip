@@ -23,11 +23,52 @@ namespace {
 
 // ------------------------------------------------------------ scores ----
 
+// One 64x64 block of scores: landmark query rows a[0..63] against landmark key
+// rows b[0..63] (rows at and past a_n / b_n repeat the last existing row; their
+// scores are discarded by the caller), contracted over D in 64-column chunks.
+// The workgroup copies each chunk of both row blocks into LDS with coalesced
+// direct-to-LDS loads (128 contiguous bytes per row and copy), two stages deep,
+// the next chunk in flight during the current chunk's products; wave w computes
+// the 32x32 block of query rows 32 (w >> 1) and key rows 32 (w & 1).
+template <typename T>
+__device__ __forceinline__ f32x16 score_block(const T* a, int a_n, const T* b, int b_n, int D, T* stage) {
+  constexpr int TILE = kS * kD;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
+  const TileCopy<T, 4> ca(wave, lane, D, a_n), cb(wave, lane, D, b_n);
+  constexpr int kLoads = 2 * TileCopy<T, 4>::kN;  // one wave's copies of one chunk
+  const int nch = D / kD;
+  auto issue = [&](int c) __device__ {
+    T* st = stage + (c & 1) * 2 * TILE;
+    ca.issue(a + c * kD, st);
+    cb.issue(b + c * kD, st + TILE);
+  };
+  f32x16 acc = zero16();
+  issue(0);
+  for (int c = 0; c < nch; ++c) {
+    if (c + 1 < nch) {
+      issue(c + 1);
+      wait_vmem<kLoads>();
+    } else {
+      wait_vmem<0>();
+    }
+    block_barrier();  // every wave's copies of chunk c are in
+    const T* sa = stage + (c & 1) * 2 * TILE;
+    const T* sb = sa + TILE;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      mma32(acc, lds_frag(sa, 32 * (wave >> 1) + (lane & 31), 16 * kb + 8 * hh),
+            lds_frag(sb, 32 * (wave & 1) + (lane & 31), 16 * kb + 8 * hh));
+    block_barrier();  // the stage is free for the copy issued in the next step
+  }
+  return acc;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void chunk_scores_kernel(const T* __restrict__ lq, const T* __restrict__ lk,
                                                            float* __restrict__ scores, int64_t nQ, int64_t nC,
                                                            int D, float scale, int causal, int64_t ntq,
                                                            int64_t ntj, int64_t nwork) {
+  __shared__ __attribute__((aligned(16))) T stage[4 * kS * kD];
   const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
   if (wid >= nwork) return;
   const int64_t tj = wid % ntj;
@@ -35,29 +76,22 @@ __global__ __launch_bounds__(256) void chunk_scores_kernel(const T* __restrict__
   const int64_t tq = rest % ntq;
   const int64_t bhr = rest / ntq;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hh = lane >> 5;
-  const int64_t t0 = tq * 64 + 32 * (wave >> 1);
-  const int64_t j0 = tj * 64 + 32 * (wave & 1);
-  const int64_t j = j0 + (lane & 31);
+  const int64_t ta0 = tq * 64, tb0 = tj * 64;
+  const int64_t t0 = ta0 + 32 * (wave >> 1);
+  const int64_t j = tb0 + 32 * (wave & 1) + (lane & 31);
   float* out = scores + bhr * nQ * nC;
 
   f32x16 acc = zero16();
-  const bool any = !causal || (j0 < t0 + 31);  // some j < t inside this 32x32 block
-  if (any && t0 < nQ && j0 < nC) {
-    const int64_t ta = t0 + (lane & 31) < nQ ? t0 + (lane & 31) : nQ - 1;  // clamped rows are discarded
-    const int64_t jb = j < nC ? j : nC - 1;
-    const T* arow = lq + (bhr * nQ + ta) * D;
-    const T* brow = lk + (bhr * nC + jb) * D;
-    for (int x = 0; x < D; x += 16) {
-      const Frag<T> a = load_frag(arow + x + 8 * hh);
-      const Frag<T> bb = load_frag(brow + x + 8 * hh);
-      mma32(acc, a, bb);
-    }
-  }
+  // workgroup-uniform: the block holds some j < t (causal) and exists
+  const bool live = ta0 < nQ && tb0 < nC && (!causal || tb0 < ta0 + 63);
+  if (live)
+    acc = score_block<T>(lq + (bhr * nQ + ta0) * D, (int)min<int64_t>(64, nQ - ta0), lk + (bhr * nC + tb0) * D,
+                         (int)min<int64_t>(64, nC - tb0), D, stage);
   if (j < nC) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int64_t t = t0 + 8 * (i >> 2) + 4 * hh + (i & 3);
-      if (t < nQ) out[t * nC + j] = (!causal || j < t) ? acc[i] * scale : -INFINITY;
+      if (t < nQ) out[t * nC + j] = (live && (!causal || j < t)) ? acc[i] * scale : -INFINITY;
     }
   }
 }
@@ -91,10 +125,26 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ sco
   const float* sr = scores + row * nC;
   TopList<KM> L;
   L.init();
-  for (int64_t j = lane; j < lim; j += 64) {
-    float v = sr[j];
-    if constexpr (GUMBEL) v += gumbel_noise(seed, (uint32_t)(row / nQ), (uint32_t)t, (uint32_t)j);
-    if (__builtin_isfinite(v)) L.insert(v, (int)j);
+  // kTB scores per lane are loaded before they are inserted (in the same column
+  // order), so a row of up to 64 kTB columns costs one memory latency (fewer
+  // for the longer lists, whose unrolled inserts are larger)
+  constexpr int kTB = KM <= 8 ? 16 : KM <= 16 ? 8 : 1;
+  for (int64_t j0 = 0; j0 < lim; j0 += 64 * kTB) {
+    float vb[kTB];
+#pragma unroll
+    for (int m = 0; m < kTB; ++m) {
+      const int64_t j = j0 + 64 * m + lane;
+      vb[m] = j < lim ? sr[j] : -INFINITY;
+    }
+#pragma unroll
+    for (int m = 0; m < kTB; ++m) {
+      const int64_t j = j0 + 64 * m + lane;
+      float v = vb[m];
+      if constexpr (GUMBEL) {
+        if (j < lim) v += gumbel_noise(seed, (uint32_t)(row / nQ), (uint32_t)t, (uint32_t)j);
+      }
+      if (__builtin_isfinite(v)) L.insert(v, (int)j);  // columns past the row read -inf
+    }
   }
   float ms;
   int mj, cnt;
@@ -329,6 +379,7 @@ __global__ __launch_bounds__(256) void fused_select_kernel(const T* __restrict__
                                                            int32_t* __restrict__ idx, float* __restrict__ sel,
                                                            int64_t nQ, int64_t nC, int D, float scale, int K,
                                                            int64_t ntq, uint64_t seed) {
+  __shared__ __attribute__((aligned(16))) T stage[4 * kS * kD];
   __shared__ float sT[64][65];
   __shared__ float sRs[64][32];
   __shared__ int sRj[64][32];
@@ -345,18 +396,8 @@ __global__ __launch_bounds__(256) void fused_select_kernel(const T* __restrict__
   for (int64_t j0 = 0; j0 < jend; j0 += 64) {
     const int64_t cj0 = j0 + 32 * (wave & 1);
     const bool any = rt0 < nQ && cj0 < nC && cj0 < rt0 + 31;
-    f32x16 acc = zero16();
-    if (any) {
-      const int64_t ta = rt0 + (lane & 31) < nQ ? rt0 + (lane & 31) : nQ - 1;
-      const int64_t jb = cj0 + (lane & 31) < nC ? cj0 + (lane & 31) : nC - 1;
-      const T* arow = lq + (bhr * nQ + ta) * D;
-      const T* brow = lk + (bhr * nC + jb) * D;
-      for (int x = 0; x < D; x += 16) {
-        const Frag<T> a = load_frag(arow + x + 8 * hh);
-        const Frag<T> bb = load_frag(brow + x + 8 * hh);
-        mma32(acc, a, bb);
-      }
-    }
+    const f32x16 acc = score_block<T>(lq + (bhr * nQ + t0) * D, (int)min<int64_t>(64, nQ - t0),
+                                      lk + (bhr * nC + j0) * D, (int)min<int64_t>(64, nC - j0), D, stage);
     const int jl = 32 * (wave & 1) + (lane & 31);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
