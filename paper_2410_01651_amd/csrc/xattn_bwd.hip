@@ -31,6 +31,12 @@ constexpr int kPairs = 1;
 constexpr int kThreads = 128 * kPairs;
 constexpr int kWgPerCu = 4 / kPairs;
 
+// per key chunk, one 64-byte row: [0] offset of its list in `sorted`, [1] its
+// length, [2 .. 2 + kHeadEntries) its first entries, so the key-stationary pass
+// starts a chunk's first copy one dependent load after its launch
+constexpr int kHeadInts = 16;
+constexpr int kHeadEntries = 8;
+
 struct Ws {
   float* w;        // [B*Hr, nQ, K] fusion weights
   float* Dbuf;     // [B*H, K, Lq]  -D_s per query token (slot-major: one slot's tokens contiguous)
@@ -41,6 +47,7 @@ struct Ws {
   int* offs;       // [B*Hr, nKV+1]
   int* unsorted;   // [B*Hr, nQ*K]
   int* sorted;     // [B*Hr, nQ*K]
+  int* head;       // [B*Hr, nKV, kHeadInts]  per key chunk: list offset, count, first entries
 };
 
 Ws carve(const Shape& s, void* base) {
@@ -57,6 +64,7 @@ Ws carve(const Shape& s, void* base) {
   w.offs = (int*)take(sizeof(int) * BHr * (s.nKV + 1));
   w.unsorted = (int*)take(sizeof(int) * BHr * s.nQ * s.topk);
   w.sorted = (int*)take(sizeof(int) * BHr * s.nQ * s.topk);
+  w.head = (int*)take(sizeof(int) * BHr * s.nKV * kHeadInts);
   return w;
 }
 
@@ -69,6 +77,7 @@ size_t carve_size(const Shape& s) {
   n += align256(sizeof(int) * BHr * s.nKV) * 2;
   n += align256(sizeof(int) * BHr * (s.nKV + 1));
   n += align256(sizeof(int) * BHr * s.nQ * s.topk) * 2;
+  n += align256(sizeof(int) * BHr * s.nKV * kHeadInts);
   return n;
 }
 
@@ -183,8 +192,8 @@ __global__ void csr_fill_kernel(const int32_t* __restrict__ idx, int* __restrict
 // Order each chunk's list ascending by (t, s): an entry's position is the number
 // of smaller entries in its list (entries are distinct).  One wave per chunk.
 __global__ __launch_bounds__(256) void csr_sort_kernel(const int* __restrict__ offs, const int* __restrict__ unsorted,
-                                                       int* __restrict__ sorted, int64_t BHr, int64_t nQ, int K,
-                                                       int64_t nKV) {
+                                                       int* __restrict__ sorted, int* __restrict__ head, int64_t BHr,
+                                                       int64_t nQ, int K, int64_t nKV) {
   const int64_t wv = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (wv >= BHr * nKV) return;
   const int lane = threadIdx.x & 63;
@@ -193,11 +202,17 @@ __global__ __launch_bounds__(256) void csr_sort_kernel(const int* __restrict__ o
   const int lo = off[j], hi = off[j + 1];
   const int* src = unsorted + bhr * nQ * K;
   int* dst = sorted + bhr * nQ * K;
+  int* hd = head + wv * kHeadInts;
+  if (lane == 0) {
+    hd[0] = lo;
+    hd[1] = hi - lo;
+  }
   for (int i = lo + lane; i < hi; i += 64) {
     const int e = src[i];
     int rank = 0;
     for (int u = lo; u < hi; ++u) rank += src[u] < e ? 1 : 0;
     dst[lo + rank] = e;
+    if (rank < kHeadEntries) hd[2 + rank] = e;
   }
 }
 
@@ -537,10 +552,10 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
   const int hr = p.Hr == 1 ? 0 : h;
   const int K = p.K;
   const int64_t bhr = b * p.Hr + hr;
-  const int* off = p.ws.offs + bhr * (p.nKV + 1);
-  const int lo = off[j], hi = off[j + 1];
+  // the chunk's header row: lane i < kHeadInts holds int i
+  const int hv = lane < kHeadInts ? p.ws.head[(bhr * p.nKV + j) * kHeadInts + lane] : 0;
+  const int lo = __builtin_amdgcn_readlane(hv, 0), n = __builtin_amdgcn_readlane(hv, 1);
   const int* list_g = p.ws.sorted + bhr * p.nQ * K + lo;
-  const int n = hi - lo;
 
   const int64_t key0 = (bh * p.nKV + j) * kS;  // first key token of chunk j
   T* dk = reinterpret_cast<T*>(p.dk) + key0 * kD;
@@ -572,8 +587,8 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
   const TileCopy<T, 2> cp(wave, lane);
   const uint32_t col_off = (uint32_t)(lane * sizeof(float));
   const int64_t lq_len = p.nQ * kS;
-  auto issue = [&](int slot, int u) __device__ {
-    const int cs = sE[u];  // (query chunk << 5) | slot
+  auto enc = [&](int e) { return ((e / K + p.causal) << 5) | (e % K); };  // list entry t*K+s -> (query chunk << 5) | slot
+  auto issue = [&](int slot, int cs) __device__ {
     const int64_t c = cs >> 5;
     const int s = cs & 31;
     T* dst = ring + slot * ENTRY;
@@ -689,20 +704,27 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
   };
 
   // the retriever list is staged through LDS in batches, each streamed through
-  // the ring (one item in flight ahead of the compute) and drained at its end
+  // the ring (one item in flight ahead of the compute) and drained at its end.
+  // The first batch: its first copy straight from the header, its first entries
+  // from the header and the rest from the list, in flight with that copy and the
+  // K/V fragments (round 0's barrier makes them visible)
   for (int b0 = 0; b0 < n; b0 += NE) {
     const int nb = min(NE, n - b0);
-    __syncthreads();
-    for (int i = tid; i < nb; i += kKvThreads) {
-      const int e = list_g[b0 + i];  // t * K + s
-      sE[i] = ((e / K + p.causal) << 5) | (e % K);
+    if (b0 == 0) {
+      issue(0, enc(__builtin_amdgcn_readlane(hv, 2)));
+      const int e_head = __shfl(hv, (lane + 2) & 63);  // lane i: header entry i
+      if (wave == 0 && lane < kHeadEntries && lane < nb) sE[lane] = enc(e_head);
+      for (int i = kHeadEntries + tid; i < nb; i += kKvThreads) sE[i] = enc(list_g[i]);
+    } else {
+      __syncthreads();
+      for (int i = tid; i < nb; i += kKvThreads) sE[i] = enc(list_g[b0 + i]);
+      __syncthreads();
+      issue(0, sE[0]);
     }
-    __syncthreads();
-    issue(0, 0);
     for (int u = 0; u < nb; ++u) {
       wait_vmem<0>();
       block_barrier();
-      if (u + 1 < nb) issue((u + 1) & 1, u + 1);
+      if (u + 1 < nb) issue((u + 1) & 1, sE[u + 1]);
       run(u & 1);
     }
   }
@@ -957,7 +979,7 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
   launch_kernel("csr_fill_kernel", csr_fill_kernel, dim3(blocks_for(nent, 256)), dim3(256), 0, st, p.idx, w.cursor,
                 w.unsorted, BHr, s.nQ, s.topk, s.nKV, s.causal);
   launch_kernel("csr_sort_kernel", csr_sort_kernel, dim3(blocks_for(BHr * s.nKV, 4)), dim3(256), 0, st, w.offs,
-                w.unsorted, w.sorted, BHr, s.nQ, s.topk, s.nKV);
+                w.unsorted, w.sorted, w.head, BHr, s.nQ, s.topk, s.nKV);
   const int64_t nq_work = BH * s.nQ, nk_work = BH * s.nKV;
   // persistent: kWgPerCu workgroups per CU, kPairs chunk streams each
   const int64_t dq_wgs = std::min<int64_t>(256 * kWgPerCu, round8((nq_work + kPairs - 1) / kPairs));
