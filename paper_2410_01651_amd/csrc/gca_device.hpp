@@ -221,23 +221,6 @@ __device__ __forceinline__ void dma_column_s(const float* g, uint32_t lane_off, 
                : "m0");
 }
 
-// The same loop over one ring array with runtime slot indices (no per-slot code
-// copies, so the compiler keeps one set of lane address offsets).
-template <typename Issue, typename Run>
-__device__ __forceinline__ void pair_ring_dyn(int n, int pair, Issue&& issue, Run&& run) {
-  issue(0, 0);
-  if (n > 1) issue(1, 1);
-  for (int v = 0; 2 * v < n; ++v) {
-    wait_vmem<0>();
-    block_barrier();
-    const int base = 2 * (v & 1);
-    if (2 * v + 2 < n) issue(2 - base, 2 * v + 2);
-    if (2 * v + 3 < n) issue(3 - base, 2 * v + 3);
-    const int u = 2 * v + pair;
-    if (u < n) run(base + pair, u);
-  }
-}
-
 // Fragments from a swizzled tile: 8 consecutive elements of row r from column col
 // (a multiple of 8) ...
 __device__ __forceinline__ bf16x8 lds_frag(const __bf16* tile, int r, int col) {

@@ -871,10 +871,11 @@ inline GatherShape gather_shape(int D, int elem_bytes) {
 }
 
 // dlmk_q[t] = score_scale * sum_s dsel[t, s] lmk_k[idx[t, s]]
+// The row's dsel (as dsel_kernel computes it, the same summation order) is
+// formed here and written out, so the backward needs no separate dsel launch
+// when the landmark-query gradient is wanted: all 256 threads read the head
+// classes of the dw partials, and the first wave forms dsel.
 template <typename T>
-// The row's dsel (as dsel_kernel computes it) is formed here by the first wave
-// and written out, so the backward needs no separate dsel launch when the
-// landmark-query gradient is wanted.
 __global__ __launch_bounds__(256) void dlmk_q_kernel(const T* __restrict__ lk, const int32_t* __restrict__ idx,
                                                      const float* __restrict__ w, const float* __restrict__ dwp,
                                                      float* __restrict__ dsel, float* __restrict__ dlq,

@@ -260,6 +260,41 @@ def test_xattn_only_entry_points(dev):
         assert max_abs_rel(host64(g[key]), ref) <= 1e-4, key
 
 
+@pytest.mark.parametrize("name", ["tiny_fp32_1k", "fwdbwd_64k_bf16"])
+def test_backward_hot_key_chunk(dev, name):
+    """Every row retrieves chunk 0 (599 retrievers, more than one staged batch of the
+    key-stationary pass's list) plus up to two other earlier chunks, from an index set
+    chosen by the caller; forward and backward against the oracle."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w = get_workload(name, B=1, H=2, n_chunks=600, topk=4, whole_reseed=False)
+    inp = gi.draw_tokens(w, with_dout=True)
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    nC, k = w.n_chunks, w.topk
+    idx = np.full((1, 1, nC, k), -1, np.int32)
+    sel = np.full((1, 1, nC, k), -np.inf, np.float32)
+    rng = np.random.default_rng(5)
+    for r in range(1, nC):
+        idx[0, 0, r, 0] = 0
+        sel[0, 0, r, 0] = rng.standard_normal()
+        if r > 1:
+            for s, j in zip((1, 2), sorted(rng.choice(np.arange(1, r), size=min(r - 1, 2), replace=False))):
+                idx[0, 0, r, s] = j
+                sel[0, 0, r, s] = rng.standard_normal()
+    assert int((idx == 0).sum()) == nC - 1
+    ti, ts = torch.from_numpy(idx).to(dev), torch.from_numpy(sel).to(dev)
+    out, lse, wt = gca.grouped_xattn_fwd(p, t["q"], t["k"], t["v"], ti, ts)
+    x = decode_all(w, inp)
+    w_ref = og.fusion_weights(sel.astype(np.float64))
+    o_ref, _ = og.xattn_fwd(x["q"], x["k"], x["v"], idx, w_ref, w.S, w.attn_scale)
+    assert max_abs_rel(host64(out), o_ref) <= TOL[w.dtype]
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], ti, ts, lse, t["dout"], landmark_grads=False)
+    dq, dk, dv, dw = og.xattn_bwd(x["q"], x["k"], x["v"], idx, w_ref, x["dout"], w.S, w.attn_scale)
+    for key, ref in (("dq", dq), ("dk", dk), ("dv", dv), ("dsel", og.dsel_from_dw(w_ref, dw))):
+        assert max_abs_rel(host64(g[key]), ref) <= TOL[w.dtype], key
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_decode_xattn_only_entry_point(dev, dtype):
     """gca_grouped_xattn_fwd in decode mode with an index set chosen by the caller:
