@@ -432,3 +432,41 @@ def test_selection_reused_by_layers(dev):
         dq, dk, dv, _ = og.xattn_bwd(y["q"], y["k"], y["v"], ref["idx"], ref["w"], y["dout"], w.S, w.attn_scale)
         for key, r in (("dq", dq), ("dk", dk), ("dv", dv)):
             assert max_abs_rel(host64(g[key]), r) <= TOL[w.dtype], (layer, key)
+
+
+def test_profile_hook(dev):
+    """The per-kernel timing hook: kernels are timed in launch order up to the
+    capacity, named, with positive durations, and the results do not change."""
+    import ctypes
+    import torch
+    from paper_2410_01651_amd import gca
+    w, inp = _case("tiny_fp32_1k")
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    ref = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    ev = (ctypes.c_void_p * 4)()
+    for i in range(4):
+        assert hip.hipEventCreate(ctypes.byref(ev, i * ctypes.sizeof(ctypes.c_void_p))) == 0
+    try:
+        torch.cuda.synchronize()
+        gca.profile_arm(ev, 4)                     # room for two kernels of the three
+        f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+        torch.cuda.synchronize()
+        names = gca.profile_record()
+        gca.profile_arm(None, 0)
+        assert names == ["chunk_scores_kernel", "topk_kernel"]
+        for i in range(2):
+            ms = ctypes.c_float()
+            assert hip.hipEventElapsedTime(ctypes.byref(ms), ev[2 * i], ev[2 * i + 1]) == 0
+            assert ms.value > 0.0
+        for key in ("out", "idx", "sel", "lse", "w"):
+            assert torch.equal(f[key], ref[key]), key
+        gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])  # disarmed: nothing recorded
+        torch.cuda.synchronize()
+        assert gca.profile_record() == []
+    finally:
+        gca.profile_arm(None, 0)
+        for i in range(4):
+            hip.hipEventDestroy(ctypes.c_void_p(ev[i]))
