@@ -683,8 +683,18 @@ __device__ __forceinline__ void merge_wave_results(int K, float* sS, int* sJ, in
   }
 }
 
-// Best k (<= 32) of one retrieval row from per-range lists: list l (of `lists`)
-// holds the best k of chunks [l * pw, (l + 1) * pw), sorted best first and
+// The decode scan's lists: scan workgroup g covers chunks [4 g pw, 4 (g + 1) pw)
+// in groups of 8 consecutive chunks, its wave w taking groups w, w + 4, w + 8, ...
+// (the four waves stream one contiguous range side by side) and leaving list
+// 4 g + w.  The list that holds chunk c:
+constexpr int kScanListWaves = 4;
+__device__ __forceinline__ int64_t scan_list_of(int64_t c, int64_t pw) {
+  const int64_t span = kScanListWaves * pw;
+  return (c / span) * kScanListWaves + ((c % span) / 8) % kScanListWaves;
+}
+
+// Best k (<= 32) of one retrieval row from the decode scan's lists: list l (of
+// `lists`) holds the best k of its chunks (scan_list_of), sorted best first and
 // padded with chunk -1, at ls/lj[(row * lists + l) * K ..].  Every wave takes a
 // contiguous share of the lists and the best k of their maxima; an entry of the
 // row's top k can only sit in a list whose maximum is among the k best of its
@@ -740,7 +750,7 @@ __device__ void merge_lists(const float* __restrict__ ls, const int* __restrict_
     const int src = lane / K;
     const int head = __shfl(mj, src);  // every lane takes part in the exchange
     if (lane < ne) {
-      const int64_t l = (int64_t)head / pw;
+      const int64_t l = scan_list_of(head, pw);
       const int64_t off = l * K + (lane - src * K);
       const int jj = rj[off];
       if (jj >= 0) {
@@ -753,7 +763,7 @@ __device__ void merge_lists(const float* __restrict__ ls, const int* __restrict_
     L.init();
     for (int e = lane; e < ne; e += 64) {
       const int src = e / K;
-      const int64_t l = (int64_t)__shfl(mj, src) / pw;
+      const int64_t l = scan_list_of(__shfl(mj, src), pw);
       const int64_t off = l * K + (e - src * K);
       const int jj = rj[off];
       if (jj >= 0) L.insert(rs[off], jj);

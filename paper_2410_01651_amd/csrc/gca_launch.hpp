@@ -33,9 +33,10 @@ hipError_t launch_topk(const Shape& s, const float* scores, int32_t* idx, float*
                        hipStream_t stream);
 // Decode selection, first half: a split scan of all past landmark keys (Eq. 1)
 // that leaves, for every retrieval row, `lists` lists of the best k of `pw`
-// consecutive chunks each (in the workspace).  The decode attention merges them.
+// chunks each (in the workspace; scan_list_of gives a chunk's list).  The decode
+// attention merges them.
 struct DecodePlan {
-  int64_t pw;     // chunks per list (one scan wave's contiguous range)
+  int64_t pw;     // chunks per list (a quarter of one scan workgroup's contiguous range)
   int64_t lists;  // lists per retrieval row
   int64_t wgs;    // scan workgroups per row
 };
