@@ -142,7 +142,7 @@ def measured_traffic(kernel):
     counter summary, or None when there is none or the kernels changed since."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
-        from paper_2410_01651_amd.profiling import source_hash
+        from profiling import source_hash
         data = json.load(open(path))
         if data.get("source_sha256") != source_hash():
             return None

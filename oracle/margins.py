@@ -39,9 +39,11 @@ def row_gaps(lmk_q64, lmk_k64, score_scale, k, mode, rows=None, gumbel_seed=None
             rb = r[b, hr]
             if gumbel_seed is not None:
                 rb = rb + gca.gumbel_noise(gumbel_seed, bhr0 + b * Hr + hr, rows_[:, None], np.arange(nC)[None, :])
-            srt = -np.sort(-rb, axis=1)               # descending, -inf last
             if nC > k:
-                kth, nxt = srt[:, k - 1], srt[:, k]
+                # the k-th and (k+1)-th largest of each row (order statistics,
+                # -inf last): a partial sort gives exactly what a full sort would
+                part = -np.partition(-rb, [k - 1, k], axis=1)
+                kth, nxt = part[:, k - 1], part[:, k]
                 ok = np.isfinite(nxt)
                 gaps[b, hr] = np.where(ok, kth - np.where(ok, nxt, 0.0), np.inf)
     return gaps
@@ -68,14 +70,24 @@ def enforce(w, lmk_q, lmk_k, max_attempts=1000):
     """Redraw failing landmark-query rows in place until every margin holds."""
     target = gi.plant_target_row(w) if (w.planted and w.mode == "causal") else None
     pending = _failing_rows(w, lmk_q, lmk_k)
+    keys64 = {}                                   # decoded key slices, one per (b, hr)
+    plant = gi.plant_positions(w)
     for (b, hr, t) in pending:
         if t == target:
             raise RuntimeError("planted target row lost its margin")
+        if (b, hr) not in keys64:
+            keys64[(b, hr)] = gi.decode(w, lmk_k[b:b + 1, hr:hr + 1])
+        k64 = keys64[(b, hr)]
         for attempt in range(1, max_attempts + 1):
             gi.redraw_lmk_q_row(w, lmk_q, lmk_k, b, hr, t, attempt)
-            g = row_gaps(gi.decode(w, lmk_q[b:b + 1, hr:hr + 1]),
-                         gi.decode(w, lmk_k[b:b + 1, hr:hr + 1]),
-                         w.score_scale, w.topk, w.mode, rows=[t], gumbel_seed=_seed(w), bhr0=b * w.Hr + hr)
+            if w.planted and t == gi.plant_target_row(w):
+                k64[0, 0, plant] = gi.decode(w, lmk_k[b, hr, plant])   # planted keys follow the row
+            # row t's gap from its own query (a broadcast view stands in for the
+            # other rows, which the gap of row t does not read)
+            q_row = gi.decode(w, lmk_q[b, hr, t])
+            q64 = np.broadcast_to(q_row, (1, 1, t + 1, q_row.shape[-1]))
+            g = row_gaps(q64, k64, w.score_scale, w.topk, w.mode, rows=[t], gumbel_seed=_seed(w),
+                         bhr0=b * w.Hr + hr)
             if g[0, 0, 0] >= w.margin:
                 break
         else:

@@ -5,9 +5,10 @@
 #include <cmath>
 #include <cstddef>
 #include <cstdint>
+#include <cstdlib>
 #include <string>
 
-#include "gca_launch.hpp"
+#include "gca_plan.hpp"
 
 namespace {
 
@@ -28,7 +29,10 @@ gca_status fail(gca_status s, const std::string& msg) {
 
 gca_status from_hip(hipError_t e, const char* what) {
   if (e == hipSuccess) return GCA_OK;
-  return fail(GCA_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  std::string msg = std::string(what) + ": " + hipGetErrorString(e);
+  const char* kernel = gca::launch_error_kernel();
+  if (kernel[0]) msg += std::string(" (kernel ") + kernel + ")";
+  return fail(GCA_ERR_HIP, msg);
 }
 
 constexpr int64_t kMaxGrid = 2147483647;  // largest 1-D grid we launch
@@ -144,6 +148,8 @@ gca_status check_ws(void* ws, size_t have, size_t need) {
 
 namespace gca {
 thread_local hipError_t g_launch_error = hipSuccess;
+thread_local const char* g_launch_error_kernel = "";
+thread_local const char* g_reported_kernel = "";
 
 bool profile_slot(const char* kernel, hipEvent_t* start, hipEvent_t* stop) {
   ProfileHook& h = g_profile;
@@ -155,15 +161,33 @@ bool profile_slot(const char* kernel, hipEvent_t* start, hipEvent_t* stop) {
   return true;
 }
 
-void note_launch_error(hipError_t e) {
-  if (e != hipSuccess && g_launch_error == hipSuccess) g_launch_error = e;
+void note_launch_error(hipError_t e, const char* kernel) {
+  if (e != hipSuccess && g_launch_error == hipSuccess) {
+    g_launch_error = e;
+    g_launch_error_kernel = kernel;
+  }
 }
 
 hipError_t take_launch_error() {
   hipError_t e = g_launch_error;
+  g_reported_kernel = g_launch_error_kernel;
   g_launch_error = hipSuccess;
-  if (e == hipSuccess) e = hipGetLastError();
+  g_launch_error_kernel = "";
+  if (e == hipSuccess) {
+    e = hipGetLastError();
+    g_reported_kernel = "";
+  }
   return e;
+}
+
+const char* launch_error_kernel() { return g_reported_kernel; }
+
+bool debug_sync() {
+  static const bool on = [] {
+    const char* v = std::getenv("GCA_DEBUG_SYNC");
+    return v != nullptr && v[0] != '\0' && !(v[0] == '0' && v[1] == '\0');
+  }();
+  return on;
 }
 }  // namespace gca
 
@@ -285,24 +309,11 @@ gca_status gca_grouped_xattn_bwd(const gca_problem* p, const void* q, const void
                   "gca_grouped_xattn_bwd");
 }
 
-gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_k, const void* q, const void* k,
-                       const void* v, void* out, int32_t* idx, float* sel, float* lse, float* w, void* workspace,
-                       size_t ws_bytes, hipStream_t stream) {
-  gca::Shape s;
-  GCA_TRY(check_problem(p, s));
-  GCA_TRY(check_ptr(lmk_q, "lmk_q", true, 16));
-  GCA_TRY(check_ptr(lmk_k, "lmk_k", true, 16));
-  GCA_TRY(check_ptr(q, "q", true, 16));
-  GCA_TRY(check_ptr(k, "k", true, 16));
-  GCA_TRY(check_ptr(v, "v", true, 16));
-  GCA_TRY(check_ptr(out, "out", true, 16));
-  GCA_TRY(check_ptr(idx, "idx", true, 4));
-  GCA_TRY(check_ptr(sel, "sel", true, 4));
-  GCA_TRY(check_ptr(lse, "lse", false, 4));
-  GCA_TRY(check_ptr(w, "w", false, 4));
-  GCA_TRY(check_ws(workspace, ws_bytes, forward_ws(p, s)));
-  GCA_TRY(device_view(p, k, "k"));
-  GCA_TRY(device_view(p, v, "v"));
+// The forward path after validation: the selection (decode scan, single-pass
+// select or score matrix + top-k) then the attention, on `workspace`.
+static gca_status forward_dispatch(const gca_problem* p, const gca::Shape& s, const void* lmk_q, const void* lmk_k,
+                                   const void* q, const void* k, const void* v, void* out, int32_t* idx,
+                                   float* sel, float* lse, float* w, void* workspace, hipStream_t stream) {
   (void)hipGetLastError();
   (void)gca::take_launch_error();
   hipError_t e;
@@ -324,6 +335,34 @@ gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_
   }
   if (e != hipSuccess) return from_hip(e, "gca_forward (selection)");
   return from_hip(gca::launch_xattn_fwd(s, q, k, v, idx, sel, out, lse, w, stream), "gca_forward (attention)");
+}
+
+static gca_status check_forward_args(const gca_problem* p, gca::Shape& s, const void* lmk_q,
+                                     const void* lmk_k, const void* q, const void* k, const void* v, void* out,
+                                     int32_t* idx, float* sel, float* lse, float* w) {
+  GCA_TRY(check_problem(p, s));
+  GCA_TRY(check_ptr(lmk_q, "lmk_q", true, 16));
+  GCA_TRY(check_ptr(lmk_k, "lmk_k", true, 16));
+  GCA_TRY(check_ptr(q, "q", true, 16));
+  GCA_TRY(check_ptr(k, "k", true, 16));
+  GCA_TRY(check_ptr(v, "v", true, 16));
+  GCA_TRY(check_ptr(out, "out", true, 16));
+  GCA_TRY(check_ptr(idx, "idx", true, 4));
+  GCA_TRY(check_ptr(sel, "sel", true, 4));
+  GCA_TRY(check_ptr(lse, "lse", false, 4));
+  GCA_TRY(check_ptr(w, "w", false, 4));
+  return GCA_OK;
+}
+
+gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_k, const void* q, const void* k,
+                       const void* v, void* out, int32_t* idx, float* sel, float* lse, float* w, void* workspace,
+                       size_t ws_bytes, hipStream_t stream) {
+  gca::Shape s;
+  GCA_TRY(check_forward_args(p, s, lmk_q, lmk_k, q, k, v, out, idx, sel, lse, w));
+  GCA_TRY(check_ws(workspace, ws_bytes, forward_ws(p, s)));
+  GCA_TRY(device_view(p, k, "k"));
+  GCA_TRY(device_view(p, v, "v"));
+  return forward_dispatch(p, s, lmk_q, lmk_k, q, k, v, out, idx, sel, lse, w, workspace, stream);
 }
 
 }  // extern "C"

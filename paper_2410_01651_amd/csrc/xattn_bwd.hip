@@ -31,56 +31,6 @@ constexpr int kPairs = 1;
 constexpr int kThreads = 128 * kPairs;
 constexpr int kWgPerCu = 4 / kPairs;
 
-// per key chunk, one 64-byte row: [0] offset of its list in `sorted`, [1] its
-// length, [2 .. 2 + kHeadEntries) its first entries, so the key-stationary pass
-// starts a chunk's first copy one dependent load after its launch
-constexpr int kHeadInts = 16;
-constexpr int kHeadEntries = 8;
-
-struct Ws {
-  float* w;        // [B*Hr, nQ, K] fusion weights
-  float* Dbuf;     // [B*H, K, Lq]  -D_s per query token (slot-major: one slot's tokens contiguous)
-  float* Lbuf;     // [B*H, K, Lq]  log2 of 1 / (w_s exp(-lse)): log2(e) lse - log2(w_s)
-  float* dwp;      // [B*H, nQ, K, 2] dw partials per head and query half
-  int* counts;     // [B*Hr, nKV]
-  int* cursor;     // [B*Hr, nKV]
-  int* offs;       // [B*Hr, nKV+1]
-  int* unsorted;   // [B*Hr, nQ*K]
-  int* sorted;     // [B*Hr, nQ*K]
-  int* head;       // [B*Hr, nKV, kHeadInts]  per key chunk: list offset, count, first entries
-};
-
-Ws carve(const Shape& s, void* base) {
-  const int64_t BHr = (int64_t)s.B * s.Hr, BH = (int64_t)s.B * s.H;
-  char* p = reinterpret_cast<char*>(base);
-  Ws w;
-  auto take = [&](size_t bytes) { char* r = p; p += align256(bytes); return r; };
-  w.w = (float*)take(sizeof(float) * BHr * s.nQ * s.topk);
-  w.Dbuf = (float*)take(sizeof(float) * BH * s.nQ * kS * s.topk);
-  w.Lbuf = (float*)take(sizeof(float) * BH * s.nQ * kS * s.topk);
-  w.dwp = (float*)take(sizeof(float) * BH * s.nQ * s.topk * 2);
-  w.counts = (int*)take(sizeof(int) * BHr * s.nKV);
-  w.cursor = (int*)take(sizeof(int) * BHr * s.nKV);
-  w.offs = (int*)take(sizeof(int) * BHr * (s.nKV + 1));
-  w.unsorted = (int*)take(sizeof(int) * BHr * s.nQ * s.topk);
-  w.sorted = (int*)take(sizeof(int) * BHr * s.nQ * s.topk);
-  w.head = (int*)take(sizeof(int) * BHr * s.nKV * kHeadInts);
-  return w;
-}
-
-size_t carve_size(const Shape& s) {
-  const int64_t BHr = (int64_t)s.B * s.Hr, BH = (int64_t)s.B * s.H;
-  size_t n = 0;
-  n += align256(sizeof(float) * BHr * s.nQ * s.topk);
-  n += align256(sizeof(float) * BH * s.nQ * kS * s.topk) * 2;
-  n += align256(sizeof(float) * BH * s.nQ * s.topk * 2);
-  n += align256(sizeof(int) * BHr * s.nKV) * 2;
-  n += align256(sizeof(int) * BHr * (s.nKV + 1));
-  n += align256(sizeof(int) * BHr * s.nQ * s.topk) * 2;
-  n += align256(sizeof(int) * BHr * s.nKV * kHeadInts);
-  return n;
-}
-
 struct BwdParams {
   const void* q;
   const void* k;
@@ -92,7 +42,7 @@ struct BwdParams {
   void* dq;
   void* dk;
   void* dv;
-  Ws ws;
+  BwdWs ws;
   int B, H, Hr, K;
   int64_t nQ, nKV;
   int causal;
@@ -968,7 +918,7 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
                         float* dlmk_q, float* dlmk_k, hipStream_t st) {
   const int64_t BHr = (int64_t)s.B * s.Hr, BH = (int64_t)s.B * s.H;
   const int64_t nent = BHr * s.nQ * s.topk;
-  Ws& w = p.ws;
+  BwdWs& w = p.ws;
   launch_kernel("weights_kernel", weights_kernel, dim3(blocks_for(nent, 256)), dim3(256), 0, st, p.idx, p.sel, w.w,
                 BHr * s.nQ, s.topk, s.nKV);
   const unsigned zblocks = std::min(blocks_for(BHr * s.nKV, 256), 4096u);
@@ -983,7 +933,8 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
                 w.unsorted, w.sorted, w.head, BHr, s.nQ, s.topk, s.nKV);
   const int64_t nq_work = BH * s.nQ, nk_work = BH * s.nKV;
   // persistent: kWgPerCu workgroups per CU, kPairs chunk streams each
-  const int64_t dq_wgs = std::min<int64_t>(256 * kWgPerCu, round8((nq_work + kPairs - 1) / kPairs));
+  const int64_t dq_wgs =
+      std::min<int64_t>(round8((int64_t)device_cus() * kWgPerCu), round8((nq_work + kPairs - 1) / kPairs));
   if (s.topk <= kDqStageK)
     launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T, true>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
   else
@@ -1010,8 +961,6 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
 
 }  // namespace
 
-size_t bwd_workspace(const Shape& s) { return carve_size(s); }
-
 hipError_t launch_xattn_bwd(const Shape& s, const void* q, const void* k, const void* v, const int32_t* idx,
                             const float* sel, const float* lse, const void* dout, void* dq, void* dk, void* dv,
                             float* dsel, const void* lmk_q, const void* lmk_k, float* dlmk_q, float* dlmk_k,
@@ -1019,7 +968,7 @@ hipError_t launch_xattn_bwd(const Shape& s, const void* q, const void* k, const 
   BwdParams p;
   p.q = q; p.k = k; p.v = v; p.idx = idx; p.sel = sel; p.lse = lse; p.dout = dout;
   p.dq = dq; p.dk = dk; p.dv = dv;
-  p.ws = carve(s, ws);
+  p.ws = bwd_carve(s, ws);
   p.B = s.B; p.H = s.H; p.Hr = s.Hr; p.K = s.topk;
   p.nQ = s.nQ; p.nKV = s.nKV;
   p.causal = s.causal;

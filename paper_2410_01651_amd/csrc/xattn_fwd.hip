@@ -389,9 +389,9 @@ hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const 
   p.nwork = (int64_t)s.B * s.H * s.nQ;
   p.causal = s.causal;
   p.attn_scale = s.attn_scale;
-  // persistent workgroups: kWgPerCu per CU (256 CUs), a multiple of 8 (one share
-  // per XCD), each running kPairs chunk streams
-  const int64_t target = 256 * kWgPerCu, wgs = (p.nwork + kPairs - 1) / kPairs;
+  // persistent workgroups: kWgPerCu per CU, a multiple of 8 (one share per XCD),
+  // each running kPairs chunk streams
+  const int64_t target = round8((int64_t)device_cus() * kWgPerCu), wgs = (p.nwork + kPairs - 1) / kPairs;
   const dim3 grid((unsigned)(wgs < target ? round8(wgs) : target)), block(kThreads);
   if (s.bf16) {
     if (s.off_by_one) {

@@ -172,6 +172,17 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _alloc_on(stream):
+    """Context for allocating outputs and workspace that the kernels use on
+    `stream`: torch's caching allocator then ties the blocks to that stream, so a
+    temporary freed on return is not handed to other streams' work while the
+    kernels may still run."""
+    import contextlib
+    if stream is None:
+        return contextlib.nullcontext()
+    return _torch().cuda.stream(stream)
+
+
 @dataclass
 class Shapes:
     lmk_q: tuple
@@ -208,8 +219,9 @@ def workspace(p: Problem, op: int, device="cuda"):
 def chunk_scores(p: Problem, lmk_q, lmk_k, scores=None, stream=None):
     torch = _torch()
     sh, dt = shapes(p), _elem_dtype(p)
-    if scores is None:
-        scores = torch.empty(sh.scores, dtype=torch.float32, device=lmk_q.device)
+    with _alloc_on(stream):
+        if scores is None:
+            scores = torch.empty(sh.scores, dtype=torch.float32, device=lmk_q.device)
     _check(lib().gca_chunk_scores(ctypes.byref(p), _ptr(lmk_q, "lmk_q", dt, sh.lmk_q),
                                   _ptr(lmk_k, "lmk_k", dt, sh.lmk_k),
                                   _ptr(scores, "scores", torch.float32, sh.scores), _stream(stream)))
@@ -219,10 +231,11 @@ def chunk_scores(p: Problem, lmk_q, lmk_k, scores=None, stream=None):
 def topk(p: Problem, scores, idx=None, sel=None, stream=None):
     torch = _torch()
     sh = shapes(p)
-    if idx is None:
-        idx = torch.empty(sh.rows, dtype=torch.int32, device=scores.device)
-    if sel is None:
-        sel = torch.empty(sh.rows, dtype=torch.float32, device=scores.device)
+    with _alloc_on(stream):
+        if idx is None:
+            idx = torch.empty(sh.rows, dtype=torch.int32, device=scores.device)
+        if sel is None:
+            sel = torch.empty(sh.rows, dtype=torch.float32, device=scores.device)
     _check(lib().gca_topk(ctypes.byref(p), _ptr(scores, "scores", torch.float32, sh.scores),
                           _ptr(idx, "idx", torch.int32, sh.rows), _ptr(sel, "sel", torch.float32, sh.rows),
                           _stream(stream)))
@@ -234,12 +247,13 @@ def grouped_xattn_fwd(p: Problem, q, k, v, idx, sel, out=None, lse=None, w=None,
     torch = _torch()
     sh, dt = shapes(p), _elem_dtype(p)
     dev = q.device
-    if out is None:
-        out = torch.empty(sh.q, dtype=dt, device=dev)
-    if lse is None and want_lse:
-        lse = torch.empty(sh.lse, dtype=torch.float32, device=dev)
-    if w is None and want_w:
-        w = torch.empty(sh.rows, dtype=torch.float32, device=dev)
+    with _alloc_on(stream):
+        if out is None:
+            out = torch.empty(sh.q, dtype=dt, device=dev)
+        if lse is None and want_lse:
+            lse = torch.empty(sh.lse, dtype=torch.float32, device=dev)
+        if w is None and want_w:
+            w = torch.empty(sh.rows, dtype=torch.float32, device=dev)
     _check(lib().gca_grouped_xattn_fwd(
         ctypes.byref(p), _ptr(q, "q", dt, sh.q),
         _ptr(k, "k", dt, sh.kv, _host_kv(p)), _ptr(v, "v", dt, sh.kv, _host_kv(p)),
@@ -256,17 +270,19 @@ def grouped_xattn_bwd(p: Problem, q, k, v, idx, sel, lse, dout, lmk_q=None, lmk_
     sh, dt = shapes(p), _elem_dtype(p)
     dev = q.device
     g = dict(grads or {})
-    for name, shape, gdt in (("dq", sh.q, dt), ("dk", sh.kv, dt), ("dv", sh.kv, dt),
-                             ("dsel", sh.rows, torch.float32)):
-        if name not in g:
-            g[name] = torch.empty(shape, dtype=gdt, device=dev)
-    if landmark_grads:
-        g.setdefault("dlmk_q", torch.empty(sh.lmk_q, dtype=torch.float32, device=dev))
-        g.setdefault("dlmk_k", torch.empty(sh.lmk_k, dtype=torch.float32, device=dev))
-    if ws is None:
-        ws, nbytes = workspace(p, OP_BACKWARD, dev)
-    else:
-        nbytes = ws.numel()
+    with _alloc_on(stream):
+        for name, shape, gdt in (("dq", sh.q, dt), ("dk", sh.kv, dt), ("dv", sh.kv, dt),
+                                 ("dsel", sh.rows, torch.float32)):
+            if name not in g:
+                g[name] = torch.empty(shape, dtype=gdt, device=dev)
+        if landmark_grads:
+            for name, shape in (("dlmk_q", sh.lmk_q), ("dlmk_k", sh.lmk_k)):
+                if name not in g:
+                    g[name] = torch.empty(shape, dtype=torch.float32, device=dev)
+        if ws is None:
+            ws, nbytes = workspace(p, OP_BACKWARD, dev)
+        else:
+            nbytes = ws.numel()
     _check(lib().gca_grouped_xattn_bwd(
         ctypes.byref(p), _ptr(q, "q", dt, sh.q),
         _ptr(k, "k", dt, sh.kv, _host_kv(p)), _ptr(v, "v", dt, sh.kv, _host_kv(p)),
@@ -288,20 +304,21 @@ def forward(p: Problem, lmk_q, lmk_k, q, k, v, out=None, idx=None, sel=None, lse
     torch = _torch()
     sh, dt = shapes(p), _elem_dtype(p)
     dev = q.device
-    if out is None:
-        out = torch.empty(sh.q, dtype=dt, device=dev)
-    if idx is None:
-        idx = torch.empty(sh.rows, dtype=torch.int32, device=dev)
-    if sel is None:
-        sel = torch.empty(sh.rows, dtype=torch.float32, device=dev)
-    if lse is None and want_lse:
-        lse = torch.empty(sh.lse, dtype=torch.float32, device=dev)
-    if w is None and want_w:
-        w = torch.empty(sh.rows, dtype=torch.float32, device=dev)
-    if ws is None:
-        ws, nbytes = workspace(p, OP_FORWARD, dev)
-    else:
-        nbytes = ws.numel()
+    with _alloc_on(stream):
+        if out is None:
+            out = torch.empty(sh.q, dtype=dt, device=dev)
+        if idx is None:
+            idx = torch.empty(sh.rows, dtype=torch.int32, device=dev)
+        if sel is None:
+            sel = torch.empty(sh.rows, dtype=torch.float32, device=dev)
+        if lse is None and want_lse:
+            lse = torch.empty(sh.lse, dtype=torch.float32, device=dev)
+        if w is None and want_w:
+            w = torch.empty(sh.rows, dtype=torch.float32, device=dev)
+        if ws is None:
+            ws, nbytes = workspace(p, OP_FORWARD, dev)
+        else:
+            nbytes = ws.numel()
     _check(lib().gca_forward(
         ctypes.byref(p), _ptr(lmk_q, "lmk_q", dt, sh.lmk_q), _ptr(lmk_k, "lmk_k", dt, sh.lmk_k),
         _ptr(q, "q", dt, sh.q),

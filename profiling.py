@@ -1,7 +1,7 @@
 """Summaries of rocprofv3 output for the profiles/ folder.
 
-    python -m paper_2410_01651_amd.profiling stats   --csv DIR/run_kernel_stats.csv --cmd "..." --out profiles/X.md
-    python -m paper_2410_01651_amd.profiling traffic --fetch DIR1/run_counter_collection.csv \
+    python profiling.py stats   --csv DIR/run_kernel_stats.csv --cmd "..." --out profiles/X.md
+    python profiling.py traffic --fetch DIR1/run_counter_collection.csv \
         --write DIR2/run_counter_collection.csv --copy-bytes N --cmd "..." --out profiles/hbm_traffic.json \
         [--tag WORKLOAD --append]
 
@@ -24,7 +24,7 @@ import os
 import statistics
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-CSRC = os.path.join(HERE, "csrc")
+CSRC = os.path.join(HERE, "paper_2410_01651_amd", "csrc")
 
 
 def source_hash() -> str:

@@ -1,10 +1,12 @@
 """Parity at the full workload sizes, in the launch configuration bench.py times.
 
-The GPU runs the whole workload; the oracle checks what it can compute one by
-one: top-k indices (exact) on every row or on a seeded sample of rows, and the
-attention outputs / gradients on sampled query chunks, heads or (batch, head)
-slices.  Per-token tensors of the large workloads are drawn on the device by the
-shared seeded generator and only the sampled slices are copied back.
+The GPU runs the whole workload and the oracle checks it: top-k indices (exact)
+on every landmark row of every workload; fusion weights, outputs and log-sum-exp
+of every chunk of the 16K training and 64K workloads; every gradient of every
+(batch, head) slice of the 64K backward.  At 1M tokens the attention output is
+checked on sampled query chunks, and at 16M on the one new chunk.  Per-token
+tensors of the large workloads are drawn on the device by the shared seeded
+generator and copied back for the oracle.
 """
 
 import numpy as np
@@ -97,22 +99,52 @@ def _check_rows_and_chunks(w, inp, t, f, rows, chunks):
         assert max_abs_rel(host64(lse[b, :, c * w.S:(c + 1) * w.S]), l_ref) <= tol, (b, c)
 
 
+def _oracle_all_rows(w, inp, b, hr=0, block=2048):
+    """Oracle scores -> top-k -> weights for every landmark row of (b, hr), computed
+    in blocks of rows."""
+    nQ = w.n_query_chunks
+    parts = [_oracle_rows(w, inp, list(range(r0, min(nQ, r0 + block))), b=b, hr=hr)
+             for r0 in range(0, nQ, block)]
+    return tuple(np.concatenate([p[i] for p in parts]) for i in range(3))
+
+
+def _check_all_rows(w, inp, f):
+    """Exact indices and fusion weights on every landmark row of every batch;
+    returns the oracle's (idx, w) per batch."""
+    tol = TOL[w.dtype]
+    gi_idx = f["idx"].cpu().numpy()
+    gs = host64(f["sel"])
+    gw = host64(f["w"])
+    ref = {}
+    for b in range(w.B):
+        ri, rs, rw = _oracle_all_rows(w, inp, b)
+        np.testing.assert_array_equal(gi_idx[b, 0], ri, err_msg=f"batch {b}")
+        assert max_abs_rel(gs[b, 0], rs) <= tol, b
+        assert max_abs_rel(gw[b, 0], rw) <= tol, b
+        ref[b] = (ri, rw)
+    return ref
+
+
 def test_train_16k_forward(dev):
-    """16,384 tokens x batch 8, 12 heads, width 768, top-8: every row's indices; sampled outputs."""
+    """16,384 tokens x batch 8, 12 heads, width 768, top-8: every row's indices and
+    weights, and out / lse of every chunk of every batch and head."""
     from paper_2410_01651_amd import gca
     w, inp, t = _setup("train_16k_bf16", dev)
     f = gca.forward(problem_for(w), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
-    rows = list(range(w.n_chunks))
-    rng = np.random.default_rng(20)
-    chunks = [(0, 0), (0, 1), (0, 2), (w.B - 1, w.n_chunks - 1)]
-    chunks += [(int(rng.integers(w.B)), int(rng.integers(2, w.n_chunks))) for _ in range(12)]
-    _check_rows_and_chunks(w, inp, t, f, rows, chunks)
+    ref = _check_all_rows(w, inp, f)
+    tol = TOL[w.dtype]
+    for b in range(w.B):
+        ri, rw = ref[b]
+        sl = lambda name: host64(t[name][b:b + 1])
+        o_ref, l_ref = og.xattn_fwd(sl("q"), sl("k"), sl("v"), ri[None, None], rw[None, None], w.S,
+                                    w.attn_scale, w.mode)
+        assert max_abs_rel(host64(f["out"][b:b + 1]), o_ref) <= tol, b
+        assert max_abs_rel(host64(f["lse"][b:b + 1]), l_ref) <= tol, b
 
 
-def test_fwdbwd_64k(dev):
-    """65,536 tokens x batch 2, 16 heads, top-8, forward + backward.  Indices on every
-    row; outputs on sampled chunks; dq/dk/dv on two whole (batch, head) slices; dsel
-    and the landmark gradients for batch 0 (which sum over all 16 heads)."""
+@pytest.fixture(scope="module")
+def fwdbwd_64k(dev):
+    """The 64K forward + backward, run once on the GPU for the tests below."""
     import torch
     from paper_2410_01651_amd import gca
     w, inp, t = _setup("fwdbwd_64k_bf16", dev)
@@ -121,29 +153,48 @@ def test_fwdbwd_64k(dev):
     g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
                               t["lmk_q"], t["lmk_k"])
     torch.cuda.synchronize()
-    rows = list(range(w.n_chunks))
-    rng = np.random.default_rng(30)
-    chunks = [(0, 1), (1, 2), (1, w.n_chunks - 1)]
-    chunks += [(int(rng.integers(w.B)), int(rng.integers(2, w.n_chunks))) for _ in range(8)]
-    _check_rows_and_chunks(w, inp, t, f, rows, chunks)
+    state = {"w": w, "inp": inp, "t": t, "f": f, "g": g, "ref": {}}
+    yield state
+    state.clear()
+    torch.cuda.empty_cache()
 
+
+def test_fwdbwd_64k_forward(fwdbwd_64k):
+    """65,536 tokens x batch 2, 16 heads, top-8: every row's indices and weights, and
+    out / lse of every chunk of both batches and all heads."""
+    w, inp, t, f = (fwdbwd_64k[k] for k in ("w", "inp", "t", "f"))
+    fwdbwd_64k["ref"] = ref = _check_all_rows(w, inp, f)
     tol = TOL[w.dtype]
-    b = 0
-    ri, rs, rw = _oracle_rows(w, inp, rows, b=b)
-    idx = ri[None, None]
-    wt = rw[None, None]
-    # dq/dk/dv on two whole slices
-    for h in (0, w.H - 1):
-        sl = lambda name: host64(t[name][b:b + 1, h:h + 1])
-        dq, dk, dv, _ = og.xattn_bwd(sl("q"), sl("k"), sl("v"), idx, wt, sl("dout"), w.S, w.attn_scale)
-        for key, ref in (("dq", dq), ("dk", dk), ("dv", dv)):
-            e = max_abs_rel(host64(g[key][b:b + 1, h:h + 1]), ref)
-            assert e <= tol, (key, h, e)
-    # score and landmark gradients of batch 0: dw sums over all heads
+    for b in range(w.B):
+        ri, rw = ref[b]
+        sl = lambda name: host64(t[name][b:b + 1])
+        o_ref, l_ref = og.xattn_fwd(sl("q"), sl("k"), sl("v"), ri[None, None], rw[None, None], w.S,
+                                    w.attn_scale, w.mode)
+        assert max_abs_rel(host64(f["out"][b:b + 1]), o_ref) <= tol, b
+        assert max_abs_rel(host64(f["lse"][b:b + 1]), l_ref) <= tol, b
+
+
+@pytest.mark.parametrize("b", [0, 1])
+def test_fwdbwd_64k_backward(fwdbwd_64k, b):
+    """The backward of one whole batch: dq, dk, dv of each of its 16 (batch, head)
+    slices, and dsel and both landmark gradients (which sum over all heads)."""
+    w, inp, t, g = (fwdbwd_64k[k] for k in ("w", "inp", "t", "g"))
+    ref = fwdbwd_64k["ref"]
+    if b in ref:
+        ri, rw = ref[b]
+    else:
+        ri, _, rw = _oracle_all_rows(w, inp, b)
+    tol = TOL[w.dtype]
     full = lambda name: host64(t[name][b:b + 1])
-    _, _, _, dw = og.xattn_bwd(full("q"), full("k"), full("v"), idx, wt, full("dout"), w.S, w.attn_scale)
-    dsel = og.dsel_from_dw(wt, dw)
-    dlq, dlk = og.landmark_grads(dsel, idx, gi.decode(w, inp["lmk_q"][b:b + 1]),
+    dq, dk, dv, dw = og.xattn_bwd(full("q"), full("k"), full("v"), ri[None, None], rw[None, None], full("dout"),
+                                  w.S, w.attn_scale)
+    for key, r in (("dq", dq), ("dk", dk), ("dv", dv)):
+        x = host64(g[key][b:b + 1])
+        for h in range(w.H):
+            e = max_abs_rel(x[:, h], r[:, h])
+            assert e <= tol, (key, b, h, e)
+    dsel = og.dsel_from_dw(rw[None, None], dw)
+    dlq, dlk = og.landmark_grads(dsel, ri[None, None], gi.decode(w, inp["lmk_q"][b:b + 1]),
                                  gi.decode(w, inp["lmk_k"][b:b + 1]), w.score_scale)
     assert max_abs_rel(host64(g["dsel"][b:b + 1]), dsel) <= tol
     assert max_abs_rel(host64(g["dlmk_q"][b:b + 1]), dlq) <= tol
@@ -152,21 +203,22 @@ def test_fwdbwd_64k(dev):
 
 def test_planted_1m_forward(dev):
     """1,048,576 tokens, 16,384 chunks (single-pass select, no score matrix): the last
-    row's top-8 is exactly the eight planted chunks with weight 1/8 each; sampled rows'
-    indices are exact and sampled chunks' outputs match."""
+    row's top-8 is exactly the eight planted chunks with weight 1/8 each; every row's
+    indices are exact; sampled chunks' outputs match."""
     from paper_2410_01651_amd import gca
     w, inp, t = _setup("planted_1m_bf16", dev)
     p = problem_for(w)
-    assert gca.workspace_size(p, gca.OP_FORWARD) == 0          # the fused path is chosen
+    ws = gca.workspace_size(p, gca.OP_FORWARD)
+    assert ws < 4 * w.n_chunks * w.n_chunks                      # the single-pass select, no score matrix
     f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
     last = w.n_chunks - 1
     pos = gi.plant_positions(w)
     assert list(f["idx"][0, 0, last].cpu().numpy()) == list(pos)
     np.testing.assert_allclose(f["w"][0, 0, last].cpu().numpy(), np.full(8, 1 / 8), rtol=1e-6)
+    _check_all_rows(w, inp, f)
     rng = np.random.default_rng(40)
-    rows = sorted(set([0, 1, 2, 7, 8, 9, 63, 64, 65, last] + [int(x) for x in rng.integers(0, w.n_chunks, 300)]))
-    chunks = [(0, 1), (0, last)] + [(0, int(c)) for c in rng.integers(2, w.n_chunks, 10)]
-    _check_rows_and_chunks(w, inp, t, f, rows, chunks)
+    chunks = [(0, 1), (0, 2), (0, 3), (0, last)] + [(0, int(c)) for c in rng.integers(4, w.n_chunks, 28)]
+    _check_rows_and_chunks(w, inp, t, f, [], chunks)
 
 
 def test_decode_16m(dev):
