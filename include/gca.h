@@ -187,6 +187,27 @@ gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_
                        int32_t* idx, float* sel, float* lse, float* w, void* workspace,
                        size_t ws_bytes, hipStream_t stream);
 
+/* gca_forward for callers that cannot allocate memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * path and results as gca_forward on the same arguments, with the workspace
+ * taken from a device array of GCA_NOALLOC_SCRATCH_BYTES that the library
+ * holds on every device it runs on until the process ends.  The caller still
+ * passes every input and output.  No memory is allocated or freed.
+ * - GCA_ERR_UNSUPPORTED if gca_workspace_size(p, GCA_OP_FORWARD) exceeds
+ *   GCA_NOALLOC_SCRATCH_BYTES (nothing is launched);
+ * - all calls on one device share that device's array: calls that overlap in
+ *   time on one device (different streams, or different threads without
+ *   ordering) race on it and must not be issued.  Calls ordered on one stream
+ *   are safe: no part of the array needs to start at any value, every byte a
+ *   call reads was written earlier in the same call.
+ * - GCA_ERR_HIP if the array's device address cannot be looked up (once per
+ *   device, on the first call there). */
+#define GCA_NOALLOC_SCRATCH_BYTES (16u << 20)
+gca_status gca_forward_noalloc(const gca_problem* p, const void* lmk_q, const void* lmk_k,
+                               const void* q, const void* k, const void* v, void* out,
+                               int32_t* idx, float* sel, float* lse, float* w,
+                               hipStream_t stream);
+
 /* Profiling aid (outside the method).  While armed, the i-th kernel that libgca
  * launches from the calling thread (i = 0, 1, ... while 2 (i + 1) <= capacity,
  * capacity <= 4096) is dispatched with events[2 i] and events[2 i + 1] as its

@@ -37,6 +37,8 @@ gca_status from_hip(hipError_t e, const char* what) {
 
 constexpr int64_t kMaxGrid = 2147483647;  // largest 1-D grid we launch
 
+static_assert(GCA_NOALLOC_SCRATCH_BYTES == gca::kScratchBytes, "scratch size in the header and the library");
+
 // the layout the Python binding mirrors
 static_assert(sizeof(gca_problem) == 72 && offsetof(gca_problem, n_chunks) == 16 &&
                   offsetof(gca_problem, flags) == 56 && offsetof(gca_problem, gumbel_seed) == 64,
@@ -363,6 +365,27 @@ gca_status gca_forward(const gca_problem* p, const void* lmk_q, const void* lmk_
   GCA_TRY(device_view(p, k, "k"));
   GCA_TRY(device_view(p, v, "v"));
   return forward_dispatch(p, s, lmk_q, lmk_k, q, k, v, out, idx, sel, lse, w, workspace, stream);
+}
+
+gca_status gca_forward_noalloc(const gca_problem* p, const void* lmk_q, const void* lmk_k, const void* q,
+                               const void* k, const void* v, void* out, int32_t* idx, float* sel, float* lse,
+                               float* w, hipStream_t stream) {
+  gca::Shape s;
+  GCA_TRY(check_forward_args(p, s, lmk_q, lmk_k, q, k, v, out, idx, sel, lse, w));
+  const size_t need = forward_ws(p, s);
+  if (need > gca::kScratchBytes)
+    return fail(GCA_ERR_UNSUPPORTED, "gca_forward_noalloc: the problem needs " + std::to_string(need) +
+                                         " bytes of scratch, more than the " + std::to_string(gca::kScratchBytes) +
+                                         " bytes the library holds per device; use gca_forward with a workspace");
+  GCA_TRY(device_view(p, k, "k"));
+  GCA_TRY(device_view(p, v, "v"));
+  void* scratch = nullptr;
+  if (need > 0) {
+    hipError_t e = hipSuccess;
+    scratch = gca::scratch_ptr(&e);
+    if (!scratch) return from_hip(e != hipSuccess ? e : hipErrorInvalidSymbol, "gca_forward_noalloc (scratch address)");
+  }
+  return forward_dispatch(p, s, lmk_q, lmk_k, q, k, v, out, idx, sel, lse, w, scratch, stream);
 }
 
 }  // extern "C"

@@ -134,4 +134,9 @@ const char* launch_error_kernel();
 // by a stream synchronisation and an error check naming the kernel.
 bool debug_sync();
 
+// The allocation-free forward's device scratch array: this device's address of
+// it (looked up once per device), or null with the HIP error in *err.
+constexpr size_t kScratchBytes = size_t(16) << 20;
+void* scratch_ptr(hipError_t* err);
+
 }  // namespace gca

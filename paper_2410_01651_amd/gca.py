@@ -20,6 +20,7 @@ EXPORTS = (
     "gca_grouped_xattn_fwd",
     "gca_grouped_xattn_bwd",
     "gca_forward",
+    "gca_forward_noalloc",
     "gca_workspace_size",
     "gca_status_string",
     "gca_last_error",
@@ -33,6 +34,7 @@ GCA_FP32, GCA_BF16 = 0, 1
 GCA_CAUSAL, GCA_DECODE = 0, 1
 FLAG_FUSED_TOPK, FLAG_MATERIALIZE, FLAG_GUMBEL, FLAG_HOST_KV = 1, 2, 4, 8
 OP_FORWARD, OP_BACKWARD = 0, 1
+NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 class Problem(ctypes.Structure):
@@ -86,6 +88,7 @@ def lib():
             "gca_grouped_xattn_bwd": [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                       vp, ctypes.c_size_t, vp],
             "gca_forward": [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp],
+            "gca_forward_noalloc": [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -327,6 +330,21 @@ def forward(p: Problem, lmk_q, lmk_k, q, k, v, out=None, idx=None, sel=None, lse
         _ptr(sel, "sel", torch.float32, sh.rows), _ptr(lse, "lse", torch.float32, sh.lse),
         _ptr(w, "w", torch.float32, sh.rows), _ptr(ws, "workspace"), ctypes.c_size_t(nbytes),
         _stream(stream)))
+    return {"out": out, "idx": idx, "sel": sel, "lse": lse, "w": w}
+
+
+def forward_noalloc(p: Problem, lmk_q, lmk_k, q, k, v, out, idx, sel, lse=None, w=None, stream=None):
+    """gca_forward_noalloc: the whole forward path into caller-provided outputs,
+    with the library's own per-device scratch as workspace (nothing allocated)."""
+    torch = _torch()
+    sh, dt = shapes(p), _elem_dtype(p)
+    _check(lib().gca_forward_noalloc(
+        ctypes.byref(p), _ptr(lmk_q, "lmk_q", dt, sh.lmk_q), _ptr(lmk_k, "lmk_k", dt, sh.lmk_k),
+        _ptr(q, "q", dt, sh.q),
+        _ptr(k, "k", dt, sh.kv, _host_kv(p)), _ptr(v, "v", dt, sh.kv, _host_kv(p)),
+        _ptr(out, "out", dt, sh.q), _ptr(idx, "idx", torch.int32, sh.rows),
+        _ptr(sel, "sel", torch.float32, sh.rows), _ptr(lse, "lse", torch.float32, sh.lse),
+        _ptr(w, "w", torch.float32, sh.rows), _stream(stream)))
     return {"out": out, "idx": idx, "sel": sel, "lse": lse, "w": w}
 
 
