@@ -62,7 +62,7 @@ SelectPlan select_plan(const Shape& s) {
   SelectPlan p{};
   // landmark queries stay in registers (bf16 up to 512 columns, fp32 up to 256)
   // next to each lane's best-16 list at most
-  p.split = false && s.causal && s.topk <= 16 && (s.bf16 ? s.D <= 512 : s.D <= 256);
+  p.split = s.causal && s.topk <= 16 && (s.bf16 ? s.D <= 512 : s.D <= 256);
   p.blocks = (s.nQ + kSelRows - 1) / kSelRows;
   p.tiles = (s.nKV + kSelTile - 1) / kSelTile;
   p.tiles_per_part = 8;

@@ -56,7 +56,10 @@ def test_workspace_sizes(gca):
     p = gca.problem(2, 16, 1024, 8)                     # materialised scores
     assert gca.workspace_size(p, gca.OP_FORWARD) == r(4 * 2 * 1024 * 1024)
     big = gca.problem(1, 8, 16384, 8)                   # 1 GiB matrix -> single-pass select
-    assert gca.workspace_size(big, gca.OP_FORWARD) == 0
+    lists = gca.workspace_size(big, gca.OP_FORWARD)     # per-row best-k lists, no matrix
+    assert 0 < lists <= 16384 * 64 * 8 * 8
+    wide = gca.problem(1, 8, 16384, 8, D=1024)          # landmarks too wide for the split select
+    assert gca.workspace_size(wide, gca.OP_FORWARD) == 0
     forced = gca.problem(1, 8, 16384, 8, flags=gca.FLAG_MATERIALIZE)
     assert gca.workspace_size(forced, gca.OP_FORWARD) == r(4 * 16384 * 16384)
     dec = gca.problem(1, 8, 262144, 8, mode="decode")

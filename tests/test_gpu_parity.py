@@ -97,18 +97,33 @@ def test_topk_ties_to_lower_chunk(dev, dtype):
         np.testing.assert_array_equal(sel.cpu().numpy(), rs.astype(np.float32))
 
 
-@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_fused_select_equals_oracle(dev, dtype):
-    """The single-pass causal select (no score matrix) against the oracle and the
+FUSED = [
+    # split select (per-row lists of key-tile parts, then a merge)
+    ("planted_1m_bf16", "fp32", dict(H=2, n_chunks=300)),
+    ("planted_1m_bf16", "bf16", dict(H=2, n_chunks=300)),
+    ("planted_1m_bf16", "bf16", dict(H=8, n_chunks=700, topk=12)),        # width 512, best-16 lists, 3 row blocks
+    ("planted_1m_bf16", "bf16", dict(H=1, D=64, n_chunks=5000, topk=8)),  # 79 key tiles: 2 parts per class
+    ("train_16k_bf16", "fp32", dict(B=2, H=4, n_chunks=1100, topk=3)),    # fp32 at width 256
+    # one pass per 64-row block (outside the split form's register budget)
+    ("planted_1m_bf16", "bf16", dict(H=2, n_chunks=300, topk=20)),
+    ("planted_1m_bf16", "bf16", dict(H=16, n_chunks=200, topk=8)),        # width 1024
+    ("planted_1m_bf16", "fp32", dict(H=8, n_chunks=300, topk=8)),         # fp32 at width 512
+]
+
+
+@pytest.mark.parametrize("name,dtype,kw", FUSED)
+def test_fused_select_equals_oracle(dev, name, dtype, kw):
+    """The causal select without the score matrix against the oracle and the
     materialised path."""
     from paper_2410_01651_amd import gca
-    w, inp = _case("planted_1m_bf16", H=2, n_chunks=300, dtype=dtype)
+    w, inp = _case(name, dtype=dtype, **kw)
     t = upload(w, inp, dev)
     fa = gca.forward(problem_for(w, flags=gca.FLAG_FUSED_TOPK), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
     fb = gca.forward(problem_for(w, flags=gca.FLAG_MATERIALIZE), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
     assert np.array_equal(fa["idx"].cpu().numpy(), fb["idx"].cpu().numpy())
     ref = _check_forward(w, inp, fa)
-    assert list(ref["idx"][0, 0, -1]) == list(gi.plant_positions(w))
+    if w.planted:           # the planted chunks are the last row's best (with k >= 8 of them)
+        assert set(gi.plant_positions(w).tolist()) <= set(ref["idx"][0, 0, -1].tolist())
 
 
 SWEEP = [
@@ -336,6 +351,7 @@ GUMBEL = [
     ("train_16k_bf16", dict(B=2, H=2, n_chunks=70, topk=5, gumbel_seed=11), "materialize"),
     ("train_16k_bf16", dict(B=1, H=2, n_chunks=300, topk=8, gumbel_seed=12, dtype="fp32"), "fused"),
     ("planted_1m_bf16", dict(H=2, n_chunks=500, topk=8, gumbel_seed=13), "fused"),
+    ("planted_1m_bf16", dict(H=2, n_chunks=600, topk=12, gumbel_seed=17), "fused"),
     ("decode_16m_bf16", dict(H=2, n_chunks=3001, topk=8, gumbel_seed=14, device_kv=False), None),
     ("decode_16m_bf16", dict(H=1, D=64, n_chunks=40000, topk=4, gumbel_seed=15, device_kv=False), None),
     ("decode_16m_bf16", dict(H=8, n_chunks=2500, topk=8, gumbel_seed=16, device_kv=False), None),
