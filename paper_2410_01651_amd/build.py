@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(HERE, "libgca.so")
 OBJ_DIR = os.path.join(HERE, "_build")
 
-SOURCES = ["api.cpp", "plan.cpp", "noalloc.hip", "scores.hip", "xattn_fwd.hip", "xattn_decode.hip",
+SOURCES = ["api.cpp", "plan.cpp", "noalloc.hip", "scores.hip", "select.hip", "xattn_fwd.hip", "xattn_decode.hip",
            "xattn_bwd.hip"]
 # The attention kernels never rely on NaN semantics: without IEEE mode the
 # softmax max needs no operand canonicalisation, and MFMA accumulators in

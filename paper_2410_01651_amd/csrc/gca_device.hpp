@@ -146,6 +146,18 @@ struct Swz {
   __device__ static __forceinline__ int off(int r, int col) {
     return r * kD + (((col / kVec) ^ sw(r)) * kVec) + (col % kVec);
   }
+  // For tiles read only by 16-byte row fragments: a map that also keeps 16
+  // consecutive rows apart when the LDS serves 16 lanes (256 bytes) per cycle.
+  // bf16 rows are 128 bytes, so a 256-byte window holds two rows; the 8 rows of
+  // one parity among 16 consecutive ones must take 8 different chunks, and so
+  // must any 8 consecutive rows: chunk c ^ (r mod 8) ^ (5 if bit 3 of r).  fp32
+  // rows are 256 bytes: c ^ (r mod 16) already does both.
+  __device__ static __forceinline__ int sw16(int r) {
+    return kCPR == 8 ? ((r & 7) ^ ((r & 8) ? 5 : 0)) : (r & (kCPR - 1));
+  }
+  __device__ static __forceinline__ int off16(int r, int col) {
+    return r * kD + (((col / kVec) ^ sw16(r)) * kVec) + (col % kVec);
+  }
 };
 
 template <int N>
@@ -183,9 +195,12 @@ __device__ __forceinline__ uint32_t uniform_lds(const void* lds, uint32_t add = 
 // (the scalar-base form of the instruction), so issuing a tile costs one scalar
 // move and one vector-memory instruction per 16-byte chunk and no vector address
 // arithmetic.  `g` and `lds` must hold the same value in every lane.
-template <typename T, int NW>
+// ROWS: rows of the tile (64, or 32 for a half tile); SW16: lay the tile out by
+// Swz::off16 (tiles read by row fragments only) instead of Swz::off.
+template <typename T, int NW, int ROWS = kS, bool SW16 = false>
 struct TileCopy {
-  static constexpr int kVec = Swz<T>::kVec, kCPR = Swz<T>::kCPR, kN = kCPR / NW;
+  static constexpr int kVec = Swz<T>::kVec, kCPR = Swz<T>::kCPR, kN = kCPR * ROWS / (64 * NW);
+  static_assert(kN >= 1 && kN * 64 * NW == kCPR * ROWS, "the waves' 16-byte pieces cover the tile");
   uint32_t goff[kN];
   uint32_t lwave;  // this wave's first 1 KiB block of the tile in LDS (scalar)
 
@@ -196,7 +211,7 @@ struct TileCopy {
     for (int ii = 0; ii < kN; ++ii) {
       const int pch = (ii * NW + wave) * 64 + lane;
       const int r = pch / kCPR;
-      const int c = (pch % kCPR) ^ Swz<T>::sw(r);
+      const int c = (pch % kCPR) ^ (SW16 ? Swz<T>::sw16(r) : Swz<T>::sw(r));
       const int rs = r < rows ? r : rows - 1;
       goff[ii] = (uint32_t)((rs * row_stride + c * kVec) * sizeof(T));
     }
@@ -230,6 +245,16 @@ __device__ __forceinline__ f32x8 lds_frag(const float* tile, int r, int col) {
   f32x8 f;
   f.lo = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off(r, col));
   f.hi = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off(r, col + 4));
+  return f;
+}
+// ... from a tile laid out by Swz::off16
+__device__ __forceinline__ bf16x8 lds_frag16(const __bf16* tile, int r, int col) {
+  return *reinterpret_cast<const bf16x8*>(tile + Swz<__bf16>::off16(r, col));
+}
+__device__ __forceinline__ f32x8 lds_frag16(const float* tile, int r, int col) {
+  f32x8 f;
+  f.lo = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off16(r, col));
+  f.hi = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off16(r, col + 4));
   return f;
 }
 
@@ -527,6 +552,27 @@ __device__ __forceinline__ float key_score(uint64_t k) {
   return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
 }
 __device__ __forceinline__ int key_chunk(uint64_t k) { return (int)~(uint32_t)k; }
+
+// A lane's running best-KM list as packed candidate keys (pack_key), sorted
+// largest first; 0 marks an empty entry (below every real key).  One insert is
+// KM 64-bit compares against the old entries and a shift by selects.
+template <int KM>
+struct TopKeys {
+  uint64_t k[KM];
+
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int i = 0; i < KM; ++i) k[i] = 0;
+  }
+  __device__ __forceinline__ void insert(uint64_t x) {
+    bool b[KM];
+#pragma unroll
+    for (int i = 0; i < KM; ++i) b[i] = x > k[i];
+#pragma unroll
+    for (int i = KM - 1; i > 0; --i) k[i] = b[i - 1] ? k[i - 1] : (b[i] ? x : k[i]);
+    k[0] = b[0] ? x : k[0];
+  }
+};
 
 template <int CTRL>
 __device__ __forceinline__ uint64_t dpp64(uint64_t x) {

@@ -53,8 +53,8 @@ int* decode_list_chunks(const Shape& s, void* ws);
 // `tiles_per_part` tiles, and every (block, class, part) work item leaves the
 // best k of its candidates for each of its rows.  A row has at most `lists`
 // such lists (list number = class * parts_max + part).
-constexpr int kSelRows = 256;
-constexpr int kSelTile = 64;
+constexpr int kSelRows = 128;
+constexpr int kSelTile = 32;
 constexpr int kSelClasses = 8;
 struct SelectPlan {
   bool split;            // the split form applies (else one pass per row block, no workspace)
@@ -107,9 +107,13 @@ hipError_t launch_decode_scan(const Shape& s, const void* lmk_q, const void* lmk
 hipError_t launch_xattn_decode(const Shape& s, const float* list_s, const int* list_j, const void* q,
                                const void* k, const void* v, int32_t* idx, float* sel, void* out, float* lse,
                                float* w, const void* lmk_q, const void* lmk_k, hipStream_t stream);
-// Causal: scores and top-k without the score matrix (workspace: fused_workspace).
+// Causal: scores and top-k without the score matrix (workspace: fused_workspace),
+// split over key-tile parts when select_plan(s).split ...
 hipError_t launch_fused_select(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx,
                                float* sel, void* ws, hipStream_t stream);
+// ... else one pass per 64-row block (no workspace).
+hipError_t launch_fused_rowblocks(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx,
+                                  float* sel, hipStream_t stream);
 // Eq. 2-3 forward.
 hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const void* v,
                             const int32_t* idx, const float* sel, void* out, float* lse, float* w,

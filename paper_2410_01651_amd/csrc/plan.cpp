@@ -65,7 +65,7 @@ SelectPlan select_plan(const Shape& s) {
   p.split = s.causal && s.topk <= 16 && (s.bf16 ? s.D <= 512 : s.D <= 256);
   p.blocks = (s.nQ + kSelRows - 1) / kSelRows;
   p.tiles = (s.nKV + kSelTile - 1) / kSelTile;
-  p.tiles_per_part = 8;
+  p.tiles_per_part = 64;  // a power of two
   if (!p.split) return p;
   // the largest row block needs every key tile
   const int64_t per_class = (p.tiles + kSelClasses - 1) / kSelClasses;
@@ -91,7 +91,9 @@ size_t fused_workspace(const Shape& s) {
   const SelectPlan p = select_plan(s);
   if (!p.split) return 0;
   const size_t n = (size_t)s.B * s.Hr * s.nQ * p.lists * s.topk;
-  return align256(n * sizeof(float)) + align256(n * sizeof(int));
+  // the lists' scores and chunks, then one published threshold per row
+  return align256(n * sizeof(float)) + align256(n * sizeof(int)) +
+         align256(sizeof(uint32_t) * (size_t)s.B * s.Hr * s.nQ);
 }
 
 // --------------------------------------------------------- backward ----

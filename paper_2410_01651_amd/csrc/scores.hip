@@ -475,268 +475,6 @@ __global__ __launch_bounds__(256) void fused_select_kernel(const T* __restrict__
   }
 }
 
-// --------------------------------------- split causal select (no matrix) ----
-//
-// The work of a long causal selection is a triangle of (landmark row, key
-// chunk) pairs.  It is cut into work items: a block of kSelRows rows against a
-// part of the key tiles (kSelTile key chunks each) that the block reaches, the
-// tiles of one item all of one class (tile index mod 8, one class per XCD, so
-// that each XCD's L2 holds one eighth of the landmark keys).  Each item leaves
-// the best k of its candidates for every one of its rows in the workspace, and
-// a merge pass takes each row's best k over its lists: an exact top-k, since
-// any member of a row's top k is among the best k of its own item.
-//
-// An item is one workgroup of 8 waves; wave w owns 32 of the block's rows and
-// keeps their landmark queries in registers as MFMA B operands (queries are the
-// product's columns), so a lane holds, per 64-key tile, 32 candidate scores of
-// one row in registers and folds them into its own running best-k list; the
-// two lanes of a row share their lists' thresholds once per tile, so that a
-// candidate below the k-th best of either list is dropped with one compare.
-// Key tiles (64 keys x D columns) are staged in LDS by direct-to-LDS copies,
-// two tiles deep.
-
-template <typename T> struct SelMax;
-template <> struct SelMax<__bf16> { static constexpr int kCh = 8; };  // D <= 512 in registers
-template <> struct SelMax<float> { static constexpr int kCh = 4; };   // D <= 256
-constexpr int kSelThreads = 512;
-constexpr int kSelWaves = kSelThreads / 64;
-static_assert(kSelWaves * 32 == kSelRows, "one 32-row column block per wave");
-
-struct SelParams {
-  int64_t nQ, nKV, tiles, blocks, items_per_class, parts_max, lists;
-  int D, K, tpp;
-  float scale;
-  uint64_t seed;
-};
-
-// Key tiles row block r reaches (key chunks below its last row).
-__device__ __forceinline__ int64_t sel_block_tiles(const SelParams& p, int64_t r) {
-  const int64_t last = min((r + 1) * kSelRows - 1, p.nQ - 1);
-  if (last < 1) return 0;
-  return min((last - 1) / kSelTile + 1, p.tiles);
-}
-// Tiles of class x among the first nt; parts they form.
-__device__ __forceinline__ int64_t sel_class_tiles(int64_t nt, int x) {
-  return nt > x ? (nt - x + kSelClasses - 1) / kSelClasses : 0;
-}
-
-template <typename T, int KM, bool GUMBEL>
-__global__ __launch_bounds__(kSelThreads, 1) void select_part_kernel(const T* __restrict__ lq,
-                                                                     const T* __restrict__ lk,
-                                                                     float* __restrict__ ls, int* __restrict__ lj,
-                                                                     SelParams p) {
-  constexpr int TILE = kS * kD;
-  constexpr int NCH = SelMax<T>::kCh;
-  __shared__ __attribute__((aligned(16))) T stage[2 * NCH * TILE];
-
-  // block -> (retrieval slice, class, item); items of a class in order of
-  // descending row block, so the longest items start first
-  const int x = (int)(blockIdx.x % kSelClasses);
-  const int64_t rest = blockIdx.x / kSelClasses;
-  const int64_t bhr = rest / p.items_per_class;
-  int64_t it = rest % p.items_per_class;
-  int64_t r = p.blocks - 1, part = -1, ncls = 0;
-  for (; r >= 0; --r) {
-    ncls = sel_class_tiles(sel_block_tiles(p, r), x);
-    const int64_t np = (ncls + p.tpp - 1) / p.tpp;
-    if (it < np) {
-      part = it;
-      break;
-    }
-    it -= np;
-  }
-  if (part < 0) return;  // this class has fewer items
-  const int nu = (int)min<int64_t>(p.tpp, ncls - part * p.tpp);  // tiles of this item
-  auto tile_of = [&](int u) -> int64_t { return x + kSelClasses * (part * p.tpp + u); };
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5, l32 = lane & 31;
-  const int nch = p.D / kD;
-  const int64_t t0w = r * kSelRows + 32 * wave;  // this wave's first row
-  const int64_t t = t0w + l32;                   // this lane's row
-  const T* qrow = lq + (bhr * p.nQ + min(t, p.nQ - 1)) * p.D;
-  Frag<T> qf[NCH][4];
-#pragma unroll
-  for (int c = 0; c < NCH; ++c)
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-      if (c < nch) qf[c][kb] = load_frag(qrow + c * kD + 16 * kb + 8 * hh);
-
-  // copies: every wave copies its share of each 64 x 64 chunk of a tile; the
-  // last key tile may hold fewer than 64 keys (rows past it repeat the last)
-  const TileCopy<T, kSelWaves> cp_full(wave, lane, p.D, kS);
-  const int last_rows = (int)(p.nKV - (p.tiles - 1) * kSelTile);
-  const TileCopy<T, kSelWaves> cp_last(wave, lane, p.D, last_rows);
-  const T* kbase = lk + bhr * p.nKV * p.D;
-  auto issue = [&](int u) __device__ {
-    const int64_t j = tile_of(u);
-    const T* src = kbase + j * kSelTile * p.D;
-    T* dst = stage + (u & 1) * NCH * TILE;
-    const bool last = j == p.tiles - 1;
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      if (c < nch) {
-        if (last) cp_last.issue(src + c * kD, dst + c * TILE);
-        else cp_full.issue(src + c * kD, dst + c * TILE);
-      }
-    }
-  };
-
-  TopList<KM> L;
-  L.init();
-  issue(0);
-  for (int u = 0; u < nu; ++u) {
-    wait_vmem<0>();
-    block_barrier();  // tile u is in; every wave is done with the other slot
-    if (u + 1 < nu) issue(u + 1);
-    const int64_t j0 = tile_of(u) * kSelTile;  // first key chunk of the tile
-    // wave-uniform: some (row, key) pair of this wave's block is a candidate
-    if (j0 < t0w + 31 && t0w < p.nQ) {
-      const T* sK = stage + (u & 1) * NCH * TILE;
-      f32x16 a0 = zero16(), a1 = zero16();
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        if (c < nch) {
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb) {
-            mma32(a0, lds_frag(sK + c * TILE, l32, 16 * kb + 8 * hh), qf[c][kb]);
-            mma32(a1, lds_frag(sK + c * TILE, 32 + l32, 16 * kb + 8 * hh), qf[c][kb]);
-          }
-        }
-      }
-      // the row's threshold: the better k-th best of its two lanes' lists
-      uint32_t pa, pb;
-      pair32(__float_as_uint(L.s[KM - 1]), pa, pb);
-      const float ts = fmaxf(__uint_as_float(pa), __uint_as_float(pb));
-      // full tile: every key below every row of the wave (and inside the keys)
-      const bool full = j0 + kSelTile <= t0w && j0 + kSelTile <= p.nKV && t0w + 31 < p.nQ;
-      // accumulator register i holds key 8 (i / 4) + 4 hh + i % 4 of its 32-key half:
-      // four consecutive keys per group of four registers (one generator call
-      // gives their Gumbel noise)
-      auto fold4 = [&](const f32x16& a, int g, int key0) __device__ {
-        const int64_t jg = j0 + key0;
-        f32x4 nz = f32x4{0.f, 0.f, 0.f, 0.f};
-        if constexpr (GUMBEL) nz = gumbel_noise4(p.seed, (uint32_t)bhr, (uint32_t)t, (uint32_t)(jg >> 2));
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          const int64_t jc = jg + m;
-          const float v = a[4 * g + m] * p.scale + nz[m];
-          const bool ok = full || (jc < t && t < p.nQ);
-          if (ok && v >= fmaxf(ts, L.s[KM - 1])) L.insert(v, (int)jc);
-        }
-      };
-#pragma unroll
-      for (int g = 0; g < 4; ++g) fold4(a0, g, 8 * g + 4 * hh);
-#pragma unroll
-      for (int g = 0; g < 4; ++g) fold4(a1, g, 32 + 8 * g + 4 * hh);
-    }
-  }
-
-  // the row's best k: the partner lane's list entries inserted into this lane's
-  // (the two lanes hold disjoint keys, so the partner's entry is the one whose
-  // chunk differs from this lane's; equal chunks are both empty entries)
-  float ps[KM];
-  int pj[KM];
-#pragma unroll
-  for (int e = 0; e < KM; ++e) {
-    uint32_t sa, sb, ja, jb;
-    pair32(__float_as_uint(L.s[e]), sa, sb);
-    pair32((uint32_t)L.j[e], ja, jb);
-    const bool own_first = ja == (uint32_t)L.j[e];
-    ps[e] = __uint_as_float(own_first ? sb : sa);
-    pj[e] = (int)(own_first ? jb : ja);
-  }
-#pragma unroll
-  for (int e = 0; e < KM; ++e)
-    if (pj[e] != kNoChunk) L.insert(ps[e], pj[e]);
-  if (hh == 0 && t < p.nQ) {
-    const int64_t o = ((bhr * p.nQ + t) * p.lists + x * p.parts_max + part) * p.K;
-#pragma unroll
-    for (int e = 0; e < KM; ++e) {
-      if (e < p.K) {
-        const bool real = L.j[e] != kNoChunk;
-        ls[o + e] = real ? L.s[e] : -INFINITY;
-        lj[o + e] = real ? L.j[e] : -1;
-      }
-    }
-  }
-}
-
-// One wave per landmark row: the best k over the row's lists, written in
-// ascending chunk order (GUMBEL: the lists rank noisy scores; sel gets the
-// chosen chunks' raw scores, recomputed from the landmark rows).
-template <typename T, int KM, bool GUMBEL>
-__global__ __launch_bounds__(256) void select_merge_kernel(const float* __restrict__ ls, const int* __restrict__ lj,
-                                                           int32_t* __restrict__ idx, float* __restrict__ sel,
-                                                           const T* __restrict__ lq, const T* __restrict__ lk,
-                                                           int64_t rows, SelParams p) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const int64_t t = row % p.nQ, bhr = row / p.nQ;
-  const int64_t nt = sel_block_tiles(p, t / kSelRows);
-  TopList<KM> L;
-  L.init();
-  const int64_t base = row * p.lists * p.K;
-  // entry e of the row: class e / (parts_max K), part, rank
-  const int64_t per_class = p.parts_max * p.K;
-  for (int64_t e = lane; e < p.lists * p.K; e += 64) {
-    const int x = (int)(e / per_class);
-    const int64_t in_class = e % per_class;
-    const int64_t parts = (sel_class_tiles(nt, x) + p.tpp - 1) / p.tpp;
-    if (in_class / p.K < parts) {
-      const int jj = lj[base + e];
-      if (jj >= 0) L.insert(ls[base + e], jj);
-    }
-  }
-  float ms;
-  int mj, cnt;
-  wave_merge(L, p.K, ms, mj, cnt);
-  if constexpr (GUMBEL) {
-    if (lane < cnt) ms = p.scale * dot_rows(lq + (bhr * p.nQ + t) * p.D, lk + (bhr * p.nKV + mj) * p.D, p.D);
-  }
-  const int rank = rank_by_chunk(mj, cnt);
-  int32_t* io = idx + row * p.K;
-  float* so = sel + row * p.K;
-  if (lane < cnt) {
-    io[rank] = mj;
-    so[rank] = ms;
-  } else if (lane < p.K) {
-    io[lane] = -1;
-    so[lane] = -INFINITY;
-  }
-}
-
-template <typename T, int KM, bool GUMBEL>
-hipError_t launch_split_select(const Shape& s, const void* lq, const void* lk, int32_t* idx, float* sel, void* ws,
-                               hipStream_t st) {
-  const SelectPlan plan = select_plan(s);
-  SelParams p;
-  p.nQ = s.nQ;
-  p.nKV = s.nKV;
-  p.tiles = plan.tiles;
-  p.blocks = plan.blocks;
-  p.items_per_class = plan.items_per_class;
-  p.parts_max = plan.parts_max;
-  p.lists = plan.lists;
-  p.D = s.D;
-  p.K = s.topk;
-  p.tpp = plan.tiles_per_part;
-  p.scale = s.score_scale;
-  p.seed = s.gumbel_seed;
-  const int64_t BHr = (int64_t)s.B * s.Hr;
-  const size_t n = (size_t)BHr * s.nQ * plan.lists * s.topk;
-  float* ls = reinterpret_cast<float*>(ws);
-  int* lj = reinterpret_cast<int*>(reinterpret_cast<char*>(ws) + align256(n * sizeof(float)));
-  const int64_t items = BHr * kSelClasses * plan.items_per_class;
-  if (items > 0)
-    launch_kernel("select_part_kernel", select_part_kernel<T, KM, GUMBEL>, dim3((unsigned)items),
-                  dim3(kSelThreads), 0, st, (const T*)lq, (const T*)lk, ls, lj, p);
-  const int64_t rows = BHr * s.nQ;
-  launch_kernel("select_merge_kernel", select_merge_kernel<T, KM, GUMBEL>, dim3((unsigned)((rows + 3) / 4)),
-                dim3(256), 0, st, ls, lj, idx, sel, (const T*)lq, (const T*)lk, rows, p);
-  return take_launch_error();
-}
-
 template <typename T, int KM, bool GUMBEL>
 hipError_t launch_fused_k(const Shape& s, const void* lq, const void* lk, int32_t* idx, float* sel,
                           hipStream_t st) {
@@ -826,16 +564,11 @@ hipError_t launch_decode_scan(const Shape& s, const void* lmk_q, const void* lmk
   return s.gumbel ? run(float{}, std::true_type{}) : run(float{}, std::false_type{});
 }
 
-hipError_t launch_fused_select(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx, float* sel,
-                               void* ws, hipStream_t stream) {
-  const bool split = select_plan(s).split;
+hipError_t launch_fused_rowblocks(const Shape& s, const void* lmk_q, const void* lmk_k, int32_t* idx, float* sel,
+                                  hipStream_t stream) {
   auto run = [&](auto tag, auto gumbel) {
     using T = decltype(tag);
     constexpr bool G = decltype(gumbel)::value;
-    if (split) {
-      if (s.topk <= 8) return launch_split_select<T, 8, G>(s, lmk_q, lmk_k, idx, sel, ws, stream);
-      return launch_split_select<T, 16, G>(s, lmk_q, lmk_k, idx, sel, ws, stream);
-    }
     if (s.topk <= 8) return launch_fused_k<T, 8, G>(s, lmk_q, lmk_k, idx, sel, stream);
     if (s.topk <= 16) return launch_fused_k<T, 16, G>(s, lmk_q, lmk_k, idx, sel, stream);
     return launch_fused_k<T, 32, G>(s, lmk_q, lmk_k, idx, sel, stream);
