@@ -13,17 +13,24 @@ Prints ONE JSON line.  Besides the headline tokens/s it carries:
                  the stream) gives ms_per_step; the same K steps are then run
                  again with every kernel dispatched with its own start and stop
                  events (the kernel alone, on its stream), which give each
-                 kernel's average duration;
+                 kernel's average duration; traffic and matrix-core busy
+                 fraction come from the committed rocprofv3 counter summaries
+                 when they were taken from the current kernel sources;
   cpu_baseline - the CPU oracle timed on a bounded sample of the same workload;
+  forward_16k  - the forward of the 16K training workload (B=8, H=12), tokens/s;
+  planted_1m   - the forward of the 1M-token planted workload, tokens/s, with the
+                 selection's matrix-core rate;
   decode_scan  - the 16M-context decode retrieval (one 64-token chunk scored
                  against 262,144 past landmark keys, top-8, attention over the
-                 8 gathered chunks) in GB/s against HBM peak.
+                 8 gathered chunks) in GB/s against HBM peak;
+  peaks_measured - on-device streaming-read and matrix-core loop rates (the
+                 spec peaks stay the roofline reference).
+Every leg with an oracle baseline reports it in the leg's own unit.
 """
 
 import argparse
 import ctypes
 import json
-import math
 import os
 import sys
 import time
@@ -35,6 +42,10 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 S, DH = 64, 64
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 # ------------------------------------------------------------ HIP events ----
@@ -107,6 +118,11 @@ def kernel_times(run_step, steps, stream, gca, per_step_capacity=32):
     return total, per
 
 
+def kernel_table(per, steps):
+    return {k: {"avg_ms": sum(v) / len(v), "launches_per_step": len(v) / steps, "ms_per_step": sum(v) / steps}
+            for k, v in per.items()}
+
+
 # ------------------------------------------------------------ workloads ----
 
 def upload(w, a, dev):
@@ -127,29 +143,40 @@ def landmarks(w):
 
 def valid_units(idx_host, w):
     """Valid (batch, head, query chunk, slot) tuples the attention kernels process."""
-    import numpy as np
     valid = (idx_host >= 0)
     if w.mode == "causal":
         per_row = valid[:, :, :-1, :].sum()      # row t feeds chunk t+1
     else:
         per_row = valid.sum()
-    heads_per_rhead = w.H // w.Hr
-    return int(per_row) * heads_per_rhead
+    return int(per_row) * (w.H // w.Hr)
+
+
+def _profile_entry(path, kernel):
+    """Entry `kernel` of a committed rocprofv3 summary, or None when there is none or
+    the kernel sources changed since it was taken."""
+    try:
+        from profiling import source_hash
+        data = json.load(open(os.path.join(ROOT, "profiles", path)))
+        if data.get("source_sha256") != source_hash():
+            return None
+        return data["kernels"][kernel]
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def measured_traffic(kernel):
-    """HBM bytes per launch (fetch + write) for `kernel` from the committed rocprofv3
-    counter summary, or None when there is none or the kernels changed since."""
-    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-    try:
-        from profiling import source_hash
-        data = json.load(open(path))
-        if data.get("source_sha256") != source_hash():
-            return None
-        k = data["kernels"][kernel]
-        return k["fetch_bytes_per_launch"] + k["write_bytes_per_launch"]
-    except (OSError, KeyError, ValueError):
+    """HBM bytes per launch (fetch + write) from the committed counter summary."""
+    k = _profile_entry("hbm_traffic.json", kernel)
+    return None if k is None else k["fetch_bytes_per_launch"] + k["write_bytes_per_launch"]
+
+
+def measured_mfma(kernel):
+    """Matrix-core busy fraction and bf16 matrix-core ops per launch from the
+    committed counter summary."""
+    k = _profile_entry("mfma_counters.json", kernel)
+    if k is None:
         return None
+    return {key: k.get(key) for key in ("mfma_busy_frac", "mfma_bf16_flops_per_launch", "l2_hit_frac")}
 
 
 def flops_per_unit():
@@ -159,8 +186,29 @@ def flops_per_unit():
             "bwd_dkdv_kernel": 2 * (2 * S * DH)}      # dV = P^T dO, dK = dS^T Q (its own S/dP recompute not counted)
 
 
+def mfma_roofline(kern, units, dom):
+    fpu = flops_per_unit()
+    fl = units * S * fpu[dom]
+    ach = fl / (kern[dom]["avg_ms"] * 1e-3) / 1e12
+    return {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": ach / BF16_PEAK_TFLOPS, "traffic": measured_traffic(dom), "counters": measured_mfma(dom),
+            "algorithmic_flops_per_launch": fl, "avg_launch_ms": kern[dom]["avg_ms"]}
+
+
+def forward_outputs(p, gca, dev):
+    import torch
+    sh = gca.shapes(p)
+    dt = torch.bfloat16 if p.dtype == gca.GCA_BF16 else torch.float32
+    return {"out": torch.empty(sh.q, dtype=dt, device=dev),
+            "idx": torch.empty(sh.rows, dtype=torch.int32, device=dev),
+            "sel": torch.empty(sh.rows, dtype=torch.float32, device=dev),
+            "lse": torch.empty(sh.lse, dtype=torch.float32, device=dev),
+            "w": torch.empty(sh.rows, dtype=torch.float32, device=dev)}
+
+
+# ------------------------------------------------------ 64K fwd + bwd ----
+
 def bench_train(args, dev, gca):
-    import numpy as np
     import torch
     from gen import get_workload, inputs as gi
 
@@ -170,11 +218,7 @@ def bench_train(args, dev, gca):
     t.update(gi.device_tensors(w, ("q", "k", "v", "dout"), dev))
     p = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode)
     sh = gca.shapes(p)
-    fo = {"out": torch.empty(sh.q, dtype=torch.bfloat16, device=dev),
-          "idx": torch.empty(sh.rows, dtype=torch.int32, device=dev),
-          "sel": torch.empty(sh.rows, dtype=torch.float32, device=dev),
-          "lse": torch.empty(sh.lse, dtype=torch.float32, device=dev),
-          "w": torch.empty(sh.rows, dtype=torch.float32, device=dev)}
+    fo = forward_outputs(p, gca, dev)
     grads = {"dq": torch.empty(sh.q, dtype=torch.bfloat16, device=dev),
              "dk": torch.empty(sh.kv, dtype=torch.bfloat16, device=dev),
              "dv": torch.empty(sh.kv, dtype=torch.bfloat16, device=dev),
@@ -185,8 +229,7 @@ def bench_train(args, dev, gca):
     wsb, _ = gca.workspace(p, gca.OP_BACKWARD, dev)
 
     def step(pp=p):
-        gca.forward(pp, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"], out=fo["out"], idx=fo["idx"],
-                    sel=fo["sel"], lse=fo["lse"], w=fo["w"], ws=wsf)
+        gca.forward(pp, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"], ws=wsf, **fo)
         gca.grouped_xattn_bwd(pp, t["q"], t["k"], t["v"], fo["idx"], fo["sel"], fo["lse"], t["dout"],
                               t["lmk_q"], t["lmk_k"], ws=wsb, grads=grads)
 
@@ -194,18 +237,16 @@ def bench_train(args, dev, gca):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+    log(f"warmup done ({args.warmup} steps)")
 
     # timed region: K steps bracketed by synchronisation, nothing else on the stream
     t0 = time.perf_counter()
     ms_step = timed(step, args.steps, stream) / args.steps
     wall = time.perf_counter() - t0
-    tokens = w.B * w.Lq
-    print(f"[bench] timed {args.steps} steps: {ms_step:.3f} ms/step (wall {wall:.2f}s)", file=sys.stderr,
-          flush=True)
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step (wall {wall:.2f}s)")
     # the same K steps again with every kernel's dispatch carrying start/stop events
     prof_ms, per = kernel_times(step, args.steps, stream, gca)
-    print(f"[bench] profiled {args.steps} steps: {prof_ms / args.steps:.3f} ms/step", file=sys.stderr, flush=True)
+    log(f"profiled {args.steps} steps: {prof_ms / args.steps:.3f} ms/step")
     idx_host = fo["idx"].cpu().numpy()
     # the Gumbel top-k variant of the same step (noise in the selection only)
     pg = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, gumbel_seed=1)
@@ -215,48 +256,290 @@ def bench_train(args, dev, gca):
     gumbel = {"value": w.B * w.Lq / (g_ms * 1e-3), "unit": "tokens/s", "ms_per_step": g_ms,
               "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()
                           if k in ("chunk_scores_kernel", "topk_kernel")}}
-    print(f"[bench] gumbel top-k {args.steps} steps: {g_ms:.3f} ms/step", file=sys.stderr, flush=True)
+    log(f"gumbel top-k {args.steps} steps: {g_ms:.3f} ms/step")
 
     units = valid_units(idx_host, w)
-    fpu = flops_per_unit()
-    kern = {}
-    for name, ds in per.items():
-        avg = sum(ds) / len(ds)
-        kern[name] = {"avg_ms": avg, "launches_per_step": len(ds) / args.steps,
-                      "ms_per_step": sum(ds) / args.steps}
-        if name in fpu:
-            fl = units * S * fpu[name]
-            kern[name]["tflops"] = fl / (avg * 1e-3) / 1e12
+    kern = kernel_table(per, args.steps)
+    for name in flops_per_unit():
+        if name in kern:
+            kern[name]["tflops"] = mfma_roofline(kern, units, name)["achieved"]
     dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
-    if dom in fpu:
-        ach = kern[dom]["tflops"]
-        roof = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": ach / BF16_PEAK_TFLOPS, "traffic": measured_traffic(dom),
-                "algorithmic_flops_per_launch": units * S * fpu[dom], "avg_launch_ms": kern[dom]["avg_ms"]}
-    else:
-        roof = {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
-                "traffic": None}
-    algo_fl = units * S * (fpu["xattn_fwd_kernel"] + 5 * 2 * S * DH)
+    roof = mfma_roofline(kern, units, dom) if dom in flops_per_unit() else \
+        {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None}
+    algo_fl = units * S * (flops_per_unit()["xattn_fwd_kernel"] + 5 * 2 * S * DH)
     return {
-        "w": w, "t": t, "tokens": tokens, "ms_step": ms_step, "profiled_ms_step": prof_ms / args.steps,
-        "gumbel": gumbel,
-        "kernels": kern, "roofline": roof,
-        "units": units, "path_tflops": algo_fl / (ms_step * 1e-3) / 1e12,
+        "w": w, "t": t, "tokens": w.B * w.Lq, "ms_step": ms_step, "profiled_ms_step": prof_ms / args.steps,
+        "gumbel": gumbel, "kernels": kern, "roofline": roof, "units": units,
+        "path_tflops": algo_fl / (ms_step * 1e-3) / 1e12,
     }
+
+
+# ---------------------------------------------- forward-only workloads ----
+
+def bench_forward(args, dev, gca, name):
+    """Forward tokens/s of a causal workload (train_16k_bf16 or planted_1m_bf16)."""
+    import torch
+    from gen import get_workload, inputs as gi
+
+    w = get_workload(name)
+    lq, lk = landmarks(w)
+    t = {"lmk_q": upload(w, lq, dev), "lmk_k": upload(w, lk, dev)}
+    t.update(gi.device_tensors(w, ("q", "k", "v"), dev))
+    p = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode)
+    fo = forward_outputs(p, gca, dev)
+    ws, _ = gca.workspace(p, gca.OP_FORWARD, dev)
+
+    def call():
+        gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"], ws=ws, **fo)
+
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        call()
+    steps = args.fwd_steps
+    ms = timed(call, steps, stream) / steps
+    _, per = kernel_times(call, steps, stream, gca)
+    kern = kernel_table(per, steps)
+    idx_host = fo["idx"].cpu().numpy()
+    units = valid_units(idx_host, w)
+    kern["xattn_fwd_kernel"]["tflops"] = mfma_roofline(kern, units, "xattn_fwd_kernel")["achieved"]
+    leg = {"metric": "GCA forward tokens/s", "value": w.B * w.Lq / (ms * 1e-3), "unit": "tokens/s",
+           "ms_per_call": ms, "calls": steps, "kernels": kern,
+           "roofline": mfma_roofline(kern, units, "xattn_fwd_kernel")}
+    # the selection's matrix-core rate: 2 D flops per causal (row, earlier chunk) pair
+    pairs = w.B * w.Hr * w.n_chunks * (w.n_chunks - 1) // 2
+    sel_kernel = "select_part_kernel" if "select_part_kernel" in kern else \
+        "fused_select_kernel" if "fused_select_kernel" in kern else "chunk_scores_kernel"
+    sfl = 2 * w.Dl * pairs
+    sach = sfl / (kern[sel_kernel]["avg_ms"] * 1e-3) / 1e12
+    leg["selection"] = {"kernel": sel_kernel, "bound": "mfma", "achieved": sach, "peak": BF16_PEAK_TFLOPS,
+                        "unit": "TFLOP/s", "frac": sach / BF16_PEAK_TFLOPS, "algorithmic_flops_per_launch": sfl,
+                        "avg_launch_ms": kern[sel_kernel]["avg_ms"], "traffic": measured_traffic(sel_kernel),
+                        "counters": measured_mfma(sel_kernel)}
+    if w.planted:
+        pos = gi.plant_positions(w)
+        leg["planted_retrieved"] = sorted(idx_host[0, 0, -1].tolist()) == sorted(pos.tolist())
+    log(f"{name} forward: {ms:.3f} ms/call")
+    host = None
+    if not args.no_cpu_baseline:
+        host = {"lq": lq, "lk": lk, "q": t["q"][:1, :1].cpu(), "k": t["k"][:1, :1].cpu(),
+                "v": t["v"][:1, :1].cpu()}
+    del t, fo, ws
+    torch.cuda.empty_cache()
+    return w, leg, host
+
+
+def cpu_forward_baseline(w, host, rows=None, chunks=None):
+    """The oracle's forward on a bounded sample: scores and top-k for `rows` landmark
+    rows of batch 0 and attention of head 0 over `chunks` query chunks, each
+    extrapolated to the whole workload (selection by causal candidate pairs,
+    attention by (batch, head, chunk))."""
+    import numpy as np
+    from gen import inputs as gi
+    from oracle import gca as og
+    nQ = w.n_chunks
+    rows = np.arange(nQ) if rows is None else np.asarray(rows)
+    chunks = range(nQ) if chunks is None else chunks
+    lq = gi.decode(w, host["lq"][:1, :1])
+    lk = gi.decode(w, host["lk"][:1, :1])
+    t0 = time.perf_counter()
+    r = og.scores(lq, lk, w.score_scale, w.mode, rows=rows)
+    idx_s, sel_s = og.topk(r, w.topk, rows=rows)
+    t_sel = time.perf_counter() - t0
+    # the attention sample needs the full row set of its chunks' retrieval rows
+    need = sorted({c - 1 for c in chunks if c >= 1})
+    r2 = og.scores(lq, lk, w.score_scale, w.mode, rows=need)
+    i2, s2 = og.topk(r2, w.topk, rows=need)
+    idx = np.full((1, 1, nQ, w.topk), -1, np.int32)
+    sel = np.full((1, 1, nQ, w.topk), -np.inf)
+    idx[0, 0, need], sel[0, 0, need] = i2[0, 0], s2[0, 0]
+    wt = og.fusion_weights(sel)
+    host64 = lambda x: x.float().double().numpy()
+    q, k, v = host64(host["q"]), host64(host["k"]), host64(host["v"])
+    t1 = time.perf_counter()
+    og.xattn_fwd(q, k, v, idx, wt, w.S, w.attn_scale, w.mode, chunks=chunks)
+    t_att = time.perf_counter() - t1
+    pairs_sample = int(sum(min(int(t), nQ) for t in rows))
+    pairs_all = w.B * w.Hr * nQ * (nQ - 1) // 2
+    full = t_sel * pairs_all / max(pairs_sample, 1) + t_att * (w.B * w.H * nQ) / len(list(chunks))
+    return {"value": w.B * w.Lq / full, "unit": "tokens/s", "kind": "oracle",
+            "sample": f"batch 0, retrieval head 0: scores + top-k for {len(rows)} landmark rows ({t_sel:.2f}s), "
+                      f"attention of head 0 over {len(list(chunks))} query chunks ({t_att:.2f}s); extrapolated "
+                      f"by candidate pairs and by (batch, head, chunk) to B={w.B}, H={w.H}, {nQ} chunks",
+            "sample_seconds": t_sel + t_att, **host_info()}
+
+
+# -------------------------------------------------------- 16M decode ----
+
+def bench_decode(args, dev, gca):
+    """16M-context decode retrieval: GB/s of algorithmic bytes against HBM peak."""
+    import torch
+    from gen import get_workload, inputs as gi
+
+    w = get_workload("decode_16m_bf16")
+    lq, lk = landmarks(w)
+    lmk_q = upload(w, lq, dev)
+    keys = [upload(w, lk, dev)]
+    keys.append(keys[0].clone())                   # 2 x 268 MB: rotation defeats the 256 MB MALL
+    kv = gi.device_kv(w, dev)
+    q = gi.device_tensors(w, ("q",), dev)["q"]
+    p = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode)
+    fo = forward_outputs(p, gca, dev)
+    ws, _ = gca.workspace(p, gca.OP_FORWARD, dev)
+    it = [0]
+
+    def call(pp=p):
+        gca.forward(pp, lmk_q, keys[it[0] % 2], q, kv["k"], kv["v"], ws=ws, **fo)
+        it[0] += 1
+
+    for _ in range(5):
+        call()
+    torch.cuda.synchronize()
+    steps = args.decode_steps
+    stream = torch.cuda.current_stream()
+    ms_call = timed(call, steps, stream) / steps
+    prof_ms, per = kernel_times(call, steps, stream, gca)
+    planted = int(gi.plant_positions(w)[0])
+    idx_host = fo["idx"].cpu().numpy()
+    found = planted in idx_host.ravel().tolist()
+    # the Gumbel top-k variant of the same call
+    pg = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, gumbel_seed=1)
+    call(pg)
+    g_ms = timed(lambda: call(pg), steps, stream) / steps
+    _, g_per = kernel_times(lambda: call(pg), steps, stream, gca)
+    key_bytes = w.n_chunks * w.Dl * 2
+    kv_bytes = 2 * w.topk * w.H * S * DH * 2
+    io_bytes = 2 * w.H * S * DH * 2 + w.Dl * 2
+    total_bytes = key_bytes + kv_bytes + io_bytes
+    scan_ms = sum(per["decode_scan_kernel"]) / len(per["decode_scan_kernel"])
+    scan_gbs = key_bytes / (scan_ms * 1e-3) / 1e9
+    host = None
+    if not args.no_cpu_baseline:
+        # what the oracle needs for the same call: the landmarks and the K/V of
+        # the chunks it retrieves (the rest of the cache is never read)
+        sel_chunks = sorted(set(int(j) for j in idx_host.ravel() if j >= 0))
+        host = {"lq": lq, "lk": lk, "q": q.cpu(), "chunks": sel_chunks,
+                "k": {j: kv["k"][:, :, j * S:(j + 1) * S].cpu() for j in sel_chunks},
+                "v": {j: kv["v"][:, :, j * S:(j + 1) * S].cpu() for j in sel_chunks}}
+    del kv, keys
+    torch.cuda.empty_cache()
+    leg = {
+        "metric": "retrieval-scan GB/s at 16M-ctx decode", "unit": "GB/s",
+        "value": total_bytes / (ms_call * 1e-3) / 1e9, "ms_per_call": ms_call, "calls": steps,
+        "profiled_ms_per_call": prof_ms / steps,
+        "bytes_per_call": total_bytes, "frac_of_hbm_peak": total_bytes / (ms_call * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "planted_retrieved": found,
+        "config": {"workload": "decode_16m_bf16: B=1 H=8 d=64, 16,777,216 past tokens (262,144 chunks), "
+                               "S=64, top-8, D=512, bf16"},
+        "roofline": {"kernel": "decode_scan_kernel", "bound": "hbm", "achieved": scan_gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": scan_gbs / HBM_PEAK_GBS,
+                     "traffic": measured_traffic("decode_scan_kernel@decode_16m"),
+                     "algorithmic_bytes_per_launch": key_bytes, "avg_launch_ms": scan_ms},
+        "kernels": kernel_table(per, steps),
+        "gumbel_topk": {"value": total_bytes / (g_ms * 1e-3) / 1e9, "unit": "GB/s", "ms_per_call": g_ms,
+                        "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()}},
+    }
+    return w, leg, host, total_bytes
+
+
+def cpu_decode_baseline(w, host, total_bytes):
+    """The oracle's whole decode call: scores of the one landmark query against all
+    262,144 past keys, top-k, weights, and the attention of all 8 heads over the
+    retrieved chunks (the oracle reads only those chunks' K/V)."""
+    import numpy as np
+    from gen import inputs as gi
+    from oracle import gca as og
+    t0 = time.perf_counter()
+    lq = gi.decode(w, host["lq"])
+    lk = gi.decode(w, host["lk"])
+    r = og.scores(lq, lk, w.score_scale, w.mode)
+    idx, sel = og.topk(r, w.topk)
+    wt = og.fusion_weights(sel)
+    js = [int(j) for j in idx[0, 0, 0] if j >= 0]
+    host64 = lambda x: x.float().double().numpy()
+    k = np.concatenate([host64(host["k"][j]) for j in js], axis=2)
+    v = np.concatenate([host64(host["v"][j]) for j in js], axis=2)
+    loc = np.full_like(idx, -1)
+    loc[0, 0, 0, :len(js)] = np.arange(len(js))      # the gathered chunks, in retrieval order
+    og.xattn_fwd(host64(host["q"]), k, v, loc, wt, w.S, w.attn_scale, mode="decode")
+    sec = time.perf_counter() - t0
+    return {"value": total_bytes / sec / 1e9, "unit": "GB/s", "kind": "oracle",
+            "sample": "the whole decode call (bf16 landmark keys widened to fp64 included)",
+            "sample_seconds": sec, "retrieved_same_set": sorted(js) == host["chunks"], **host_info()}
+
+
+def bench_decode_host_kv(args, dev, gca):
+    """Decode with the past chunks' K/V offloaded to pinned host memory (landmarks,
+    q and outputs in HBM): the decode attention gathers the k retrieved chunks over
+    the host link.  1M past tokens (16,384 chunks, 2 x 1.07 GB of host K/V)."""
+    import torch
+    from gen import get_workload, inputs as gi
+
+    w = get_workload("decode_16m_bf16", n_chunks=16384)
+    lq, lk = landmarks(w)
+    lmk_q, lmk_k = upload(w, lq, dev), upload(w, lk, dev)
+    kv = gi.device_kv(w, dev)
+    host = {n: torch.empty(kv[n].shape, dtype=kv[n].dtype, pin_memory=True) for n in ("k", "v")}
+    for n in ("k", "v"):
+        host[n].copy_(kv[n])
+    q = gi.device_tensors(w, ("q",), dev)["q"]
+    stream = torch.cuda.current_stream()
+    res = {}
+    for where, flags, k, v in (("device", 0, kv["k"], kv["v"]), ("host", gca.FLAG_HOST_KV, host["k"], host["v"])):
+        p = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, flags=flags)
+        fo = forward_outputs(p, gca, dev)
+        ws, _ = gca.workspace(p, gca.OP_FORWARD, dev)
+
+        def call():
+            gca.forward(p, lmk_q, lmk_k, q, k, v, ws=ws, **fo)
+
+        for _ in range(5):
+            call()
+        ms = timed(call, args.decode_steps, stream) / args.decode_steps
+        _, per = kernel_times(call, args.decode_steps, stream, gca)
+        res[where] = {"ms_per_call": ms, "kernels": {n: {"avg_ms": sum(d) / len(d)} for n, d in per.items()}}
+    gathered = 2 * w.topk * w.H * S * DH * 2      # K and V tiles of the retrieved chunks, every head
+    att_host = res["host"]["kernels"]["xattn_decode_kernel"]["avg_ms"]
+    att_dev = res["device"]["kernels"]["xattn_decode_kernel"]["avg_ms"]
+    del kv, host
+    torch.cuda.empty_cache()
+    return {"config": {"workload": "decode with host-resident K/V: B=1 H=8 d=64, 1,048,576 past tokens "
+                                   "(16,384 chunks), S=64, top-8, D=512, bf16; K/V in pinned host memory"},
+            "ms_per_call": res["host"]["ms_per_call"], "ms_per_call_device_kv": res["device"]["ms_per_call"],
+            "host_link_bytes_per_call": gathered,
+            "host_link_GBps": gathered / ((att_host - att_dev) * 1e-3) / 1e9 if att_host > att_dev else None,
+            "kernels": res["host"]["kernels"], "kernels_device_kv": res["device"]["kernels"]}
+
+
+# ------------------------------------------------------- CPU baselines ----
+
+def host_info():
+    """Threads the oracle's numpy backend uses, the CPU model and the BLAS library."""
+    info = {"cores": 1, "cpu_model": None, "blas": None}
+    try:
+        from threadpoolctl import threadpool_info
+        pools = threadpool_info()
+        info["cores"] = max([i.get("num_threads", 1) for i in pools] or [1])
+        blas = [i for i in pools if i.get("user_api") == "blas"]
+        if blas:
+            info["blas"] = f"{blas[0].get('internal_api')} {blas[0].get('version')}"
+    except Exception:
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    info["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return info
 
 
 def cpu_baseline(w, t, heads=16):
     """The oracle (as it stands) on a bounded sample: batch 0's scores and top-k over
     all 1,024 landmark rows, then attention forward and backward for `heads` heads of
     batch 0 over every chunk.  Extrapolated to the whole batch in tokens/s."""
-    import numpy as np
-    from gen import inputs as gi
     from oracle import gca as og
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        cores = 1
 
     def host(x):
         return x.float().cpu().double().numpy()
@@ -277,143 +560,78 @@ def cpu_baseline(w, t, heads=16):
     og.xattn_bwd(q, k, v, idx, wt, do, w.S, w.attn_scale, w.mode)
     t_attn = time.perf_counter() - t1
     full = w.B * t_sel + (w.B * w.H / heads) * t_attn
-    return {"value": w.B * w.Lq / full, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+    return {"value": w.B * w.Lq / full, "unit": "tokens/s", "kind": "oracle",
             "sample": f"batch 0: scores+top-k over all {w.n_chunks} landmark rows ({t_sel:.2f}s), then "
                       f"attention fwd+bwd for {heads} of {w.H} heads over all chunks ({t_attn:.2f}s); "
                       f"extrapolated to B={w.B}, H={w.H}",
-            "sample_seconds": t_sel + t_attn}
+            "sample_seconds": t_sel + t_attn, **host_info()}
 
 
-def bench_decode(args, dev, gca):
-    """16M-context decode retrieval: GB/s of algorithmic bytes against HBM peak."""
-    import numpy as np
+# --------------------------------------------------------------- peaks ----
+
+def measured_peaks(dev):
+    """On-device reference rates: a streaming read of 4 GiB (the HBM rate a plain
+    coalesced read reaches) and a register-resident bf16 32x32x16 product loop (the
+    matrix-core rate at the running clock)."""
     import torch
-    from gen import get_workload, inputs as gi
-
-    w = get_workload("decode_16m_bf16")
-    lq, lk = landmarks(w)
-    lmk_q = upload(w, lq, dev)
-    keys = [upload(w, lk, dev)]
-    keys.append(keys[0].clone())                   # 2 x 268 MB: rotation defeats the 256 MB MALL
-    kv = gi.device_kv(w, dev)
-    q = gi.device_tensors(w, ("q",), dev)["q"]
-    p = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode)
-    sh = gca.shapes(p)
-    out = torch.empty(sh.q, dtype=torch.bfloat16, device=dev)
-    idx = torch.empty(sh.rows, dtype=torch.int32, device=dev)
-    sel = torch.empty(sh.rows, dtype=torch.float32, device=dev)
-    lse = torch.empty(sh.lse, dtype=torch.float32, device=dev)
-    wts = torch.empty(sh.rows, dtype=torch.float32, device=dev)
-    ws, _ = gca.workspace(p, gca.OP_FORWARD, dev)
-    it = [0]
-
-    def call(pp=p):
-        gca.forward(pp, lmk_q, keys[it[0] % 2], q, kv["k"], kv["v"], out=out, idx=idx, sel=sel, lse=lse, w=wts,
-                    ws=ws)
-        it[0] += 1
-
-    for _ in range(5):
-        call()
-    torch.cuda.synchronize()
-    steps = args.decode_steps
+    path = os.path.join(ROOT, "peaks", "libpeaks.so")
+    if not os.path.exists(path):
+        return None
+    L = ctypes.CDLL(path)
+    L.peaks_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    L.peaks_mfma_loop.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
     stream = torch.cuda.current_stream()
-    ms_call = timed(call, steps, stream) / steps
-    prof_ms, per = kernel_times(call, steps, stream, gca)
-    planted = int(gi.plant_positions(w)[0])
-    found = planted in idx.cpu().numpy().ravel().tolist()
-    # the Gumbel top-k variant of the same call
-    pg = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, gumbel_seed=1)
-    call(pg)
-    g_ms = timed(lambda: call(pg), steps, stream) / steps
-    _, g_per = kernel_times(lambda: call(pg), steps, stream, gca)
-    key_bytes = w.n_chunks * w.Dl * 2
-    kv_bytes = 2 * w.topk * w.H * S * DH * 2
-    io_bytes = 2 * w.H * S * DH * 2 + w.Dl * 2
-    total_bytes = key_bytes + kv_bytes + io_bytes
-    scan_ms = sum(per["decode_scan_kernel"]) / len(per["decode_scan_kernel"])
-    kern = {k: {"avg_ms": sum(v) / len(v)} for k, v in per.items()}
-    scan_gbs = key_bytes / (scan_ms * 1e-3) / 1e9
-    del kv, keys
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    nbytes = 4 << 30
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    buf.fill_(1)
+    sink = torch.zeros(16, dtype=torch.float32, device=dev)
+    blocks = cus * 8
+
+    def read():
+        assert L.peaks_stream_read(ctypes.c_void_p(buf.data_ptr()), nbytes // 16, blocks,
+                                   ctypes.c_void_p(sink.data_ptr()), sp) == 0
+
+    for _ in range(3):
+        read()
+    ms = timed(read, 10, stream) / 10
+    read_gbs = nbytes / (ms * 1e-3) / 1e9
+    del buf
+    iters = 20000
+    mblocks = cus * 2                                  # 8 waves per CU, two per SIMD
+
+    def mfma():
+        assert L.peaks_mfma_loop(mblocks, iters, ctypes.c_void_p(sink.data_ptr()), sp) == 0
+
+    mfma()
+    mms = timed(mfma, 5, stream) / 5
+    flops = mblocks * 4 * iters * 8 * 32768
     torch.cuda.empty_cache()
-    return {
-        "metric": "retrieval-scan GB/s at 16M-ctx decode", "unit": "GB/s",
-        "value": total_bytes / (ms_call * 1e-3) / 1e9, "ms_per_call": ms_call, "calls": steps,
-        "profiled_ms_per_call": prof_ms / steps,
-        "bytes_per_call": total_bytes, "frac_of_hbm_peak": total_bytes / (ms_call * 1e-3) / 1e9 / HBM_PEAK_GBS,
-        "planted_retrieved": found,
-        "config": {"workload": "decode_16m_bf16: B=1 H=8 d=64, 16,777,216 past tokens (262,144 chunks), "
-                               "S=64, top-8, D=512, bf16"},
-        "roofline": {"kernel": "decode_scan_kernel", "bound": "hbm", "achieved": scan_gbs, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": scan_gbs / HBM_PEAK_GBS,
-                     "traffic": measured_traffic("decode_scan_kernel@decode_16m"),
-                     "algorithmic_bytes_per_launch": key_bytes, "avg_launch_ms": scan_ms},
-        "kernels": kern,
-        "gumbel_topk": {"value": total_bytes / (g_ms * 1e-3) / 1e9, "unit": "GB/s", "ms_per_call": g_ms,
-                        "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()}},
-    }
+    return {"stream_read_GBps": read_gbs, "stream_read_frac_of_spec": read_gbs / HBM_PEAK_GBS,
+            "mfma_bf16_TFLOPs": flops / (mms * 1e-3) / 1e12,
+            "mfma_bf16_frac_of_spec": flops / (mms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+            "compute_units": cus, "read_bytes": nbytes}
 
 
-def bench_decode_host_kv(args, dev, gca):
-    """Decode with the past chunks' K/V offloaded to pinned host memory (landmarks,
-    q and outputs in HBM): the decode attention gathers the k retrieved chunks over
-    the host link.  1M past tokens (16,384 chunks, 2 x 1.07 GB of host K/V)."""
-    import torch
-    from gen import get_workload, inputs as gi
-
-    w = get_workload("decode_16m_bf16", n_chunks=16384)
-    lq, lk = landmarks(w)
-    lmk_q, lmk_k = upload(w, lq, dev), upload(w, lk, dev)
-    kv = gi.device_kv(w, dev)
-    host = {n: torch.empty(kv[n].shape, dtype=kv[n].dtype, pin_memory=True) for n in ("k", "v")}
-    for n in ("k", "v"):
-        host[n].copy_(kv[n])
-    q = gi.device_tensors(w, ("q",), dev)["q"]
-    sh = gca.shapes(gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, mode=w.mode))
-    out = torch.empty(sh.q, dtype=torch.bfloat16, device=dev)
-    idx = torch.empty(sh.rows, dtype=torch.int32, device=dev)
-    sel = torch.empty(sh.rows, dtype=torch.float32, device=dev)
-    lse = torch.empty(sh.lse, dtype=torch.float32, device=dev)
-    wts = torch.empty(sh.rows, dtype=torch.float32, device=dev)
-    stream = torch.cuda.current_stream()
-    res = {}
-    for where, flags, k, v in (("device", 0, kv["k"], kv["v"]), ("host", gca.FLAG_HOST_KV, host["k"], host["v"])):
-        p = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, flags=flags)
-        ws, _ = gca.workspace(p, gca.OP_FORWARD, dev)
-
-        def call():
-            gca.forward(p, lmk_q, lmk_k, q, k, v, out=out, idx=idx, sel=sel, lse=lse, w=wts, ws=ws)
-
-        for _ in range(5):
-            call()
-        ms = timed(call, args.decode_steps, stream) / args.decode_steps
-        _, per = kernel_times(call, args.decode_steps, stream, gca)
-        res[where] = {"ms_per_call": ms, "kernels": {n: {"avg_ms": sum(d) / len(d)} for n, d in per.items()}}
-    gathered = 2 * w.topk * w.H * S * DH * 2      # K and V tiles of the retrieved chunks, every head
-    att_host = res["host"]["kernels"]["xattn_decode_kernel"]["avg_ms"]
-    att_dev = res["device"]["kernels"]["xattn_decode_kernel"]["avg_ms"]
-    del kv, host
-    torch.cuda.empty_cache()
-    return {"config": {"workload": "decode with host-resident K/V: B=1 H=8 d=64, 1,048,576 past tokens "
-                                   "(16,384 chunks), S=64, top-8, D=512, bf16; K/V in pinned host memory"},
-            "ms_per_call": res["host"]["ms_per_call"], "ms_per_call_device_kv": res["device"]["ms_per_call"],
-            "host_link_bytes_per_call": gathered,
-            "host_link_GBps": gathered / ((att_host - att_dev) * 1e-3) / 1e9 if att_host > att_dev else None,
-            "kernels": res["host"]["kernels"], "kernels_device_kv": res["device"]["kernels"]}
-
+# ---------------------------------------------------------------- main ----
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--fwd-steps", type=int, default=20)
     ap.add_argument("--decode-steps", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-host-kv", action="store_true", help="skip the decode leg with host-resident K/V")
+    ap.add_argument("--no-forward-legs", action="store_true", help="skip the 16K and 1M forward legs")
+    ap.add_argument("--no-peaks", action="store_true")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="first run one plain device copy of this many MiB (a known-size reference for "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE)")
-    ap.add_argument("--only", choices=["train", "decode"], default=None,
+    ap.add_argument("--only", choices=["train", "decode", "forward_16k", "planted_1m"], default=None,
                     help="run one leg only (for profiling); the JSON line then carries that leg")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -439,15 +657,21 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    if args.only == "decode":
-        line = {"decode_scan": bench_decode(args, dev, gca)}
-        if not args.no_host_kv:
-            line["decode_host_kv"] = bench_decode_host_kv(args, dev, gca)
+    if args.only:
+        args.no_cpu_baseline = True
+        if args.only == "decode":
+            _, leg, _, _ = bench_decode(args, dev, gca)
+            line = {"decode_scan": leg}
+        elif args.only == "train":
+            tr = bench_train(args, dev, gca)
+            line = {"ms_per_step": tr["ms_step"], "kernels": tr["kernels"], "roofline": tr["roofline"]}
+        else:
+            name = {"forward_16k": "train_16k_bf16", "planted_1m": "planted_1m_bf16"}[args.only]
+            _, leg, _ = bench_forward(args, dev, gca, name)
+            line = {args.only: leg}
         print(json.dumps(line), flush=True)
         return
-    if args.only == "train":
-        args.no_decode = True
-        args.no_cpu_baseline = True
+
     tr = bench_train(args, dev, gca)
     w = tr["w"]
     line = {
@@ -470,21 +694,41 @@ def main():
     # the GPU legs first, the host oracle last: a host-K/V decode leg measured
     # after the oracle's host-memory churn and the 16M decode leg ran 20x slower
     # per call with unchanged kernel times (a host-side stall, not the library's)
-    t_host = None
+    baselines = []
     if not args.no_cpu_baseline:
         t_host = {n: tr["t"][n][:1, :16].cpu() if n in ("q", "k", "v", "dout") else tr["t"][n][:1].cpu()
                   for n in ("lmk_q", "lmk_k", "q", "k", "v", "dout")}
+        baselines.append(("cpu_baseline", lambda: cpu_baseline(w, t_host)))
     del tr
     torch.cuda.empty_cache()
+    if not args.no_forward_legs:
+        for key, name, sample in (("forward_16k", "train_16k_bf16", dict(rows=None, chunks=None)),
+                                  ("planted_1m", "planted_1m_bf16",
+                                   dict(rows=list(range(16384 - 512, 16384)), chunks=list(range(2, 16384, 16))))):
+            log(f"{key} forward")
+            wf, leg, host = bench_forward(args, dev, gca, name)
+            line[key] = leg
+            if host is not None:
+                baselines.append((key, lambda wf=wf, host=host, sample=sample: cpu_forward_baseline(wf, host,
+                                                                                                  **sample)))
     if not args.no_decode:
-        print("[bench] decode scan at 16M context", file=sys.stderr, flush=True)
-        line["decode_scan"] = bench_decode(args, dev, gca)
+        log("decode scan at 16M context")
+        wd, leg, host, nbytes = bench_decode(args, dev, gca)
+        line["decode_scan"] = leg
+        if host is not None:
+            baselines.append(("decode_scan", lambda: cpu_decode_baseline(wd, host, nbytes)))
         if not args.no_host_kv:
-            print("[bench] decode with host-resident K/V at 1M context", file=sys.stderr, flush=True)
+            log("decode with host-resident K/V at 1M context")
             line["decode_host_kv"] = bench_decode_host_kv(args, dev, gca)
-    if t_host is not None:
-        print("[bench] cpu baseline (oracle sample)", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(w, t_host)
+    if not args.no_peaks:
+        log("on-device reference rates")
+        line["peaks_measured"] = measured_peaks(dev)
+    for key, fn in baselines:
+        log(f"cpu baseline ({key})")
+        if key == "cpu_baseline":
+            line["cpu_baseline"] = fn()
+        else:
+            line[key]["cpu_baseline"] = fn()
     print(json.dumps(line), flush=True)
 
 

@@ -81,5 +81,20 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
     return OUT
 
 
+def build_peaks() -> str:
+    """The on-device reference-rate probes bench.py reports next to the spec peaks
+    (a measurement aid, not part of libgca): peaks/libpeaks.so."""
+    src = os.path.join(ROOT, "peaks", "peaks.hip")
+    out = os.path.join(ROOT, "peaks", "libpeaks.so")
+    cmd = [hipcc(), "-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wno-unused-command-line-argument",
+           src, "-o", out + ".tmp"]
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
+    if r.returncode != 0:
+        raise RuntimeError("peaks build failed:\n" + r.stdout.decode(errors="replace"))
+    os.replace(out + ".tmp", out)
+    return out
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

@@ -4,6 +4,8 @@
     python profiling.py traffic --fetch DIR1/run_counter_collection.csv \
         --write DIR2/run_counter_collection.csv --copy-bytes N --cmd "..." --out profiles/hbm_traffic.json \
         [--tag WORKLOAD --append]
+    python profiling.py counters --mfma DIR3/run_counter_collection.csv --l2 DIR4/run_counter_collection.csv \
+        --simds 1024 --cmd "..." --out profiles/mfma_counters.json [--tag WORKLOAD --append]
 
 `traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
 launch for every GCA kernel, scaled by what the same counters read for a plain
@@ -40,7 +42,7 @@ def source_hash() -> str:
 
 def short_name(kernel: str) -> str:
     for key in ("xattn_fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel", "chunk_scores_kernel", "topk_kernel",
-                "fused_select_kernel", "decode_scan_kernel", "xattn_decode_kernel", "weights_kernel",
+                "fused_select_kernel", "select_part_kernel", "select_merge_kernel", "decode_scan_kernel", "xattn_decode_kernel", "weights_kernel",
                 "fill_zero_kernel", "csr_count_kernel", "csr_scan_kernel", "csr_fill_kernel", "csr_sort_kernel",
                 "dsel_kernel", "dlmk_q_kernel", "dlmk_k_kernel"):
         if key in kernel:
@@ -112,6 +114,45 @@ def traffic(fetch_csv: str, write_csv: str, copy_bytes: int, cmd: str, tag: str 
             "fetch_scale": f_scale, "write_scale": w_scale, "command": [cmd], "kernels": kernels}
 
 
+def _per_kernel_all(counter_csv: str):
+    """{kernel: {counter: [value per dispatch]}} of one rocprofv3 counter run."""
+    vals = {}
+    for r in csv.DictReader(open(counter_csv)):
+        k = vals.setdefault(short_name(r["Kernel_Name"]), {})
+        k.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    return vals
+
+
+def counters(mfma_csv: str, l2_csv: str, simds: int, cmd: str, tag: str = "") -> dict:
+    """Matrix-core busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE x
+    SIMDs, the MfmaUtil definition), bf16 matrix-core flops (SQ_INSTS_VALU_MFMA_MOPS_BF16
+    x 512) and the L2 hit fraction (TCC_HIT / (TCC_HIT + TCC_MISS)) per launch, the
+    median over each kernel's dispatches."""
+    m = _per_kernel_all(mfma_csv)
+    l2 = _per_kernel_all(l2_csv) if l2_csv else {}
+    med = statistics.median
+    kernels = {}
+    for k, c in sorted(m.items()):
+        if k == "copy":
+            continue
+        e = {"dispatches": len(c.get("GRBM_GUI_ACTIVE", []))}
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in c and "GRBM_GUI_ACTIVE" in c:
+            busy = [b / (g * simds) for b, g in zip(c["SQ_VALU_MFMA_BUSY_CYCLES"], c["GRBM_GUI_ACTIVE"]) if g > 0]
+            e["mfma_busy_frac"] = med(busy) if busy else None
+            e["gui_active_cycles"] = med(c["GRBM_GUI_ACTIVE"])
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in c:
+            e["mfma_bf16_flops_per_launch"] = med(c["SQ_INSTS_VALU_MFMA_MOPS_BF16"]) * 512.0
+        if "SQ_BUSY_CU_CYCLES" in c:
+            e["sq_busy_cu_cycles"] = med(c["SQ_BUSY_CU_CYCLES"])
+        h = l2.get(k, {})
+        if "TCC_HIT_sum" in h and "TCC_MISS_sum" in h:
+            fr = [a / (a + b) for a, b in zip(h["TCC_HIT_sum"], h["TCC_MISS_sum"]) if a + b > 0]
+            e["l2_hit_frac"] = med(fr) if fr else None
+            e["l2_requests_per_launch"] = med([a + b for a, b in zip(h["TCC_HIT_sum"], h["TCC_MISS_sum"])])
+        kernels[k + ("@" + tag if tag else "")] = e
+    return {"source_sha256": source_hash(), "simds": simds, "command": [cmd], "kernels": kernels}
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="what", required=True)
@@ -128,7 +169,28 @@ def main():
     b.add_argument("--out", required=True)
     b.add_argument("--tag", default="")
     b.add_argument("--append", action="store_true")
+    c = sub.add_parser("counters")
+    c.add_argument("--mfma", required=True, help="counter CSV with SQ_VALU_MFMA_BUSY_CYCLES, "
+                                                 "SQ_INSTS_VALU_MFMA_MOPS_BF16, GRBM_GUI_ACTIVE")
+    c.add_argument("--l2", default="", help="counter CSV with TCC_HIT_sum, TCC_MISS_sum")
+    c.add_argument("--simds", type=int, required=True)
+    c.add_argument("--cmd", required=True)
+    c.add_argument("--out", required=True)
+    c.add_argument("--tag", default="")
+    c.add_argument("--append", action="store_true")
     args = ap.parse_args()
+    if args.what == "counters":
+        data = counters(args.mfma, args.l2, args.simds, args.cmd, args.tag)
+        if args.append and os.path.exists(args.out):
+            old = json.load(open(args.out))
+            if old.get("source_sha256") != data["source_sha256"]:
+                raise SystemExit(f"{args.out} was taken from other kernel sources")
+            old["command"] = list(old["command"]) + data["command"]
+            old["kernels"].update(data["kernels"])
+            data = old
+        json.dump(data, open(args.out, "w"), indent=1)
+        print(args.out)
+        return
     if args.what == "stats":
         text = stats_md(args.csv, args.cmd)
         trace = os.path.join(os.path.dirname(args.csv), os.path.basename(args.csv).replace("kernel_stats",
