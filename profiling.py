@@ -5,7 +5,7 @@
         --write DIR2/run_counter_collection.csv --copy-bytes N --cmd "..." --out profiles/hbm_traffic.json \
         [--tag WORKLOAD --append]
     python profiling.py counters --mfma DIR3/run_counter_collection.csv --l2 DIR4/run_counter_collection.csv \
-        --simds 1024 --cmd "..." --out profiles/mfma_counters.json [--tag WORKLOAD --append]
+        --cmd "..." --out profiles/mfma_counters.json [--tag WORKLOAD --append]
 
 `traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
 launch for every GCA kernel, scaled by what the same counters read for a plain
@@ -123,11 +123,23 @@ def _per_kernel_all(counter_csv: str):
     return vals
 
 
-def counters(mfma_csv: str, l2_csv: str, simds: int, cmd: str, tag: str = "") -> dict:
-    """Matrix-core busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE x
-    SIMDs, the MfmaUtil definition), bf16 matrix-core flops (SQ_INSTS_VALU_MFMA_MOPS_BF16
-    x 512) and the L2 hit fraction (TCC_HIT / (TCC_HIT + TCC_MISS)) per launch, the
-    median over each kernel's dispatches."""
+def agent_counts(counter_csv: str):
+    """(SIMDs, XCCs) of the GPU from the run_agent_info.csv beside a counter CSV."""
+    path = os.path.join(os.path.dirname(counter_csv), os.path.basename(counter_csv).replace(
+        "counter_collection", "agent_info"))
+    for r in csv.DictReader(open(path)):
+        if r.get("Name", "").startswith("gfx"):
+            return int(r["Simd_Count"]), int(r["Num_Xcc"])
+    raise SystemExit(f"no GPU agent in {path}")
+
+
+def counters(mfma_csv: str, l2_csv: str, cmd: str, tag: str = "") -> dict:
+    """Matrix-core busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over the busy cycles of
+    every SIMD, the MfmaUtil definition: GRBM_GUI_ACTIVE is reported summed over the
+    XCCs, so one XCC's count is the sum divided by their number), bf16 matrix-core
+    flops (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) and the L2 hit fraction (TCC_HIT /
+    (TCC_HIT + TCC_MISS)) per launch, the median over each kernel's dispatches."""
+    simds, xccs = agent_counts(mfma_csv)
     m = _per_kernel_all(mfma_csv)
     l2 = _per_kernel_all(l2_csv) if l2_csv else {}
     med = statistics.median
@@ -137,9 +149,10 @@ def counters(mfma_csv: str, l2_csv: str, simds: int, cmd: str, tag: str = "") ->
             continue
         e = {"dispatches": len(c.get("GRBM_GUI_ACTIVE", []))}
         if "SQ_VALU_MFMA_BUSY_CYCLES" in c and "GRBM_GUI_ACTIVE" in c:
-            busy = [b / (g * simds) for b, g in zip(c["SQ_VALU_MFMA_BUSY_CYCLES"], c["GRBM_GUI_ACTIVE"]) if g > 0]
+            busy = [b / (g / xccs * simds) for b, g in zip(c["SQ_VALU_MFMA_BUSY_CYCLES"], c["GRBM_GUI_ACTIVE"])
+                    if g > 0]
             e["mfma_busy_frac"] = med(busy) if busy else None
-            e["gui_active_cycles"] = med(c["GRBM_GUI_ACTIVE"])
+            e["gui_active_cycles_per_xcc"] = med(c["GRBM_GUI_ACTIVE"]) / xccs
         if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in c:
             e["mfma_bf16_flops_per_launch"] = med(c["SQ_INSTS_VALU_MFMA_MOPS_BF16"]) * 512.0
         if "SQ_BUSY_CU_CYCLES" in c:
@@ -150,7 +163,7 @@ def counters(mfma_csv: str, l2_csv: str, simds: int, cmd: str, tag: str = "") ->
             e["l2_hit_frac"] = med(fr) if fr else None
             e["l2_requests_per_launch"] = med([a + b for a, b in zip(h["TCC_HIT_sum"], h["TCC_MISS_sum"])])
         kernels[k + ("@" + tag if tag else "")] = e
-    return {"source_sha256": source_hash(), "simds": simds, "command": [cmd], "kernels": kernels}
+    return {"source_sha256": source_hash(), "simds": simds, "xccs": xccs, "command": [cmd], "kernels": kernels}
 
 
 def main():
@@ -173,14 +186,13 @@ def main():
     c.add_argument("--mfma", required=True, help="counter CSV with SQ_VALU_MFMA_BUSY_CYCLES, "
                                                  "SQ_INSTS_VALU_MFMA_MOPS_BF16, GRBM_GUI_ACTIVE")
     c.add_argument("--l2", default="", help="counter CSV with TCC_HIT_sum, TCC_MISS_sum")
-    c.add_argument("--simds", type=int, required=True)
     c.add_argument("--cmd", required=True)
     c.add_argument("--out", required=True)
     c.add_argument("--tag", default="")
     c.add_argument("--append", action="store_true")
     args = ap.parse_args()
     if args.what == "counters":
-        data = counters(args.mfma, args.l2, args.simds, args.cmd, args.tag)
+        data = counters(args.mfma, args.l2, args.cmd, args.tag)
         if args.append and os.path.exists(args.out):
             old = json.load(open(args.out))
             if old.get("source_sha256") != data["source_sha256"]:
