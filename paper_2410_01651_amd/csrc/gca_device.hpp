@@ -123,13 +123,18 @@ __device__ __forceinline__ float to_f32(float x) { return x; }
 // LDS with global_load_lds_dwordx4: each lane supplies a global address and the
 // 64 lanes of one instruction fill 1 KB of consecutive LDS.  The LDS copy is
 // XOR-swizzled at 16-byte granularity: LDS chunk c' of row r holds the row's
-// global chunk c' ^ (r mod chunks-per-row).  A bf16 row is 128 bytes, one pass
-// over the 32 LDS banks; a 16-byte read per row (A/B fragments) serves 8 lanes =
-// 8 consecutive rows per cycle, which this map spreads over all banks.  The
-// transposed 8-byte reads (16 lanes = 4 rows x 2 adjacent chunks per cycle) see
-// 2-way conflicts under it; a map that removes those too (f(r) = (2 (r mod 4) +
-// bit 2 of r) ^ (2 * bit 3 of r)) measured no faster, its address arithmetic
-// costing what the conflicts did, so the plain map stays.
+// global chunk c' ^ sw(r).  The LDS serves 256 bytes (64 banks) per cycle: a
+// 16-byte read per lane (A/B fragments, lane l on row l mod 32) takes 16 lanes
+// per cycle, i.e. 16 consecutive rows, and a bf16 row is 128 bytes, so the 8
+// rows of one parity among them share a bank window and must take 8 different
+// chunks; the transposed 8-byte reads (32 lanes per cycle: rows r0 .. r0 + 3,
+// each four adjacent chunks 4 m .. 4 m + 3) need rows r0 and r0 + 2 (one
+// window) in different halves of the row.  For bf16, sw(r) = (b0 ^ b3) +
+// 2 b2 + 4 b1 (bits b of r mod 16) does both, and also keeps any 8 aligned
+// consecutive rows apart; it repeats every 16 rows, so row offsets of +16 and +32
+// stay constant displacements but +8 does not (the transposed reads at +8 rows
+// take their own addresses).  An fp32 row is 256 bytes (16 chunks): sw(r) =
+// r mod 16 already spreads 16 consecutive rows over the banks.
 //
 // The copies are asynchronous: a wave's own copies are complete once its
 // vector-memory counter has dropped to the number issued after them
@@ -142,21 +147,12 @@ template <typename T>
 struct Swz {
   static constexpr int kVec = 16 / sizeof(T);  // elements per 16-byte chunk
   static constexpr int kCPR = kD / kVec;       // chunks per row (8 bf16, 16 fp32)
-  __device__ static __forceinline__ int sw(int r) { return r & (kCPR - 1); }
+  __device__ static __forceinline__ int sw(int r) {
+    if constexpr (kCPR == 8) return ((r ^ (r >> 3)) & 1) | ((r >> 1) & 2) | ((r << 1) & 4);
+    else return r & (kCPR - 1);
+  }
   __device__ static __forceinline__ int off(int r, int col) {
     return r * kD + (((col / kVec) ^ sw(r)) * kVec) + (col % kVec);
-  }
-  // For tiles read only by 16-byte row fragments: a map that also keeps 16
-  // consecutive rows apart when the LDS serves 16 lanes (256 bytes) per cycle.
-  // bf16 rows are 128 bytes, so a 256-byte window holds two rows; the 8 rows of
-  // one parity among 16 consecutive ones must take 8 different chunks, and so
-  // must any 8 consecutive rows: chunk c ^ (r mod 8) ^ (5 if bit 3 of r).  fp32
-  // rows are 256 bytes: c ^ (r mod 16) already does both.
-  __device__ static __forceinline__ int sw16(int r) {
-    return kCPR == 8 ? ((r & 7) ^ ((r & 8) ? 5 : 0)) : (r & (kCPR - 1));
-  }
-  __device__ static __forceinline__ int off16(int r, int col) {
-    return r * kD + (((col / kVec) ^ sw16(r)) * kVec) + (col % kVec);
   }
 };
 
@@ -195,9 +191,8 @@ __device__ __forceinline__ uint32_t uniform_lds(const void* lds, uint32_t add = 
 // (the scalar-base form of the instruction), so issuing a tile costs one scalar
 // move and one vector-memory instruction per 16-byte chunk and no vector address
 // arithmetic.  `g` and `lds` must hold the same value in every lane.
-// ROWS: rows of the tile (64, or 32 for a half tile); SW16: lay the tile out by
-// Swz::off16 (tiles read by row fragments only) instead of Swz::off.
-template <typename T, int NW, int ROWS = kS, bool SW16 = false>
+// ROWS: rows of the tile (64, or 32 for a half tile).
+template <typename T, int NW, int ROWS = kS>
 struct TileCopy {
   static constexpr int kVec = Swz<T>::kVec, kCPR = Swz<T>::kCPR, kN = kCPR * ROWS / (64 * NW);
   static_assert(kN >= 1 && kN * 64 * NW == kCPR * ROWS, "the waves' 16-byte pieces cover the tile");
@@ -211,7 +206,7 @@ struct TileCopy {
     for (int ii = 0; ii < kN; ++ii) {
       const int pch = (ii * NW + wave) * 64 + lane;
       const int r = pch / kCPR;
-      const int c = (pch % kCPR) ^ (SW16 ? Swz<T>::sw16(r) : Swz<T>::sw(r));
+      const int c = (pch % kCPR) ^ Swz<T>::sw(r);
       const int rs = r < rows ? r : rows - 1;
       goff[ii] = (uint32_t)((rs * row_stride + c * kVec) * sizeof(T));
     }
@@ -247,30 +242,18 @@ __device__ __forceinline__ f32x8 lds_frag(const float* tile, int r, int col) {
   f.hi = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off(r, col + 4));
   return f;
 }
-// ... from a tile laid out by Swz::off16
-__device__ __forceinline__ bf16x8 lds_frag16(const __bf16* tile, int r, int col) {
-  return *reinterpret_cast<const bf16x8*>(tile + Swz<__bf16>::off16(r, col));
-}
-__device__ __forceinline__ f32x8 lds_frag16(const float* tile, int r, int col) {
-  f32x8 f;
-  f.lo = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off16(r, col));
-  f.hi = *reinterpret_cast<const f32x4*>(tile + Swz<float>::off16(r, col + 4));
-  return f;
-}
-
 // Fragment reads at precomputed LDS byte addresses (address space 3), so that a
 // constant displacement folds into the instruction's offset field.
 typedef __attribute__((address_space(3))) char lds_char;
 __device__ __forceinline__ bf16x8 lds_b128_at(const lds_char* p) {
   return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(p);
 }
-// Transposed fragment (see lds_frag_t): the two 8-byte transposed reads at p and
-// p + gap bytes (rows r0.. and r1.. of the same 16 columns).
-template <int GAP>
-__device__ __forceinline__ bf16x8 lds_tr_at(const lds_char* p) {
+// Transposed fragment (see lds_frag_t): the two 8-byte transposed reads at p0
+// and p1 (rows r0.. and r1.. of the same 16 columns).
+__device__ __forceinline__ bf16x8 lds_tr2(const lds_char* p0, const lds_char* p1) {
   typedef __attribute__((address_space(3))) bf16x4_tr lds_v4;
-  bf16x4_tr a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p));
-  bf16x4_tr b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p + GAP));
+  bf16x4_tr a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p0));
+  bf16x4_tr b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_v4*)(p1));
   bf16x8 f;
   f[0] = a[0]; f[1] = a[1]; f[2] = a[2]; f[3] = a[3];
   f[4] = b[0]; f[5] = b[1]; f[6] = b[2]; f[7] = b[3];

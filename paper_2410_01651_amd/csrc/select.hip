@@ -99,9 +99,9 @@ __global__ __launch_bounds__(kSelThreads, 2) void select_part_kernel(const T* __
 
   // copies: every wave copies its share of each 32 x 64 chunk of a tile; the
   // last key tile may hold fewer than 32 keys (rows past it repeat the last)
-  const TileCopy<T, kSelWaves, kSelTile, true> cp_full(wave, lane, p.D, kSelTile);
+  const TileCopy<T, kSelWaves, kSelTile> cp_full(wave, lane, p.D, kSelTile);
   const int last_rows = (int)(p.nKV - (p.tiles - 1) * kSelTile);
-  const TileCopy<T, kSelWaves, kSelTile, true> cp_last(wave, lane, p.D, last_rows);
+  const TileCopy<T, kSelWaves, kSelTile> cp_last(wave, lane, p.D, last_rows);
   const T* kbase = lk + bhr * p.nKV * p.D;
   auto issue = [&](int u) __device__ {
     const int64_t j = tile_of(u);
@@ -144,7 +144,7 @@ __global__ __launch_bounds__(kSelThreads, 2) void select_part_kernel(const T* __
 #pragma unroll
         for (int c = 0; c < NCH; ++c)
 #pragma unroll
-          for (int kb = 0; kb < 4; ++kb) mma32(a, lds_frag16(sK + c * TILE, key0 + l32, 16 * kb + 8 * hh), qf[c][kb]);
+          for (int kb = 0; kb < 4; ++kb) mma32(a, lds_frag(sK + c * TILE, key0 + l32, 16 * kb + 8 * hh), qf[c][kb]);
         return a;
       };
       const f32x16 acc = half_scores(0);

@@ -300,7 +300,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
   constexpr bool kB16 = std::is_same<T, __bf16>::value;
   constexpr uint32_t kTileB = TILE * sizeof(T), kRowB = kD * sizeof(T);
   const lds_char* const lds0 = (const lds_char*)(ring);
-  uint32_t kofs[4], tofs[2];
+  uint32_t kofs[4], tofs[2][2];
   {
     const uint32_t pb = (uint32_t)pair * 4 * kTileB;
     const int s16 = lane & 15;
@@ -308,7 +308,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     for (int kb = 0; kb < 4; ++kb) kofs[kb] = pb + Swz<T>::off(lane & 31, 16 * kb + 8 * hh) * sizeof(T);
 #pragma unroll
     for (int dh = 0; dh < 2; ++dh)
-      tofs[dh] = pb + Swz<T>::off(4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
+#pragma unroll
+      for (int r8 = 0; r8 < 2; ++r8)
+        tofs[dh][r8] = pb + Swz<T>::off(8 * r8 + 4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
   }
 
   f32x16 g0a = zero16(), g1a = zero16();  // dQ^T, d rows 0-31 / 32-63
@@ -365,8 +367,10 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       if constexpr (kB16) {
-        mma32(g0a, lds_tr_at<8 * kRowB>(lds0 + (tofs[0] + co) + 16 * kb * kRowB), f[kb]);
-        mma32(g1a, lds_tr_at<8 * kRowB>(lds0 + (tofs[1] + co) + 16 * kb * kRowB), f[kb]);
+        mma32(g0a, lds_tr2(lds0 + (tofs[0][0] + co) + 16 * kb * kRowB, lds0 + (tofs[0][1] + co) + 16 * kb * kRowB),
+              f[kb]);
+        mma32(g1a, lds_tr2(lds0 + (tofs[1][0] + co) + 16 * kb * kRowB, lds0 + (tofs[1][1] + co) + 16 * kb * kRowB),
+              f[kb]);
       } else {
         mma32(g0a, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), f[kb]);
         mma32(g1a, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb), f[kb]);
@@ -559,14 +563,16 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
   constexpr bool kB16 = std::is_same<T, __bf16>::value;
   constexpr uint32_t kTileB = TILE * sizeof(T), kRowB = kD * sizeof(T), kEntryB = ENTRY * sizeof(T);
   const lds_char* const lds0 = (const lds_char*)(ring);
-  uint32_t rofs[4], tofs[2];
+  uint32_t rofs[4], tofs[2][2];
   {
     const int s16 = lane & 15;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) rofs[kb] = Swz<T>::off(lane & 31, 16 * kb + 8 * hh) * sizeof(T);
 #pragma unroll
     for (int dh = 0; dh < 2; ++dh)
-      tofs[dh] = Swz<T>::off(4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
+#pragma unroll
+      for (int r8 = 0; r8 < 2; ++r8)
+        tofs[dh][r8] = Swz<T>::off(8 * r8 + 4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
   }
   auto row_frag = [&](const T* tile, uint32_t so, int kb, int half32) __device__ -> Frag<T> {
     if constexpr (kB16) {
@@ -577,7 +583,7 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
   };
   auto col_frag = [&](const T* tile, uint32_t so, int kb, int dh) __device__ -> Frag<T> {
     if constexpr (kB16) {
-      return lds_tr_at<8 * kRowB>(lds0 + (tofs[dh] + so) + 16 * kb * kRowB);
+      return lds_tr2(lds0 + (tofs[dh][0] + so) + 16 * kb * kRowB, lds0 + (tofs[dh][1] + so) + 16 * kb * kRowB);
     } else {
       return lds_frag_t(tile, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 * dh + cb);
     }

@@ -182,7 +182,7 @@ __global__ __launch_bounds__(kDecThreads) void xattn_decode_kernel(DecParams p) 
   const T* const gv = reinterpret_cast<const T*>(p.v);
   const int64_t kvb = wi * p.nKV * TILE;  // this (batch, head)'s key/value slice
   const lds_char* const lds0 = (const lds_char*)(ring);
-  uint32_t kofs[4], vofs[2];
+  uint32_t kofs[4], vofs[2][2];
   {
     const uint32_t pb = (uint32_t)pair * SP * 2 * kTileB;
     const int s16 = lane & 15;
@@ -190,7 +190,10 @@ __global__ __launch_bounds__(kDecThreads) void xattn_decode_kernel(DecParams p) 
     for (int kb = 0; kb < 4; ++kb) kofs[kb] = pb + Swz<T>::off(lane & 31, 16 * kb + 8 * hh) * sizeof(T);
 #pragma unroll
     for (int dh = 0; dh < 2; ++dh)
-      vofs[dh] = pb + kTileB + Swz<T>::off(4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
+#pragma unroll
+      for (int r8 = 0; r8 < 2; ++r8)
+        vofs[dh][r8] =
+            pb + kTileB + Swz<T>::off(8 * r8 + 4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
   }
 
   // slot s (chunk tiles in the pair's resident slot t) against this wave's queries
@@ -220,8 +223,9 @@ __global__ __launch_bounds__(kDecThreads) void xattn_decode_kernel(DecParams p) 
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       if constexpr (kB16) {
-        va[2 * kb] = lds_tr_at<8 * kRowB>(lds0 + (vofs[0] + co) + 16 * kb * kRowB);
-        va[2 * kb + 1] = lds_tr_at<8 * kRowB>(lds0 + (vofs[1] + co) + 16 * kb * kRowB);
+        va[2 * kb] = lds_tr2(lds0 + (vofs[0][0] + co) + 16 * kb * kRowB, lds0 + (vofs[0][1] + co) + 16 * kb * kRowB);
+        va[2 * kb + 1] =
+            lds_tr2(lds0 + (vofs[1][0] + co) + 16 * kb * kRowB, lds0 + (vofs[1][1] + co) + 16 * kb * kRowB);
       } else {
         va[2 * kb] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
         va[2 * kb + 1] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);

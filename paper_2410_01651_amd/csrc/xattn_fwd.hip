@@ -194,7 +194,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
   constexpr bool kB16 = std::is_same<T, __bf16>::value;
   constexpr uint32_t kTileB = TILE * sizeof(T), kRowB = kD * sizeof(T);
   const lds_char* const lds0 = (const lds_char*)(ring);
-  uint32_t kofs[4], vofs[2];
+  uint32_t kofs[4], vofs[2][2];
   {
     const uint32_t pb = (uint32_t)pair * 4 * kTileB;
     const int s16 = lane & 15;
@@ -202,7 +202,10 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     for (int kb = 0; kb < 4; ++kb) kofs[kb] = pb + Swz<T>::off(lane & 31, 16 * kb + 8 * hh) * sizeof(T);
 #pragma unroll
     for (int dh = 0; dh < 2; ++dh)
-      vofs[dh] = pb + kTileB + Swz<T>::off(4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
+#pragma unroll
+      for (int r8 = 0; r8 < 2; ++r8)
+        vofs[dh][r8] =
+            pb + kTileB + Swz<T>::off(8 * r8 + 4 * hh + (s16 >> 2), 32 * dh + cb + 4 * (s16 & 3)) * sizeof(T);
   }
 
   // one retrieved chunk (item u of the current chunk, tokens from tok0) against
@@ -236,8 +239,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       if constexpr (kB16) {
-        va[2 * kb] = lds_tr_at<8 * kRowB>(lds0 + (vofs[0] + co) + 16 * kb * kRowB);
-        va[2 * kb + 1] = lds_tr_at<8 * kRowB>(lds0 + (vofs[1] + co) + 16 * kb * kRowB);
+        va[2 * kb] = lds_tr2(lds0 + (vofs[0][0] + co) + 16 * kb * kRowB, lds0 + (vofs[0][1] + co) + 16 * kb * kRowB);
+        va[2 * kb + 1] =
+            lds_tr2(lds0 + (vofs[1][0] + co) + 16 * kb * kRowB, lds0 + (vofs[1][1] + co) + 16 * kb * kRowB);
       } else {
         va[2 * kb] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
         va[2 * kb + 1] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
