@@ -32,10 +32,15 @@ Readings where the paper is silent or ambiguous (all configurable):
   the weights and everything after use the raw scores;
 * ``lse`` is the log of each (row, slot) softmax denominator, -inf for pads;
 * one retrieval head shared by all heads (Hr = 1, as Eq. 1 yields one score per
-  chunk pair) or one per head (Hr = H).
+  chunk pair) or one per head (Hr = H);
+* query rows per chunk ``Sq``: S by default; S + 1 when every chunk carries its
+  landmark (LMK) token as a last query row (Methodology, Model Architecture: the
+  LMK token is inserted at the end of each chunk, and Grouped Cross-Attention
+  takes the S + 1 hidden states of chunk t+1 as queries against the S-row
+  memories C_k of the retrieved chunks).
 
 Array layouts are row-major: lmk_q [B,Hr,nQ,D], lmk_k [B,Hr,nC,D],
-q/dout [B,H,nQ*S,d], k/v [B,H,nC*S,d]; all inputs are taken as fp64.
+q/dout [B,H,nQ*Sq,d], k/v [B,H,nC*S,d]; all inputs are taken as fp64.
 """
 
 import numpy as np
@@ -186,7 +191,7 @@ def chunk_attention(qc, kc, vc, attn_scale, off_by_one=False):
 
 
 def xattn_fwd(q, k, v, idx, w, S, attn_scale, mode="causal", off_by_one=False,
-              chunks=None, heads=None):
+              chunks=None, heads=None, Sq=None):
     """Grouped cross attention forward (Eq. 2-3).
 
     For each head and query chunk c, every valid slot s of the retrieved set
@@ -194,12 +199,14 @@ def xattn_fwd(q, k, v, idx, w, S, attn_scale, mode="causal", off_by_one=False,
     O_c = sum_s w[t, s] O'_s.  Returns (O [B,H,Lq,d], lse [B,H,Lq,k]); rows of
     chunks whose set is empty are 0 and their lse is -inf.  ``chunks`` /
     ``heads`` restrict the work to the listed query chunks / heads (other rows
-    are left 0 / -inf).
+    are left 0 / -inf).  Query chunk c is rows [c*Sq, (c+1)*Sq) of q (Sq = S
+    unless given); key chunk j is rows [j*S, (j+1)*S) of k and v.
     """
     q, k, v, w = _f64(q), _f64(k), _f64(v), _f64(w)
     B, H, Lq, d = q.shape
     Hr, kk = idx.shape[1], idx.shape[-1]
-    nQ = Lq // S
+    Sq = S if Sq is None else Sq
+    nQ = Lq // Sq
     out = np.zeros((B, H, Lq, d))
     lse = np.full((B, H, Lq, kk), NEG_INF)
     chunks = range(nQ) if chunks is None else chunks
@@ -211,7 +218,7 @@ def xattn_fwd(q, k, v, idx, w, S, attn_scale, mode="causal", off_by_one=False,
                 t = retrieval_row(c, mode)
                 if t < 0:
                     continue
-                rows = slice(c * S, (c + 1) * S)
+                rows = slice(c * Sq, (c + 1) * Sq)
                 for s in range(kk):
                     j = int(idx[b, hr, t, s])
                     if j < 0:
@@ -225,7 +232,7 @@ def xattn_fwd(q, k, v, idx, w, S, attn_scale, mode="causal", off_by_one=False,
 
 
 def xattn_bwd(q, k, v, idx, w, dout, S, attn_scale, mode="causal", off_by_one=False,
-              chunks=None, heads=None):
+              chunks=None, heads=None, Sq=None):
     """Backward of grouped cross attention (chain rule through Eq. 2-3).
 
     With L = sum(dout o O), for every (head, query chunk c, valid slot s):
@@ -233,12 +240,14 @@ def xattn_bwd(q, k, v, idx, w, dout, S, attn_scale, mode="causal", off_by_one=Fa
     dS = w P_s o (dP_s - D_s) (the softmax Jacobian, which has the same form for
     softmax-off-by-one), dV_j += w P_s^T dout_c, dQ_c += attn_scale dS K_j,
     dK_j += attn_scale dS^T Q_c, and dL/dw[t, s] = sum over heads of the retrieval
-    head and rows of D_s.  Returns (dq, dk, dv, dw [B,Hr,nQr,k]).
+    head and rows of D_s.  Returns (dq, dk, dv, dw [B,Hr,nQr,k]).  Query chunks
+    have Sq rows (S unless given), key chunks S.
     """
     q, k, v, w, dout = _f64(q), _f64(k), _f64(v), _f64(w), _f64(dout)
     B, H, Lq, d = q.shape
     Hr, nQr, kk = idx.shape[1], idx.shape[2], idx.shape[-1]
-    nQ = Lq // S
+    Sq = S if Sq is None else Sq
+    nQ = Lq // Sq
     dq = np.zeros_like(q)
     dk = np.zeros_like(k)
     dv = np.zeros_like(v)
@@ -252,7 +261,7 @@ def xattn_bwd(q, k, v, idx, w, dout, S, attn_scale, mode="causal", off_by_one=Fa
                 t = retrieval_row(c, mode)
                 if t < 0:
                     continue
-                rows = slice(c * S, (c + 1) * S)
+                rows = slice(c * Sq, (c + 1) * Sq)
                 qc, doc = q[b, h, rows], dout[b, h, rows]
                 for s in range(kk):
                     j = int(idx[b, hr, t, s])
@@ -314,20 +323,23 @@ def forward(p, lmk_q, lmk_k, q, k, v):
     """Scores -> top-k -> weights -> grouped cross attention (Eq. 1-3).
 
     ``p`` is a mapping with S, topk, score_scale, attn_scale, mode, off_by_one
-    and optionally gumbel_seed (Gumbel top-k selection).  Returns a dict with scores, idx, sel, w, out and lse.
+    and optionally gumbel_seed (Gumbel top-k selection) and Sq (query rows per
+    chunk, S + 1 with the LMK row).  Returns a dict with scores, idx, sel, w, out
+    and lse.
     """
     r = scores(lmk_q, lmk_k, p["score_scale"], p["mode"])
     idx, sel = topk(r, p["topk"], p.get("gumbel_seed"))
     w = fusion_weights(sel)
     out, lse = xattn_fwd(q, k, v, idx, w, p["S"], p["attn_scale"], p["mode"],
-                         p.get("off_by_one", False))
+                         p.get("off_by_one", False), Sq=p.get("Sq"))
     return {"scores": r, "idx": idx, "sel": sel, "w": w, "out": out, "lse": lse}
 
 
 def backward(p, fwd, lmk_q, lmk_k, q, k, v, dout):
     """Gradients of sum(dout o out) into q, k, v, the scores and the landmarks."""
     dq, dk, dv, dw = xattn_bwd(q, k, v, fwd["idx"], fwd["w"], dout, p["S"],
-                               p["attn_scale"], p["mode"], p.get("off_by_one", False))
+                               p["attn_scale"], p["mode"], p.get("off_by_one", False),
+                               Sq=p.get("Sq"))
     dsel = dsel_from_dw(fwd["w"], dw)
     dlq, dlk = landmark_grads(dsel, fwd["idx"], lmk_q, lmk_k, p["score_scale"])
     return {"dq": dq, "dk": dk, "dv": dv, "dw": dw, "dsel": dsel,
