@@ -257,6 +257,29 @@ def bench_train(args, dev, gca):
               "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()
                           if k in ("chunk_scores_kernel", "topk_kernel")}}
     log(f"gumbel top-k {args.steps} steps: {g_ms:.3f} ms/step")
+    # the same step with S+1 query rows per chunk (each chunk's LMK token as its
+    # last query row); k/v and the landmarks are shared with the step above
+    wx = get_workload("fwdbwd_64k_bf16", lmk_row=True)
+    tx = dict(t, **gi.device_tensors(wx, ("q", "dout"), dev))
+    px = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, lmk_row=True)
+    fox = forward_outputs(px, gca, dev)
+    gx = dict(grads, dq=torch.empty(gca.shapes(px).q, dtype=torch.bfloat16, device=dev))
+    wsbx, _ = gca.workspace(px, gca.OP_BACKWARD, dev)
+
+    def step_x():
+        gca.forward(px, tx["lmk_q"], tx["lmk_k"], tx["q"], tx["k"], tx["v"], ws=wsf, **fox)
+        gca.grouped_xattn_bwd(px, tx["q"], tx["k"], tx["v"], fox["idx"], fox["sel"], fox["lse"], tx["dout"],
+                              tx["lmk_q"], tx["lmk_k"], ws=wsbx, grads=gx)
+
+    step_x()
+    x_ms = timed(step_x, args.steps, stream) / args.steps
+    _, x_per = kernel_times(step_x, args.steps, stream, gca)
+    lmk_row = {"value": wx.B * wx.Lq / (x_ms * 1e-3), "unit": "tokens/s", "ms_per_step": x_ms,
+               "query_rows_per_chunk": wx.Sq,
+               "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in x_per.items()
+                           if k in ("xattn_fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel")}}
+    log(f"S+1 query rows {args.steps} steps: {x_ms:.3f} ms/step")
+    del tx, fox, gx, wsbx
 
     units = valid_units(idx_host, w)
     kern = kernel_table(per, args.steps)
@@ -269,7 +292,7 @@ def bench_train(args, dev, gca):
     algo_fl = units * S * (flops_per_unit()["xattn_fwd_kernel"] + 5 * 2 * S * DH)
     return {
         "w": w, "t": t, "tokens": w.B * w.Lq, "ms_step": ms_step, "profiled_ms_step": prof_ms / args.steps,
-        "gumbel": gumbel, "kernels": kern, "roofline": roof, "units": units,
+        "gumbel": gumbel, "lmk_row": lmk_row, "kernels": kern, "roofline": roof, "units": units,
         "path_tflops": algo_fl / (ms_step * 1e-3) / 1e12,
     }
 
@@ -664,7 +687,8 @@ def main():
             line = {"decode_scan": leg}
         elif args.only == "train":
             tr = bench_train(args, dev, gca)
-            line = {"ms_per_step": tr["ms_step"], "kernels": tr["kernels"], "roofline": tr["roofline"]}
+            line = {"ms_per_step": tr["ms_step"], "kernels": tr["kernels"], "roofline": tr["roofline"],
+                    "lmk_row": tr["lmk_row"]}
         else:
             name = {"forward_16k": "train_16k_bf16", "planted_1m": "planted_1m_bf16"}[args.only]
             _, leg, _ = bench_forward(args, dev, gca, name)
@@ -689,6 +713,7 @@ def main():
         "roofline": tr["roofline"],
         "path_algorithmic_tflops": tr["path_tflops"],
         "gumbel_topk": tr["gumbel"],
+        "lmk_row": tr["lmk_row"],
         "kernels": tr["kernels"],
     }
     # the GPU legs first, the host oracle last: a host-K/V decode leg measured

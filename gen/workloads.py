@@ -31,6 +31,7 @@ class Workload:
     whole_reseed: bool = False   # redraw every input until all margins hold
     device_kv: bool = False      # K/V cache drawn on the device (too large for host)
     gumbel_seed: int = -1        # >= 0: Gumbel top-k selection with this generator seed
+    lmk_row: bool = False        # query chunks carry their LMK token as an S+1-th row
     notes: str = field(default="", compare=False)
 
     @property
@@ -42,8 +43,13 @@ class Workload:
         return 1 if self.mode == "decode" else self.n_chunks
 
     @property
+    def Sq(self) -> int:
+        """Query rows per chunk: S, or S + 1 with the LMK row."""
+        return self.S + 1 if self.lmk_row else self.S
+
+    @property
     def Lq(self) -> int:
-        return self.n_query_chunks * self.S
+        return self.n_query_chunks * self.Sq
 
     @property
     def Lkv(self) -> int:

@@ -20,7 +20,9 @@
  *   chunk of S tokens has one landmark query, scored against all n_chunks past
  *   chunks; that set feeds the new chunk's own tokens.
  * - nQ (landmark query rows) = n_chunks in CAUSAL mode and 1 in DECODE mode;
- *   Lq (query tokens) = nQ * S; Lkv (key/value tokens) = n_chunks * S.
+ *   Lq (query tokens) = nQ * Sq with Sq = S (S + 1 under GCA_FLAG_LMK_ROW);
+ *   Lkv (key/value tokens) = n_chunks * S.  Query chunk c is rows
+ *   [c * Sq, (c + 1) * Sq) of the query-side tensors.
  * - Retrieval heads: Hr = 1 shares one score per chunk pair across all H heads
  *   (Eq. 1 yields one scalar per pair); Hr = H gives every head its own landmarks.
  *   Head h uses retrieval head (Hr == 1 ? 0 : h).
@@ -74,6 +76,16 @@ typedef enum { GCA_CAUSAL = 0, GCA_DECODE = 1 } gca_mode;
                                   * host link (their device mapping, hipHostGetDevicePointer).
                                   * GCA_ERR_INVALID if k or v has no device mapping, or in
                                   * CAUSAL mode. */
+#define GCA_FLAG_LMK_ROW 16u     /* CAUSAL: every query chunk has S + 1 rows, its S tokens followed
+                                  * by its landmark (LMK) token (Methodology, Model Architecture:
+                                  * the LMK token is inserted at the end of each chunk, and the
+                                  * grouped cross attention of chunk t+1 takes its S + 1 hidden
+                                  * states as queries against S-row retrieved chunks).  q, out,
+                                  * lse, dout and dq then hold Lq = nQ * (S + 1) rows, row
+                                  * c * (S + 1) + S being chunk c's LMK row; k, v, dk and dv keep
+                                  * n_chunks * S rows.  The LMK row attends to and is fused over
+                                  * the same retrieved set as its chunk's tokens.
+                                  * GCA_ERR_UNSUPPORTED in DECODE mode. */
 #define GCA_FLAG_GUMBEL 4u       /* Gumbel top-k selection (Training & Inference, "Gumbel Top-k
                                   * sampling"): every selection (gca_topk, gca_forward in both
                                   * modes) ranks score + g, g = -ln(-ln u) with u from the

@@ -62,8 +62,11 @@ gca_status check_problem(const gca_problem* p, gca::Shape& s) {
   if (p->off_by_one != 0 && p->off_by_one != 1) return fail(GCA_ERR_INVALID, "off_by_one must be 0 or 1");
   if (!std::isfinite(p->score_scale) || !std::isfinite(p->attn_scale))
     return fail(GCA_ERR_INVALID, "scales must be finite");
-  if (p->flags & ~(GCA_FLAG_FUSED_TOPK | GCA_FLAG_MATERIALIZE | GCA_FLAG_GUMBEL | GCA_FLAG_HOST_KV))
+  if (p->flags & ~(GCA_FLAG_FUSED_TOPK | GCA_FLAG_MATERIALIZE | GCA_FLAG_GUMBEL | GCA_FLAG_HOST_KV |
+                   GCA_FLAG_LMK_ROW))
     return fail(GCA_ERR_INVALID, "unknown flag bits");
+  if ((p->flags & GCA_FLAG_LMK_ROW) && p->mode != GCA_CAUSAL)
+    return fail(GCA_ERR_UNSUPPORTED, "GCA_FLAG_LMK_ROW (S + 1 query rows) is supported in CAUSAL mode");
   if ((p->flags & GCA_FLAG_HOST_KV) && p->mode != GCA_DECODE)
     return fail(GCA_ERR_INVALID, "GCA_FLAG_HOST_KV is for DECODE mode");
   if ((p->flags & GCA_FLAG_FUSED_TOPK) && (p->flags & GCA_FLAG_MATERIALIZE))
@@ -76,6 +79,7 @@ gca_status check_problem(const gca_problem* p, gca::Shape& s) {
   s.causal = p->mode == GCA_CAUSAL ? 1 : 0;
   s.nKV = p->n_chunks;
   s.nQ = s.causal ? p->n_chunks : 1;
+  s.Sq = (p->flags & GCA_FLAG_LMK_ROW) ? gca::kChunk + 1 : gca::kChunk;
   s.bf16 = p->dtype == GCA_BF16 ? 1 : 0;
   s.off_by_one = p->off_by_one;
   s.score_scale = p->score_scale;

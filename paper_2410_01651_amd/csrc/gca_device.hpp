@@ -223,6 +223,15 @@ struct TileCopy {
   }
 };
 
+// The active lanes of a wave each copy 16 bytes at g + lane_off into LDS at
+// lds + 16 * lane (one row of a tile: lane_off = 16 * lane); g and lds
+// wave-uniform.
+__device__ __forceinline__ void dma_row16(const void* g, uint32_t lane_off, const void* lds) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(lane_off), "s"(uniform_addr(g)),
+               "s"(uniform_lds(lds))
+               : "m0");
+}
+
 // One wave copies 64 floats at g + lane_off (bytes, lane_off = lane * stride
 // precomputed) into 64 consecutive LDS floats; g and lds wave-uniform.
 __device__ __forceinline__ void dma_column_s(const float* g, uint32_t lane_off, const float* lds) {
@@ -287,6 +296,69 @@ __device__ __forceinline__ f32x8 lds_frag_t(const float* tile, int r0, int r1, i
                tile[Z::off(r0 + 3, col)]};
   f.hi = f32x4{tile[Z::off(r1, col)], tile[Z::off(r1 + 1, col)], tile[Z::off(r1 + 2, col)],
                tile[Z::off(r1 + 3, col)]};
+  return f;
+}
+
+// ------------------------------------------- one row against a tile ----
+//
+// A single query row (the LMK row of a chunk) against a tile whose fragments a
+// wave already holds: the row is a plain vector x[64] in LDS, read in the entry
+// order of the fragment it meets, and the products run on the VALU as fp32 dot
+// products (v_dot2_f32_bf16 for bf16: exact products, fp32 sums, as on MFMA).
+
+// sum_m a[m] b[m] + acc over the 8 entries of two fragments
+__device__ __forceinline__ float frag_dot(const bf16x8& a, const bf16x8& b, float acc) {
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 0, 1), __builtin_shufflevector(b, b, 0, 1),
+                                        acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 2, 3), __builtin_shufflevector(b, b, 2, 3),
+                                        acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 4, 5), __builtin_shufflevector(b, b, 4, 5),
+                                        acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(a, a, 6, 7), __builtin_shufflevector(b, b, 6, 7),
+                                        acc, false);
+  return acc;
+}
+__device__ __forceinline__ float frag_dot(const f32x8& a, const f32x8& b, float acc) {
+#pragma unroll
+  for (int m = 0; m < 4; ++m) acc = fmaf(a.lo[m], b.lo[m], acc);
+#pragma unroll
+  for (int m = 0; m < 4; ++m) acc = fmaf(a.hi[m], b.hi[m], acc);
+  return acc;
+}
+// A fragment whose entry 0 is x and whose other entries are 0.
+template <typename T> __device__ __forceinline__ Frag<T> frag_e0(float x);
+template <> __device__ __forceinline__ bf16x8 frag_e0<__bf16>(float x) {
+  bf16x8 f;
+#pragma unroll
+  for (int m = 0; m < 8; ++m) f[m] = (__bf16)0.f;
+  f[0] = (__bf16)x;
+  return f;
+}
+template <> __device__ __forceinline__ f32x8 frag_e0<float>(float x) {
+  f32x8 f;
+  f.lo = f32x4{x, 0.f, 0.f, 0.f};
+  f.hi = f32x4{0.f, 0.f, 0.f, 0.f};
+  return f;
+}
+// Entries x[c .. c+7]: meets a row fragment (contraction along the row).
+template <typename T>
+__device__ __forceinline__ Frag<T> vec_frag(const T* x, int c) {
+  return load_frag(x + c);
+}
+// Entries x[r0 .. r0+3] then x[r1 .. r1+3]: meets a column fragment (lds_frag_t,
+// lds_tr2) or the probability fragments built from an accumulator.
+__device__ __forceinline__ bf16x8 vec_frag_t(const __bf16* x, int r0, int r1) {
+  typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 v4;
+  const v4 a = *reinterpret_cast<const v4*>(x + r0), b = *reinterpret_cast<const v4*>(x + r1);
+  bf16x8 f;
+  f[0] = a[0]; f[1] = a[1]; f[2] = a[2]; f[3] = a[3];
+  f[4] = b[0]; f[5] = b[1]; f[6] = b[2]; f[7] = b[3];
+  return f;
+}
+__device__ __forceinline__ f32x8 vec_frag_t(const float* x, int r0, int r1) {
+  f32x8 f;
+  f.lo = *reinterpret_cast<const f32x4*>(x + r0);
+  f.hi = *reinterpret_cast<const f32x4*>(x + r1);
   return f;
 }
 

@@ -16,6 +16,7 @@ struct Shape {
   int B, H, Hr, D, topk;
   int64_t nQ;      // landmark query rows (query chunks)
   int64_t nKV;     // key/value chunks (score columns)
+  int Sq;          // query rows per chunk: kChunk, or kChunk + 1 with the LMK row (causal only)
   int causal;      // 1: row t feeds chunk t+1 and sees chunks [0,t); 0: decode
   int bf16;        // element type of tensors: 1 bf16, 0 fp32
   int off_by_one;
@@ -76,7 +77,7 @@ constexpr int kHeadInts = 16;
 constexpr int kHeadEntries = 8;
 struct BwdWs {
   float* w;        // [B*Hr, nQ, K] fusion weights
-  float* Dbuf;     // [B*H, K, Lq]  -D_s per query token (slot-major: one slot's tokens contiguous)
+  float* Dbuf;     // [B*H, K, Lq]  -D_s per query token (slot-major: one slot's tokens contiguous; Lq = nQ * Sq)
   float* Lbuf;     // [B*H, K, Lq]  log2(e) lse - log2(w_s)
   float* dwp;      // [B*H, nQ, K, 2] dw partials per head and query half
   int* counts;     // [B*Hr, nKV]

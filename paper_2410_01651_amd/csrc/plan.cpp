@@ -114,8 +114,8 @@ BwdWs carve(const Shape& s, Carver& c) {
   const size_t BHr = (size_t)s.B * s.Hr, BH = (size_t)s.B * s.H;
   BwdWs w;
   w.w = c.take<float>(BHr * s.nQ * s.topk);
-  w.Dbuf = c.take<float>(BH * s.nQ * kChunk * s.topk);
-  w.Lbuf = c.take<float>(BH * s.nQ * kChunk * s.topk);
+  w.Dbuf = c.take<float>(BH * s.nQ * s.Sq * s.topk);
+  w.Lbuf = c.take<float>(BH * s.nQ * s.Sq * s.topk);
   w.dwp = c.take<float>(BH * s.nQ * s.topk * 2);
   w.counts = c.take<int>(BHr * s.nKV);
   w.cursor = c.take<int>(BHr * s.nKV);

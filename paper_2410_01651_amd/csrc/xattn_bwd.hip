@@ -11,6 +11,13 @@
 // D_s equals rowsum(dO o O'_s) of Algorithm 2, computed here on chip from the
 // same tile, so the per-chunk outputs O'_s are never stored.
 //
+// With an LMK row per chunk (S + 1 query rows against S-row key chunks) the
+// 65th row takes the same steps as a vector against the tiles the waves hold:
+// in the query-stationary pass one wave per slot (alternating) forms its
+// scores, dP, D and dS with one key per lane and accumulates its dQ row, and
+// in the key-stationary pass every wave adds the row's rank-one terms to dV and
+// dK with one more, mostly zero, 16-deep MFMA step.
+//
 // No floating-point atomics: every output element is produced by exactly one
 // workgroup.  The key-stationary pass needs, for each chunk j, the list of
 // (row t, slot s) that retrieved it; an integer counting sort builds that list
@@ -47,6 +54,16 @@ struct BwdParams {
   int64_t nQ, nKV;
   int causal;
   float attn_scale;
+};
+
+// the LMK row's per-chunk exchange between the two waves of a dQ pair
+template <typename T>
+struct LmkShared {
+  T q[2][kD];      // the row's Q and dO, by chunk parity
+  T d[2][kD];
+  T p[2][kS];      // per wave: the current slot's dS (one per key)
+  float o[2][kD];  // per wave: its slots' share of the row's dQ
+  float dl[2][32]; // per slot: -D and the shifted lse of the row
 };
 
 // ------------------------------------------------------------ helpers ----
@@ -178,9 +195,12 @@ __global__ __launch_bounds__(256) void csr_sort_kernel(const int* __restrict__ o
 // STAGE (k <= kDqStageK): the per-(token, slot) values are staged in LDS and
 // stored once per chunk.
 constexpr int kDqStageK = 8;
-template <typename T, bool STAGE>
+template <typename T, bool STAGE, bool XR>
 __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p, int64_t nwork) {
   constexpr int TILE = kS * kD;
+  constexpr int SQ = XR ? kS + 1 : kS;  // query rows per chunk
+  static_assert(kPairs == 1, "the LMK row exchange assumes one pair per workgroup");
+  __shared__ __attribute__((aligned(16))) LmkShared<T> sX[1];  // used with XR only
   __shared__ __attribute__((aligned(16))) T ring[kPairs * 2 * 2 * TILE];  // pair p: slots 2p, 2p+1
   __shared__ int sJ[kPairs][2][32];     // [pair][chunk parity][slot]: chunk index or -1
   __shared__ int sSlot[kPairs][2][32];  // compacted valid slots: slot, chunk, weight
@@ -246,8 +266,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     }
     if (lane == 0) sN[pair][buf] = __popcll(mask);
   };
-  auto tok_of = [&](const Geo& g) -> int64_t { return ((g.b * p.H + g.h) * p.nQ + g.c) * kS; };
-  const int64_t lq_len = p.nQ * kS;  // query tokens per (batch, head)
+  auto tok_of = [&](const Geo& g) -> int64_t { return ((g.b * p.H + g.h) * p.nQ + g.c) * SQ; };
+  const int64_t lq_len = p.nQ * SQ;  // query tokens per (batch, head)
+  // the LMK row's Q and dO: 16-byte piece `lane` of each (lanes below kXPieces)
+  constexpr int kXPieces = kD * (int)sizeof(T) / 16;
+  u32x4 qxv{0u, 0u, 0u, 0u}, dxv{0u, 0u, 0u, 0u};
 
   // ---- prologue
   Frag<T> qf[4], df[4];  // the current chunk's Q and dO rows of this lane's query
@@ -265,6 +288,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     for (int kb = 0; kb < 4; ++kb) {
       qd[kb] = load_frag(qr + 16 * kb + 8 * hh);
       dd[kb] = load_frag(dr + 16 * kb + 8 * hh);
+    }
+    if (XR && half == 0 && lane < kXPieces) {
+      const int64_t xrow = (tok_of(g) + kS) * kD;
+      qxv = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.q) + xrow)[lane];
+      dxv = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.dout) + xrow)[lane];
     }
   };
   if (my_n > 0) {
@@ -290,11 +318,13 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
   float lw = sWc[pair][0][l32];
   int64_t kvb = uniform64(slice_of(g0)), kvb_n = 0;
   int cs = 0;
-  // this lane's saved lse of the next item to compute (loaded a round ahead)
-  float lse_next = 0.f;
+  // this lane's saved lse of the next item to compute (loaded a round ahead),
+  // and the LMK row's
+  float lse_next = 0.f, lsex_next = 0.f;
   if (my_n > 0 && sN[pair][0] > 0) {
     issue_item(kvb, __builtin_amdgcn_readlane(lj, 0), cs);
     lse_next = p.lse[(tok_of(g0) + qi) * K + __builtin_amdgcn_readlane(ls, 0)];
+    if (XR) lsex_next = p.lse[(tok_of(g0) + kS) * K + __builtin_amdgcn_readlane(ls, 0)];
   }
 
   constexpr bool kB16 = std::is_same<T, __bf16>::value;
@@ -318,10 +348,12 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
   // pre: this is the chunk's last item and a next chunk follows; its Q and dO rows
   // are loaded as soon as this item's products have read qf/df, so that the
   // next chunk's first round does not wait out the whole load
-  auto run = [&](int slot, int u, float lse_q, int64_t cbase, int64_t t, bool pre) __device__ {
+  float ox0 = 0.f, ox1 = 0.f;  // LMK row: this lane's partial dQ for d = l%32 and 32 + l%32
+  auto run = [&](int slot, int u, float lse_q, float lse_x, int64_t cbase, int64_t t, bool pre, int buf) __device__ {
     const uint32_t co = (uint32_t)slot * 2 * kTileB;
     const int s = __builtin_amdgcn_readlane(ls, u);
     const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lw), u));
+    const bool xr = XR && (u & 1) == half;  // this wave takes the LMK row of slot u
     const T* sK = ring + (2 * pair + slot) * (2 * TILE);
     const T* sV = sK + TILE;
     f32x16 s0 = zero16(), s1 = zero16(), p0 = zero16(), p1 = zero16();
@@ -388,8 +420,61 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         p.ws.Lbuf[cbase + s * lq_len + qi] = lsh;
       }
     }
-    // this wave's 32 queries' share of dw[t, s]
-    const float dsum = sum32(Dq);
+    // the LMK row: scores and dP with one key per lane (row fragments of K and V
+    // against the row's Q and dO, the two dimension halves added across l ^ 32),
+    // w P, D, dS, and its dQ against the K^T fragments
+    float Dx = 0.f;
+    if (xr) {
+      float a0 = 0.f, a1 = 0.f, b0 = 0.f, b1 = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
+        const Frag<T> xq = vec_frag(&sX[0].q[buf][0], 16 * kb + 8 * hh);
+        const Frag<T> xd = vec_frag(&sX[0].d[buf][0], 16 * kb + 8 * hh);
+        if constexpr (kB16) {
+          const lds_char* kp = lds0 + (kofs[kb] + co);
+          a0 = frag_dot(lds_b128_at(kp), xq, a0);
+          a1 = frag_dot(lds_b128_at(kp + 32 * kRowB), xq, a1);
+          b0 = frag_dot(lds_b128_at(kp + kTileB), xd, b0);
+          b1 = frag_dot(lds_b128_at(kp + (kTileB + 32 * kRowB)), xd, b1);
+        } else {
+          a0 = frag_dot(lds_frag(sK, lane & 31, 16 * kb + 8 * hh), xq, a0);
+          a1 = frag_dot(lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh), xq, a1);
+          b0 = frag_dot(lds_frag(sV, lane & 31, 16 * kb + 8 * hh), xd, b0);
+          b1 = frag_dot(lds_frag(sV, 32 + (lane & 31), 16 * kb + 8 * hh), xd, b1);
+        }
+      }
+      a0 = sum_xor32(a0);
+      a1 = sum_xor32(a1);
+      b0 = sum_xor32(b0);
+      b1 = sum_xor32(b1);
+      const float xs = hh ? a1 : a0, xdp = hh ? b1 : b0;  // key `lane`
+      const float offx = lse_x * kLog2e - __builtin_amdgcn_logf(wsf);
+      const float wpx = __builtin_amdgcn_exp2f(fmaf(xs, sc, -offx));
+      Dx = sum64(wpx * xdp) * __builtin_amdgcn_rcpf(wsf);
+      sX[0].p[half][lane] = (T)(wpx * (xdp - Dx));
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
+        Frag<T> k0, k1;
+        if constexpr (kB16) {
+          k0 = lds_tr2(lds0 + (tofs[0][0] + co) + 16 * kb * kRowB, lds0 + (tofs[0][1] + co) + 16 * kb * kRowB);
+          k1 = lds_tr2(lds0 + (tofs[1][0] + co) + 16 * kb * kRowB, lds0 + (tofs[1][1] + co) + 16 * kb * kRowB);
+        } else {
+          k0 = lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
+          k1 = lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
+        }
+        const Frag<T> xf = vec_frag_t(&sX[0].p[half][0], 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh);
+        ox0 = frag_dot(k0, xf, ox0);
+        ox1 = frag_dot(k1, xf, ox1);
+      }
+      if (lane == 0) {
+        sX[0].dl[0][s] = -Dx;
+        sX[0].dl[1][s] = lse_x * kLog2e - __builtin_amdgcn_logf(ws);
+      }
+    }
+    // this wave's 32 queries' share of dw[t, s] (and the LMK row's D)
+    const float dsum = sum32(Dq) + Dx;
     if (lane == 0) {
       if constexpr (STAGE) sDw[wave][s] = dsum;
       else p.ws.dwp[(t * K + s) * 2 + half] = dsum;
@@ -401,7 +486,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     const int buf = (int)(ci & 1);
     const int n = live ? sN[pair][buf] : 0;
     const int64_t tok0 = tok_of(g0);
-    const int64_t cbase = (g0.b * p.H + g0.h) * K * lq_len + g0.c * kS;
+    const int64_t cbase = (g0.b * p.H + g0.h) * K * lq_len + g0.c * SQ;
     const int64_t tglob = (g0.b * p.H + g0.h) * p.nQ + (p.causal ? g0.c - 1 : 0);  // dw row (b, h, t)
     const int64_t tok_n = tok_of(g1);
     for (int u = 0; u < K; ++u) {
@@ -414,6 +499,13 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
           lw = sWc[pair][buf][l32];
           kvb = kvb_n;
         }
+        // the LMK row's Q and dO for this chunk: written by the wave that takes
+        // slot 0 (its own reads follow in program order; the partner's first
+        // read is in round 1, after a barrier)
+        if (XR && half == 0 && live && lane < kXPieces) {
+          reinterpret_cast<u32x4*>(&sX[0].q[buf][0])[lane] = qxv;
+          reinterpret_cast<u32x4*>(&sX[0].d[buf][0])[lane] = dxv;
+        }
         if (live_next) {
           if (half == 0) make_slots(meta, buf ^ 1);
           if (ci + 2 < my_n) meta = load_meta(g2);
@@ -423,16 +515,18 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
       }
       const bool comp = u < n;
       const int is = comp ? cs ^ 1 : cs;
-      const float lse_q = lse_next;
+      const float lse_q = lse_next, lse_x = lsex_next;
       if (u + 1 < n) {
         issue_item(kvb, __builtin_amdgcn_readlane(lj, u + 1), is);
         lse_next = p.lse[(tok0 + qi) * K + __builtin_amdgcn_readlane(ls, u + 1)];
+        if (XR) lsex_next = p.lse[(tok0 + kS) * K + __builtin_amdgcn_readlane(ls, u + 1)];
       } else if (u == K - 1 && live_next && sN[pair][buf ^ 1] > 0) {
         issue_item(kvb_n, sJc[pair][buf ^ 1][0], is);
         lse_next = p.lse[(tok_n + qi) * K + sSlot[pair][buf ^ 1][0]];
+        if (XR) lsex_next = p.lse[(tok_n + kS) * K + sSlot[pair][buf ^ 1][0]];
       }
       if (comp) {
-        run(cs, u, lse_q, cbase, tglob, live_next && u == n - 1);
+        run(cs, u, lse_q, lse_x, cbase, tglob, live_next && u == n - 1, buf);
         cs ^= 1;
       }
       // a chunk without items loads the next chunk's Q and dO rows in its first round
@@ -451,6 +545,24 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
                as * g1a[4 * g + 3]);
       }
       const bool has_row = !p.causal || g0.c > 0;
+      if constexpr (XR) {
+        // the LMK row: add the two waves' shares of its dQ, store it and its
+        // per-slot -D and shifted lse
+        const float t0 = sum_xor32(ox0), t1 = sum_xor32(ox1);
+        sX[0].o[half][lane] = hh ? t1 : t0;  // lane l: d = l
+        block_barrier();
+        if (half == 0) {
+          const int64_t tx = tok0 + kS;
+          reinterpret_cast<T*>(p.dq)[tx * kD + lane] = (T)(as * (sX[0].o[0][lane] + sX[0].o[1][lane]));
+          if (lane < K && sJ[pair][buf][lane] >= 0) {
+            const int64_t o = cbase + lane * lq_len + kS;
+            p.ws.Dbuf[o] = sX[0].dl[0][lane];
+            p.ws.Lbuf[o] = sX[0].dl[1][lane];
+          }
+        }
+        ox0 = 0.f;
+        ox1 = 0.f;
+      }
       if constexpr (STAGE) {
         // this wave's staged values (its own LDS writes, read back in program
         // order): per valid slot one contiguous run of 32 tokens
@@ -486,11 +598,14 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
 // sums are exchanged.  With the shifted lse L = log2(e) lse - log2(w_s),
 // exp2(S log2(e) scale - L) is w_s P_s directly.
 constexpr int kKvThreads = 128;
-template <typename T>
+template <typename T, bool XR>
 __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, int64_t nwork) {
   constexpr int TILE = kS * kD;
-  // ring slot: Q_c tile, dO_c tile, shifted-lse column, D column
-  constexpr int ENTRY = 2 * TILE + 2 * kS * (int)(sizeof(float) / sizeof(T));
+  constexpr int SQ = XR ? kS + 1 : kS;  // query rows per chunk
+  // ring slot: Q_c tile, dO_c tile, shifted-lse column, D column; with the LMK
+  // row also its Q and dO rows and its shifted lse and -D (16 bytes)
+  constexpr int XOFF = 2 * TILE + 2 * kS * (int)(sizeof(float) / sizeof(T));
+  constexpr int ENTRY = XOFF + (XR ? 2 * kD + 16 / (int)sizeof(T) : 0);
   __shared__ __attribute__((aligned(16))) T ring[2 * ENTRY];
   constexpr int NE = 256;  // retrievers staged in LDS per batch
   __shared__ int sE[NE];
@@ -533,24 +648,34 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
     vf[kb] = load_frag(vrow + 16 * kb + 8 * hh);
   }
 
-  const T* qb = reinterpret_cast<const T*>(p.q) + bh * p.nQ * kS * kD;
-  const T* ob = reinterpret_cast<const T*>(p.dout) + bh * p.nQ * kS * kD;
-  const float* Lb = p.ws.Lbuf + bh * p.nQ * kS * K;
-  const float* Db = p.ws.Dbuf + bh * p.nQ * kS * K;
+  const int64_t lq_len = p.nQ * SQ;  // query tokens per (batch, head)
+  const T* qb = reinterpret_cast<const T*>(p.q) + bh * lq_len * kD;
+  const T* ob = reinterpret_cast<const T*>(p.dout) + bh * lq_len * kD;
+  const float* Lb = p.ws.Lbuf + bh * lq_len * K;
+  const float* Db = p.ws.Dbuf + bh * lq_len * K;
 
   const TileCopy<T, 2> cp(wave, lane);
   const uint32_t col_off = (uint32_t)(lane * sizeof(float));
-  const int64_t lq_len = p.nQ * kS;
+  constexpr int kXPieces = kD * (int)sizeof(T) / 16;  // 16-byte pieces of one row
   auto enc = [&](int e) { return ((e / K + p.causal) << 5) | (e % K); };  // list entry t*K+s -> (query chunk << 5) | slot
   auto issue = [&](int slot, int cs) __device__ {
     const int64_t c = cs >> 5;
     const int s = cs & 31;
     T* dst = ring + slot * ENTRY;
-    cp.issue(qb + c * TILE, dst);
-    cp.issue(ob + c * TILE, dst + TILE);
+    cp.issue(qb + c * SQ * kD, dst);
+    cp.issue(ob + c * SQ * kD, dst + TILE);
     float* cols = reinterpret_cast<float*>(dst + 2 * TILE);
-    if (wave == 0) dma_column_s(Lb + s * lq_len + c * kS, col_off, cols);
-    else dma_column_s(Db + s * lq_len + c * kS, col_off, cols + kS);
+    if (wave == 0) dma_column_s(Lb + s * lq_len + c * SQ, col_off, cols);
+    else dma_column_s(Db + s * lq_len + c * SQ, col_off, cols + kS);
+    if constexpr (XR) {
+      // the LMK row (row S of the chunk): wave 0 its Q row and shifted lse, wave 1
+      // its dO row and -D
+      const int64_t xr = c * SQ + kS;
+      T* xdst = dst + XOFF;
+      float* xcol = reinterpret_cast<float*>(xdst + 2 * kD);
+      if (lane < kXPieces) dma_row16((wave == 0 ? qb : ob) + xr * kD, lane * 16u, xdst + wave * kD);
+      if (lane == 0) dma_column_s((wave == 0 ? Lb : Db) + s * lq_len + xr, 0u, xcol + wave);
+    }
   };
 
   f32x16 dv0 = zero16(), dv1 = zero16(), dk0 = zero16(), dk1 = zero16();
@@ -646,6 +771,32 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
     frag_from_acc(ds[1], p0, 1, 1.f);
     frag_from_acc(ds[2], p1, 0, 1.f);
     frag_from_acc(ds[3], p1, 1, 1.f);
+    if constexpr (XR) {
+      // the LMK row against this wave's keys: its score and dP for key kr (row
+      // fragments of K and V held in registers, the dimension halves added
+      // across l ^ 32), w P and dS, then dV^T += dO_x^T (w P_x) and
+      // dK^T += q_x^T dS_x as one more contraction step whose only nonzero
+      // entry is the first
+      const T* sqx = sQ + XOFF;
+      const T* sdx = sqx + kD;
+      const float* slx = reinterpret_cast<const float*>(sdx + kD);
+      float a = 0.f, b = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
+        a = frag_dot(kf[kb], vec_frag(sqx, 16 * kb + 8 * hh), a);
+        b = frag_dot(vf[kb], vec_frag(sdx, 16 * kb + 8 * hh), b);
+      }
+      a = sum_xor32(a);
+      b = sum_xor32(b);
+      const float wpx = __builtin_amdgcn_exp2f(fmaf(a, sc, -slx[0]));
+      const bool e0 = hh == 0;
+      const Frag<T> bw = frag_e0<T>(e0 ? wpx : 0.f), bd = frag_e0<T>(e0 ? wpx * (b + slx[1]) : 0.f);
+      mma32(dv0, frag_e0<T>(e0 ? to_f32(sdx[lane & 31]) : 0.f), bw);
+      mma32(dv1, frag_e0<T>(e0 ? to_f32(sdx[32 + (lane & 31)]) : 0.f), bw);
+      mma32(dk0, frag_e0<T>(e0 ? to_f32(sqx[lane & 31]) : 0.f), bd);
+      mma32(dk1, frag_e0<T>(e0 ? to_f32(sqx[32 + (lane & 31)]) : 0.f), bd);
+    }
     // dV^T += dO^T (w P) and dK^T += Q^T dS  (contractions over the 64 queries)
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
@@ -941,13 +1092,18 @@ hipError_t launch_bwd_t(const Shape& s, BwdParams& p, float* dsel, const void* l
   // persistent: kWgPerCu workgroups per CU, kPairs chunk streams each
   const int64_t dq_wgs =
       std::min<int64_t>(round8((int64_t)device_cus() * kWgPerCu), round8((nq_work + kPairs - 1) / kPairs));
+  const bool xr = s.Sq != kS;  // LMK row per query chunk
+  auto dq = [&](auto kernel) {
+    launch_kernel("bwd_dq_kernel", kernel, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
+  };
   if (s.topk <= kDqStageK)
-    launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T, true>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p, nq_work);
+    xr ? dq(bwd_dq_kernel<T, true, true>) : dq(bwd_dq_kernel<T, true, false>);
   else
-    launch_kernel("bwd_dq_kernel", bwd_dq_kernel<T, false>, dim3((unsigned)dq_wgs), dim3(kThreads), 0, st, p,
-                  nq_work);
-  launch_kernel("bwd_dkdv_kernel", bwd_dkdv_kernel<T>, dim3((unsigned)round8(nk_work)), dim3(kKvThreads), 0, st, p,
-                nk_work);
+    xr ? dq(bwd_dq_kernel<T, false, true>) : dq(bwd_dq_kernel<T, false, false>);
+  auto kv = [&](auto kernel) {
+    launch_kernel("bwd_dkdv_kernel", kernel, dim3((unsigned)round8(nk_work)), dim3(kKvThreads), 0, st, p, nk_work);
+  };
+  xr ? kv(bwd_dkdv_kernel<T, true>) : kv(bwd_dkdv_kernel<T, false>);
   if (dlmk_q) {
     // dsel is formed inside the landmark-query gradient kernel
     launch_kernel("dlmk_q_kernel", dlmk_q_kernel<T>, dim3((unsigned)(BHr * s.nQ)), dim3(256), 0, st, (const T*)lmk_k,

@@ -19,6 +19,12 @@
 // lane (query = accumulator column): the softmax needs one cross-lane step, and
 // the probability tile feeds the PV product straight from registers.  V^T
 // fragments come from the row-major V tile through LDS transpose reads.
+//
+// With an LMK row per chunk (S + 1 query rows), the 65th row meets the same
+// tiles: one wave per slot (the waves alternate) takes it as a vector against
+// the K and V^T fragments it already holds, with one key per lane for the
+// softmax, and the waves' partial outputs are added through LDS at the end of
+// the chunk.
 #include "gca_device.hpp"
 #include "gca_launch.hpp"
 
@@ -48,6 +54,15 @@ struct FwdParams {
   float attn_scale;
 };
 
+// the LMK row's per-chunk exchange between the two waves of a pair
+template <typename T>
+struct LmkShared {
+  T q[2][kD];       // the row's queries, by chunk parity
+  T p[2][kS];       // per wave: the current slot's weighted probabilities (one per key)
+  float o[2][kD];   // per wave: its slots' share of the row's output
+  float lse[32];    // per slot: the row's log-sum-exp
+};
+
 // Per-lane retrieval metadata of one landmark row: lane s < K holds slot s's
 // chunk index and raw score (chunk -1 for lanes >= K or rows that do not exist).
 struct RowMeta {
@@ -65,9 +80,12 @@ __device__ __forceinline__ RowMeta load_row_meta(const FwdParams& p, int64_t row
   return m;
 }
 
-template <typename T, bool OBO>
+template <typename T, bool OBO, bool XR>
 __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams p) {
   constexpr int TILE = kS * kD;
+  constexpr int SQ = XR ? kS + 1 : kS;  // query rows per chunk
+  static_assert(kPairs == 1, "the LMK row exchange assumes one pair per workgroup");
+  __shared__ __attribute__((aligned(16))) LmkShared<T> sX[1];  // used with XR only
   __shared__ __attribute__((aligned(16))) T ring[kPairs * 2 * 2 * TILE];  // pair p: slots 2p, 2p+1 (K and V tiles)
   __shared__ int sJ[kPairs][2][32];     // [pair][chunk parity][slot]: chunk index or -1
   __shared__ int sSlot[kPairs][2][32];  // compacted lists of the valid slots: slot, chunk, weight
@@ -139,7 +157,14 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     if (p.w && exists && owner && lane < K) p.w[row_off + lane] = wv;
   };
   auto qrow_ptr = [&](int64_t w) __device__ {
-    return reinterpret_cast<const T*>(p.q) + (w * kS + qi) * kD;
+    return reinterpret_cast<const T*>(p.q) + (w * SQ + qi) * kD;
+  };
+  // the LMK row's queries: 16-byte piece `lane` (lanes below kD / 16-byte pieces)
+  constexpr int kXPieces = kD * (int)sizeof(T) / 16;
+  u32x4 qxv{0u, 0u, 0u, 0u};
+  auto load_qx = [&](int64_t w) __device__ {
+    if (lane < kXPieces)
+      qxv = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.q) + (w * SQ + kS) * kD)[lane];
   };
 
   // ---- prologue: the first chunk's slot list and Q, the second chunk's metadata
@@ -158,6 +183,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     const T* qr = qrow_ptr(c_begin);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qr + 16 * kb + 8 * hh);
+    if (XR && half == 0) load_qx(c_begin);
     if (half == 0) make_slots(m0, g0, 0);
     if (my_n > 1) {
       row_of(g1, ro, ex, ow);
@@ -210,9 +236,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
 
   // one retrieved chunk (item u of the current chunk, tokens from tok0) against
   // this wave's 32 queries; its tiles are in the pair's ring slot `slot`
-  auto compute = [&](int slot, int u, int64_t tok0, f32x16& o0, f32x16& o1) __device__ {
+  float ox0 = 0.f, ox1 = 0.f;  // LMK row: this lane's partial outputs for d = l%32 and 32 + l%32
+  auto compute = [&](int slot, int u, int64_t tok0, int buf, f32x16& o0, f32x16& o1) __device__ {
     const uint32_t co = (uint32_t)slot * 2 * kTileB;
     const int s = __builtin_amdgcn_readlane(ls, u);
+    const bool xr = XR && (u & 1) == half;  // this wave takes the LMK row of slot u
     const T* sK = ring + (2 * pair + slot) * (2 * TILE);
     const T* sV = sK + TILE;
     // all K fragments first, so the eight products issue back to back
@@ -233,6 +261,21 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     for (int kb = 0; kb < 4; ++kb) {
       mma32(st0, ka[2 * kb], qf[kb]);
       mma32(st1, ka[2 * kb + 1], qf[kb]);
+    }
+    // LMK row scores while the products run: lane l holds keys l%32 and 32 + l%32
+    // over its half of the dimensions; the halves are added across l ^ 32
+    float xs = 0.f;
+    if (xr) {
+      float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const Frag<T> xf = vec_frag(&sX[0].q[buf][0], 16 * kb + 8 * hh);
+        a0 = frag_dot(ka[2 * kb], xf, a0);
+        a1 = frag_dot(ka[2 * kb + 1], xf, a1);
+      }
+      a0 = sum_xor32(a0);
+      a1 = sum_xor32(a1);
+      xs = hh ? a1 : a0;  // the score of key `lane`
     }
     // V^T fragments are read while the softmax runs
     Frag<T> va[8];
@@ -271,6 +314,16 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     }
     const int coef_bits = __builtin_amdgcn_readlane(__float_as_int(lw), u);
     const float coef = __int_as_float(coef_bits) * __builtin_amdgcn_rcpf(sum);
+    if (xr) {
+      // the LMK row's softmax over the chunk's 64 keys, one key per lane
+      float xm = max64(xs) * sc;
+      if (OBO) xm = fmaxf(xm, 0.f);
+      const float xe = __builtin_amdgcn_exp2f(fmaf(xs, sc, -xm));
+      float xsum = sum64(xe);
+      if (OBO) xsum += __builtin_amdgcn_exp2f(-xm);
+      if (lane == 0) sX[0].lse[s] = (xm + __builtin_amdgcn_logf(xsum)) * kLn2;
+      sX[0].p[half][lane] = (T)(xe * (__int_as_float(coef_bits) * __builtin_amdgcn_rcpf(xsum)));
+    }
     Frag<T> pf[4];
     frag_from_acc(pf[0], st0, 0, coef);
     frag_from_acc(pf[1], st0, 1, coef);
@@ -280,6 +333,26 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     for (int kb = 0; kb < 4; ++kb) {
       mma32(o0, va[2 * kb], pf[kb]);
       mma32(o1, va[2 * kb + 1], pf[kb]);
+    }
+    if (xr) {
+      // LMK row output: (w P) V against the V^T fragments, read again now that
+      // the products have taken theirs (this wave's own probability writes are
+      // read back in program order)
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
+        Frag<T> v0, v1;
+        if constexpr (kB16) {
+          v0 = lds_tr2(lds0 + (vofs[0][0] + co) + 16 * kb * kRowB, lds0 + (vofs[0][1] + co) + 16 * kb * kRowB);
+          v1 = lds_tr2(lds0 + (vofs[1][0] + co) + 16 * kb * kRowB, lds0 + (vofs[1][1] + co) + 16 * kb * kRowB);
+        } else {
+          v0 = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
+          v1 = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
+        }
+        const Frag<T> xf = vec_frag_t(&sX[0].p[half][0], 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh);
+        ox0 = frag_dot(v0, xf, ox0);
+        ox1 = frag_dot(v1, xf, ox1);
+      }
     }
   };
 
@@ -294,23 +367,34 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     const int buf = (int)(ci & 1);
     const int n = live ? sN[pair][buf] : 0;
     const int64_t w = c_begin + ci * stride;
-    const int64_t tok0 = w * kS;
+    const int64_t tok0 = w * SQ;
     for (int u = 0; u < K; ++u) {
       wait_vmem<0>();
       block_barrier();
       if (u == 0) {
-        if (ci > 0 && live) {
+        if (!XR && ci > 0 && live) {
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb) qf[kb] = qn[kb];
+        }
+        if (ci > 0 && live) {
           ls = sSlot[pair][buf][l32];
           lj = sJc[pair][buf][l32];
           lw = sWc[pair][buf][l32];
           kvb = kvb_n;
         }
+        // the LMK row's queries for this chunk: written by the wave that takes
+        // slot 0 (its own reads follow in program order; the partner's first
+        // read is in round 1, after a barrier)
+        if (XR && half == 0 && live && lane < kXPieces)
+          reinterpret_cast<u32x4*>(&sX[0].q[buf][0])[lane] = qxv;
         if (live_next) {
-          const T* qr = qrow_ptr(w + stride);
+          if constexpr (!XR) {
+            const T* qr = qrow_ptr(w + stride);
 #pragma unroll
-          for (int kb = 0; kb < 4; ++kb) qn[kb] = load_frag(qr + 16 * kb + 8 * hh);
+            for (int kb = 0; kb < 4; ++kb) qn[kb] = load_frag(qr + 16 * kb + 8 * hh);
+          } else if (half == 0) {
+            load_qx(w + stride);
+          }
           if (half == 0) make_slots(meta, g1, buf ^ 1);
           if (ci + 2 < my_n) {
             int64_t ro;
@@ -330,9 +414,17 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
         issue_item(kvb_n, sJc[pair][buf ^ 1][0], is);
       }
       if (comp) {
-        compute(cs, u, tok0, o0, o1);
+        compute(cs, u, tok0, buf, o0, o1);
         cs ^= 1;
       }
+    }
+    // with the LMK row the next chunk's Q rows are loaded only now, straight into
+    // the fragments (the registers of a prefetch are what the row's own work
+    // needs); the next round's wait covers them
+    if (XR && live_next) {
+      const T* qr = qrow_ptr(w + stride);
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qr + 16 * kb + 8 * hh);
     }
 
     // ---- finish the chunk: each wave stores its 32 query rows
@@ -355,6 +447,20 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
         float* lse = p.lse + (tok0 + qi) * K;
         for (int s = 0; s < K; ++s)
           if (sJ[pair][buf][s] < 0) lse[s] = -INFINITY;
+      }
+      if constexpr (XR) {
+        // the LMK row: add the two waves' shares (each lane first adds its key
+        // half to the partner lane's), then one wave stores the row and its lse
+        const float t0 = sum_xor32(ox0), t1 = sum_xor32(ox1);
+        sX[0].o[half][lane] = hh ? t1 : t0;  // lane l: d = l
+        block_barrier();
+        if (half == 0) {
+          const int64_t tx = tok0 + kS;
+          reinterpret_cast<T*>(p.out)[tx * kD + lane] = (T)(sX[0].o[0][lane] + sX[0].o[1][lane]);
+          if (p.lse && lane < K) p.lse[tx * K + lane] = sJ[pair][buf][lane] < 0 ? -INFINITY : sX[0].lse[lane];
+        }
+        ox0 = 0.f;
+        ox1 = 0.f;
       }
       // the causal last row feeds no chunk: its weights go out with chunk 0
       if (p.w && p.causal && g0.c == 0 && half == 1) {
@@ -393,24 +499,18 @@ hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const 
   p.nwork = (int64_t)s.B * s.H * s.nQ;
   p.causal = s.causal;
   p.attn_scale = s.attn_scale;
+  const bool xr = s.Sq != kS;
   // persistent workgroups: kWgPerCu per CU, a multiple of 8 (one share per XCD),
   // each running kPairs chunk streams
   const int64_t target = round8((int64_t)device_cus() * kWgPerCu), wgs = (p.nwork + kPairs - 1) / kPairs;
   const dim3 grid((unsigned)(wgs < target ? round8(wgs) : target)), block(kThreads);
+  auto go = [&](auto kernel) { launch_kernel("xattn_fwd_kernel", kernel, grid, block, 0, stream, p); };
   if (s.bf16) {
-    if (s.off_by_one) {
-      launch_kernel("xattn_fwd_kernel", xattn_fwd_kernel<__bf16, true>, grid, block, 0, stream, p);
-    }
-    else {
-      launch_kernel("xattn_fwd_kernel", xattn_fwd_kernel<__bf16, false>, grid, block, 0, stream, p);
-    }
+    if (xr) s.off_by_one ? go(xattn_fwd_kernel<__bf16, true, true>) : go(xattn_fwd_kernel<__bf16, false, true>);
+    else s.off_by_one ? go(xattn_fwd_kernel<__bf16, true, false>) : go(xattn_fwd_kernel<__bf16, false, false>);
   } else {
-    if (s.off_by_one) {
-      launch_kernel("xattn_fwd_kernel", xattn_fwd_kernel<float, true>, grid, block, 0, stream, p);
-    }
-    else {
-      launch_kernel("xattn_fwd_kernel", xattn_fwd_kernel<float, false>, grid, block, 0, stream, p);
-    }
+    if (xr) s.off_by_one ? go(xattn_fwd_kernel<float, true, true>) : go(xattn_fwd_kernel<float, false, true>);
+    else s.off_by_one ? go(xattn_fwd_kernel<float, true, false>) : go(xattn_fwd_kernel<float, false, false>);
   }
   return take_launch_error();
 }

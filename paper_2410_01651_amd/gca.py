@@ -32,7 +32,7 @@ EXPORTS = (
 GCA_OK, GCA_ERR_INVALID, GCA_ERR_UNSUPPORTED, GCA_ERR_WORKSPACE, GCA_ERR_HIP = range(5)
 GCA_FP32, GCA_BF16 = 0, 1
 GCA_CAUSAL, GCA_DECODE = 0, 1
-FLAG_FUSED_TOPK, FLAG_MATERIALIZE, FLAG_GUMBEL, FLAG_HOST_KV = 1, 2, 4, 8
+FLAG_FUSED_TOPK, FLAG_MATERIALIZE, FLAG_GUMBEL, FLAG_HOST_KV, FLAG_LMK_ROW = 1, 2, 4, 8, 16
 OP_FORWARD, OP_BACKWARD = 0, 1
 NOALLOC_SCRATCH_BYTES = 16 << 20
 
@@ -61,6 +61,11 @@ class Problem(ctypes.Structure):
     @property
     def n_query_chunks(self) -> int:
         return self.n_chunks if self.mode == GCA_CAUSAL else 1
+
+    @property
+    def query_rows(self) -> int:
+        """Query rows per chunk: S, or S + 1 with the LMK row (GCA_FLAG_LMK_ROW)."""
+        return self.S + 1 if self.flags & FLAG_LMK_ROW else self.S
 
 
 class GcaError(RuntimeError):
@@ -117,12 +122,16 @@ def _check(status: int) -> None:
 
 
 def problem(B, H, n_chunks, topk, D=None, Hr=1, d=64, S=64, score_scale=None, attn_scale=None,
-            off_by_one=False, dtype="bf16", mode="causal", flags=0, gumbel_seed=None) -> Problem:
+            off_by_one=False, dtype="bf16", mode="causal", flags=0, gumbel_seed=None,
+            lmk_row=False) -> Problem:
     """Build a ``gca_problem``; D defaults to H*d, scales to 1/sqrt(D) and 1/sqrt(d).
-    A ``gumbel_seed`` turns on Gumbel top-k selection (GCA_FLAG_GUMBEL)."""
+    A ``gumbel_seed`` turns on Gumbel top-k selection (GCA_FLAG_GUMBEL);
+    ``lmk_row`` gives every query chunk S + 1 rows (GCA_FLAG_LMK_ROW)."""
     D = H * d if D is None else D
     if gumbel_seed is not None:
         flags |= FLAG_GUMBEL
+    if lmk_row:
+        flags |= FLAG_LMK_ROW
     return Problem(
         B=B, H=H, d=d, S=S, n_chunks=n_chunks, topk=topk, Hr=Hr, D=D,
         score_scale=1.0 / math.sqrt(D) if score_scale is None else score_scale,
@@ -201,9 +210,9 @@ def shapes(p: Problem) -> Shapes:
     nQ, nC = p.n_query_chunks, p.n_chunks
     return Shapes(
         lmk_q=(p.B, p.Hr, nQ, p.D), lmk_k=(p.B, p.Hr, nC, p.D),
-        q=(p.B, p.H, nQ * p.S, p.d), kv=(p.B, p.H, nC * p.S, p.d),
+        q=(p.B, p.H, nQ * p.query_rows, p.d), kv=(p.B, p.H, nC * p.S, p.d),
         rows=(p.B, p.Hr, nQ, p.topk), scores=(p.B, p.Hr, nQ, nC),
-        lse=(p.B, p.H, nQ * p.S, p.topk),
+        lse=(p.B, p.H, nQ * p.query_rows, p.topk),
     )
 
 

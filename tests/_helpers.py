@@ -54,13 +54,13 @@ def _gumbel(w):
 
 def oracle_params(w, off_by_one=False):
     return dict(S=w.S, topk=w.topk, score_scale=w.score_scale, attn_scale=w.attn_scale,
-                mode=w.mode, off_by_one=off_by_one, gumbel_seed=_gumbel(w))
+                mode=w.mode, off_by_one=off_by_one, gumbel_seed=_gumbel(w), Sq=w.Sq)
 
 
 def problem_for(w, off_by_one=False, flags=0):
     from paper_2410_01651_amd import gca
     return gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode,
-                       off_by_one=off_by_one, flags=flags, gumbel_seed=_gumbel(w))
+                       off_by_one=off_by_one, flags=flags, gumbel_seed=_gumbel(w), lmk_row=w.lmk_row)
 
 
 def upload(w, inp, dev):

@@ -89,7 +89,7 @@ def _fwd_call(gca, p, **override):
     ("d", 32, "UNSUPPORTED"), ("S", 128, "UNSUPPORTED"), ("topk", 0, "INVALID"),
     ("topk", 33, "UNSUPPORTED"), ("Hr", 3, "INVALID"), ("D", 96, "UNSUPPORTED"), ("D", 0, "INVALID"),
     ("n_chunks", 0, "INVALID"), ("B", 0, "INVALID"), ("dtype", 5, "INVALID"), ("mode", 2, "INVALID"),
-    ("off_by_one", 2, "INVALID"), ("flags", 3, "INVALID"), ("flags", 8, "INVALID"), ("flags", 16, "INVALID"),
+    ("off_by_one", 2, "INVALID"), ("flags", 3, "INVALID"), ("flags", 8, "INVALID"), ("flags", 32, "INVALID"),
     ("attn_scale", math.inf, "INVALID"),
 ])
 def test_invalid_problem_rejected(gca, field, value, status):
@@ -145,6 +145,21 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(g, "_lib", None)
     with pytest.raises(RuntimeError, match="not built"):
         g.lib()
+
+
+def test_lmk_row_rules(gca):
+    """S+1 query rows (GCA_FLAG_LMK_ROW) are a CAUSAL option; the backward workspace
+    holds per-(token, slot) values for the S+1 rows."""
+    dec = gca.problem(1, 2, 64, 8, mode="decode", lmk_row=True)
+    st, msg = _fwd_call(gca, dec, ws=FAKE, nbytes=1 << 20)
+    assert st == gca.GCA_ERR_UNSUPPORTED and "CAUSAL" in msg
+    assert gca.workspace_size(dec, gca.OP_FORWARD) == 0
+    p, px = gca.problem(2, 16, 1024, 8), gca.problem(2, 16, 1024, 8, lmk_row=True)
+    assert px.query_rows == 65 and gca.shapes(px).q == (2, 16, 1024 * 65, 64)
+    assert gca.shapes(px).lse == (2, 16, 1024 * 65, 8) and gca.shapes(px).kv == gca.shapes(p).kv
+    extra = gca.workspace_size(px, gca.OP_BACKWARD) - gca.workspace_size(p, gca.OP_BACKWARD)
+    assert 2 * 4 * 2 * 16 * 1024 * 8 <= extra < 2 * 4 * 2 * 16 * 1024 * 8 + 4096   # D and L of the LMK rows
+    assert gca.workspace_size(px, gca.OP_FORWARD) == gca.workspace_size(p, gca.OP_FORWARD)
 
 
 def test_host_kv_rules(gca):

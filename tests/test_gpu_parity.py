@@ -450,6 +450,42 @@ def test_selection_reused_by_layers(dev):
             assert max_abs_rel(host64(g[key]), r) <= TOL[w.dtype], (layer, key)
 
 
+LMK = [
+    # (workload, overrides, off_by_one): S+1 query rows per chunk (the LMK row)
+    ("train_16k_bf16", dict(B=2, H=3, n_chunks=70, topk=5), False),
+    ("train_16k_bf16", dict(B=2, H=3, n_chunks=70, topk=5, dtype="fp32"), False),
+    ("train_16k_bf16", dict(B=1, H=4, n_chunks=40, topk=8), True),
+    ("train_16k_bf16", dict(B=1, H=2, n_chunks=50, topk=12, Hr=2, D=128), False),  # k > 8, per-head retrieval
+    ("train_16k_bf16", dict(B=1, H=2, n_chunks=20, topk=1), False),
+    ("fwdbwd_64k_bf16", dict(B=1, H=4, n_chunks=96, topk=8), False),
+]
+
+
+@pytest.mark.parametrize("name,kw,obo", LMK)
+def test_lmk_rows_forward_backward(dev, name, kw, obo):
+    """S+1 query rows per chunk (GCA_FLAG_LMK_ROW): out, lse, w and every gradient
+    against the oracle; the LMK rows of chunks >= 2 are really attended."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case(name, lmk_row=True, **kw)
+    assert w.Sq == w.S + 1
+    if "dout" not in inp:
+        inp["dout"] = gi.draw_slices(w, "dout", (w.B, w.H, w.Lq, w.d))
+    t = upload(w, inp, dev)
+    p = problem_for(w, off_by_one=obo)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    assert tuple(f["out"].shape) == (w.B, w.H, w.n_chunks * (w.S + 1), w.d)
+    ref = _check_forward(w, inp, f, off_by_one=obo)
+    lmk_out = host64(f["out"]).reshape(w.B, w.H, w.n_chunks, w.S + 1, w.d)[:, :, :, w.S]
+    assert np.all(lmk_out[:, :, :2] == 0.0) and np.abs(lmk_out[:, :, 2:]).min(axis=-1).max() > 0.0
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                              t["lmk_q"], t["lmk_k"])
+    x = decode_all(w, inp)
+    rb = og.backward(oracle_params(w, obo), ref, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"], x["dout"])
+    for key in ("dq", "dk", "dv", "dsel", "dlmk_q", "dlmk_k"):
+        e = max_abs_rel(host64(g[key]), rb[key])
+        assert e <= TOL[w.dtype], (key, e)
+
+
 def test_profile_hook(dev):
     """The per-kernel timing hook: kernels are timed in launch order up to the
     capacity, named, with positive durations, and the results do not change."""
