@@ -268,9 +268,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
   };
   auto tok_of = [&](const Geo& g) -> int64_t { return ((g.b * p.H + g.h) * p.nQ + g.c) * SQ; };
   const int64_t lq_len = p.nQ * SQ;  // query tokens per (batch, head)
-  // the LMK row's Q and dO: 16-byte piece `lane` of each (lanes below kXPieces)
+  // the LMK row's Q and dO rows: copied straight into LDS (wave 0 the Q row, wave
+  // 1 the dO row, one 16-byte piece per lane below kXPieces) with the chunk's
+  // Q/dO fragment loads; visible to both waves after the next wait and barrier
   constexpr int kXPieces = kD * (int)sizeof(T) / 16;
-  u32x4 qxv{0u, 0u, 0u, 0u}, dxv{0u, 0u, 0u, 0u};
+  const int xh = __builtin_amdgcn_readfirstlane(half);  // the wave's half, in a scalar register
 
   // ---- prologue
   Frag<T> qf[4], df[4];  // the current chunk's Q and dO rows of this lane's query
@@ -280,7 +282,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
   g1.next(p.nQ, p.H, stride);
   Geo g2 = g1;
   g2.next(p.nQ, p.H, stride);
-  auto load_qdo = [&](const Geo& g, Frag<T>* qd, Frag<T>* dd) __device__ {
+  auto load_qdo = [&](const Geo& g, Frag<T>* qd, Frag<T>* dd, int xbuf) __device__ {
     const int64_t row = tok_of(g) + qi;
     const T* qr = reinterpret_cast<const T*>(p.q) + row * kD;
     const T* dr = reinterpret_cast<const T*>(p.dout) + row * kD;
@@ -289,15 +291,15 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
       qd[kb] = load_frag(qr + 16 * kb + 8 * hh);
       dd[kb] = load_frag(dr + 16 * kb + 8 * hh);
     }
-    if (XR && half == 0 && lane < kXPieces) {
+    if (XR && lane < kXPieces) {
       const int64_t xrow = (tok_of(g) + kS) * kD;
-      qxv = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.q) + xrow)[lane];
-      dxv = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.dout) + xrow)[lane];
+      const T* src = reinterpret_cast<const T*>(xh == 0 ? p.q : p.dout) + xrow;
+      dma_row16(src, lane * 16u, xh == 0 ? &sX[0].q[xbuf][0] : &sX[0].d[xbuf][0]);
     }
   };
   if (my_n > 0) {
     const Meta m0 = load_meta(g0);
-    load_qdo(g0, qf, df);
+    load_qdo(g0, qf, df, 0);
     if (half == 0) make_slots(m0, 0);
     if (my_n > 1) meta = load_meta(g1);
   }
@@ -353,9 +355,70 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     const uint32_t co = (uint32_t)slot * 2 * kTileB;
     const int s = __builtin_amdgcn_readlane(ls, u);
     const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lw), u));
-    const bool xr = XR && (u & 1) == half;  // this wave takes the LMK row of slot u
+    const bool xr = XR && (u & 1) == xh;  // this wave takes the LMK row of slot u
     const T* sK = ring + (2 * pair + slot) * (2 * TILE);
     const T* sV = sK + TILE;
+    // the LMK row: scores and dP with one key per lane (row fragments of K and V
+    // against the row's Q and dO, the two dimension halves added across l ^ 32),
+    // w P, D, dS, and its dQ against the K^T fragments
+    float Dx = 0.f;
+    if (xr) {
+      __builtin_amdgcn_sched_barrier(0);  // the row's reads start after the tile's products
+      float a0 = 0.f, a1 = 0.f, b0 = 0.f, b1 = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 8; ++kb) {
+        __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
+        const int kk = kb & 3;
+        const bool vt = kb >= 4;  // blocks 0-3: K against the row's Q; 4-7: V against its dO
+        const Frag<T> xv = vec_frag(vt ? &sX[0].d[buf][0] : &sX[0].q[buf][0], 16 * kk + 8 * hh);
+        Frag<T> r0, r1;
+        if constexpr (kB16) {
+          const lds_char* kp = lds0 + (kofs[kk] + co) + (vt ? kTileB : 0u);
+          r0 = lds_b128_at(kp);
+          r1 = lds_b128_at(kp + 32 * kRowB);
+        } else {
+          r0 = lds_frag(vt ? sV : sK, lane & 31, 16 * kk + 8 * hh);
+          r1 = lds_frag(vt ? sV : sK, 32 + (lane & 31), 16 * kk + 8 * hh);
+        }
+        if (vt) {
+          b0 = frag_dot(r0, xv, b0);
+          b1 = frag_dot(r1, xv, b1);
+        } else {
+          a0 = frag_dot(r0, xv, a0);
+          a1 = frag_dot(r1, xv, a1);
+        }
+      }
+      a0 = sum_xor32(a0);
+      a1 = sum_xor32(a1);
+      b0 = sum_xor32(b0);
+      b1 = sum_xor32(b1);
+      const float xs = hh ? a1 : a0, xdp = hh ? b1 : b0;  // key `lane`
+      const float wsf = fmaxf(ws, 1e-30f);
+      const float offx = lse_x * kLog2e - __builtin_amdgcn_logf(wsf);
+      const float wpx = __builtin_amdgcn_exp2f(fmaf(xs, sc, -offx));
+      Dx = sum64(wpx * xdp) * __builtin_amdgcn_rcpf(wsf);
+      sX[0].p[xh][lane] = (T)(wpx * (xdp - Dx));
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
+        Frag<T> k0, k1;
+        if constexpr (kB16) {
+          k0 = lds_tr2(lds0 + (tofs[0][0] + co) + 16 * kb * kRowB, lds0 + (tofs[0][1] + co) + 16 * kb * kRowB);
+          k1 = lds_tr2(lds0 + (tofs[1][0] + co) + 16 * kb * kRowB, lds0 + (tofs[1][1] + co) + 16 * kb * kRowB);
+        } else {
+          k0 = lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
+          k1 = lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
+        }
+        const Frag<T> xf = vec_frag_t(&sX[0].p[xh][0], 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh);
+        ox0 = frag_dot(k0, xf, ox0);
+        ox1 = frag_dot(k1, xf, ox1);
+      }
+      if (lane == 0) {
+        sX[0].dl[0][s] = -Dx;
+        sX[0].dl[1][s] = lse_x * kLog2e - __builtin_amdgcn_logf(ws);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // the tile's own products start after the row's
+    }
     f32x16 s0 = zero16(), s1 = zero16(), p0 = zero16(), p1 = zero16();
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
@@ -372,7 +435,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         mma32(p1, lds_frag(sV, 32 + (lane & 31), 16 * kb + 8 * hh), df[kb]);
       }
     }
-    if (pre) load_qdo(g1, qf, df);
+    if (pre) load_qdo(g1, qf, df, buf ^ 1);
     // w P^T (the weight folded into the exponent: wsf = max(ws, 1e-30) keeps the
     // shift finite), D = rowsum(P o dP) for this lane's query, w dS
     const float wsf = fmaxf(ws, 1e-30f);
@@ -420,59 +483,6 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         p.ws.Lbuf[cbase + s * lq_len + qi] = lsh;
       }
     }
-    // the LMK row: scores and dP with one key per lane (row fragments of K and V
-    // against the row's Q and dO, the two dimension halves added across l ^ 32),
-    // w P, D, dS, and its dQ against the K^T fragments
-    float Dx = 0.f;
-    if (xr) {
-      float a0 = 0.f, a1 = 0.f, b0 = 0.f, b1 = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
-        const Frag<T> xq = vec_frag(&sX[0].q[buf][0], 16 * kb + 8 * hh);
-        const Frag<T> xd = vec_frag(&sX[0].d[buf][0], 16 * kb + 8 * hh);
-        if constexpr (kB16) {
-          const lds_char* kp = lds0 + (kofs[kb] + co);
-          a0 = frag_dot(lds_b128_at(kp), xq, a0);
-          a1 = frag_dot(lds_b128_at(kp + 32 * kRowB), xq, a1);
-          b0 = frag_dot(lds_b128_at(kp + kTileB), xd, b0);
-          b1 = frag_dot(lds_b128_at(kp + (kTileB + 32 * kRowB)), xd, b1);
-        } else {
-          a0 = frag_dot(lds_frag(sK, lane & 31, 16 * kb + 8 * hh), xq, a0);
-          a1 = frag_dot(lds_frag(sK, 32 + (lane & 31), 16 * kb + 8 * hh), xq, a1);
-          b0 = frag_dot(lds_frag(sV, lane & 31, 16 * kb + 8 * hh), xd, b0);
-          b1 = frag_dot(lds_frag(sV, 32 + (lane & 31), 16 * kb + 8 * hh), xd, b1);
-        }
-      }
-      a0 = sum_xor32(a0);
-      a1 = sum_xor32(a1);
-      b0 = sum_xor32(b0);
-      b1 = sum_xor32(b1);
-      const float xs = hh ? a1 : a0, xdp = hh ? b1 : b0;  // key `lane`
-      const float offx = lse_x * kLog2e - __builtin_amdgcn_logf(wsf);
-      const float wpx = __builtin_amdgcn_exp2f(fmaf(xs, sc, -offx));
-      Dx = sum64(wpx * xdp) * __builtin_amdgcn_rcpf(wsf);
-      sX[0].p[half][lane] = (T)(wpx * (xdp - Dx));
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
-        Frag<T> k0, k1;
-        if constexpr (kB16) {
-          k0 = lds_tr2(lds0 + (tofs[0][0] + co) + 16 * kb * kRowB, lds0 + (tofs[0][1] + co) + 16 * kb * kRowB);
-          k1 = lds_tr2(lds0 + (tofs[1][0] + co) + 16 * kb * kRowB, lds0 + (tofs[1][1] + co) + 16 * kb * kRowB);
-        } else {
-          k0 = lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
-          k1 = lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
-        }
-        const Frag<T> xf = vec_frag_t(&sX[0].p[half][0], 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh);
-        ox0 = frag_dot(k0, xf, ox0);
-        ox1 = frag_dot(k1, xf, ox1);
-      }
-      if (lane == 0) {
-        sX[0].dl[0][s] = -Dx;
-        sX[0].dl[1][s] = lse_x * kLog2e - __builtin_amdgcn_logf(ws);
-      }
-    }
     // this wave's 32 queries' share of dw[t, s] (and the LMK row's D)
     const float dsum = sum32(Dq) + Dx;
     if (lane == 0) {
@@ -499,13 +509,6 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
           lw = sWc[pair][buf][l32];
           kvb = kvb_n;
         }
-        // the LMK row's Q and dO for this chunk: written by the wave that takes
-        // slot 0 (its own reads follow in program order; the partner's first
-        // read is in round 1, after a barrier)
-        if (XR && half == 0 && live && lane < kXPieces) {
-          reinterpret_cast<u32x4*>(&sX[0].q[buf][0])[lane] = qxv;
-          reinterpret_cast<u32x4*>(&sX[0].d[buf][0])[lane] = dxv;
-        }
         if (live_next) {
           if (half == 0) make_slots(meta, buf ^ 1);
           if (ci + 2 < my_n) meta = load_meta(g2);
@@ -530,7 +533,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         cs ^= 1;
       }
       // a chunk without items loads the next chunk's Q and dO rows in its first round
-      if (n == 0 && u == 0 && live_next) load_qdo(g1, qf, df);
+      if (n == 0 && u == 0 && live_next) load_qdo(g1, qf, df, buf ^ 1);
     }
 
     // ---- finish the chunk: dQ rows of this wave; zero dw partials of empty slots
@@ -549,9 +552,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         // the LMK row: add the two waves' shares of its dQ, store it and its
         // per-slot -D and shifted lse
         const float t0 = sum_xor32(ox0), t1 = sum_xor32(ox1);
-        sX[0].o[half][lane] = hh ? t1 : t0;  // lane l: d = l
+        sX[0].o[xh][lane] = hh ? t1 : t0;  // lane l: d = l
         block_barrier();
-        if (half == 0) {
+        if (xh == 0) {
           const int64_t tx = tok0 + kS;
           reinterpret_cast<T*>(p.dq)[tx * kD + lane] = (T)(as * (sX[0].o[0][lane] + sX[0].o[1][lane]));
           if (lane < K && sJ[pair][buf][lane] >= 0) {
@@ -657,6 +660,9 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
   const TileCopy<T, 2> cp(wave, lane);
   const uint32_t col_off = (uint32_t)(lane * sizeof(float));
   constexpr int kXPieces = kD * (int)sizeof(T) / 16;  // 16-byte pieces of one row
+  const int xw = __builtin_amdgcn_readfirstlane(wave);  // LMK row copies: wave 0 Q and L, wave 1 dO and -D
+  const T* const xrow_src = xw == 0 ? qb : ob;
+  const float* const xcol_src = xw == 0 ? Lb : Db;
   auto enc = [&](int e) { return ((e / K + p.causal) << 5) | (e % K); };  // list entry t*K+s -> (query chunk << 5) | slot
   auto issue = [&](int slot, int cs) __device__ {
     const int64_t c = cs >> 5;
@@ -669,12 +675,12 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
     else dma_column_s(Db + s * lq_len + c * SQ, col_off, cols + kS);
     if constexpr (XR) {
       // the LMK row (row S of the chunk): wave 0 its Q row and shifted lse, wave 1
-      // its dO row and -D
+      // its dO row and -D (addresses in scalar registers)
       const int64_t xr = c * SQ + kS;
       T* xdst = dst + XOFF;
       float* xcol = reinterpret_cast<float*>(xdst + 2 * kD);
-      if (lane < kXPieces) dma_row16((wave == 0 ? qb : ob) + xr * kD, lane * 16u, xdst + wave * kD);
-      if (lane == 0) dma_column_s((wave == 0 ? Lb : Db) + s * lq_len + xr, 0u, xcol + wave);
+      if (lane < kXPieces) dma_row16(xrow_src + xr * kD, lane * 16u, xdst + xw * kD);
+      if (lane == 0) dma_column_s(xcol_src + s * lq_len + xr, 0u, xcol + xw);
     }
   };
 
@@ -777,13 +783,13 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
       // across l ^ 32), w P and dS, then dV^T += dO_x^T (w P_x) and
       // dK^T += q_x^T dS_x as one more contraction step whose only nonzero
       // entry is the first
+      __builtin_amdgcn_sched_barrier(0);
       const T* sqx = sQ + XOFF;
       const T* sdx = sqx + kD;
       const float* slx = reinterpret_cast<const float*>(sdx + kD);
       float a = 0.f, b = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
         a = frag_dot(kf[kb], vec_frag(sqx, 16 * kb + 8 * hh), a);
         b = frag_dot(vf[kb], vec_frag(sdx, 16 * kb + 8 * hh), b);
       }
@@ -791,11 +797,16 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
       b = sum_xor32(b);
       const float wpx = __builtin_amdgcn_exp2f(fmaf(a, sc, -slx[0]));
       const bool e0 = hh == 0;
-      const Frag<T> bw = frag_e0<T>(e0 ? wpx : 0.f), bd = frag_e0<T>(e0 ? wpx * (b + slx[1]) : 0.f);
-      mma32(dv0, frag_e0<T>(e0 ? to_f32(sdx[lane & 31]) : 0.f), bw);
-      mma32(dv1, frag_e0<T>(e0 ? to_f32(sdx[32 + (lane & 31)]) : 0.f), bw);
-      mma32(dk0, frag_e0<T>(e0 ? to_f32(sqx[lane & 31]) : 0.f), bd);
-      mma32(dk1, frag_e0<T>(e0 ? to_f32(sqx[32 + (lane & 31)]) : 0.f), bd);
+      const float xw = e0 ? wpx : 0.f, xd = e0 ? wpx * (b + slx[1]) : 0.f;
+      const int c0 = lane & 31;
+      __builtin_amdgcn_sched_barrier(0);
+      mma32(dv0, frag_e0<T>(e0 ? to_f32(sdx[c0]) : 0.f), frag_e0<T>(xw));
+      __builtin_amdgcn_sched_barrier(0);
+      mma32(dv1, frag_e0<T>(e0 ? to_f32(sdx[32 + c0]) : 0.f), frag_e0<T>(xw));
+      __builtin_amdgcn_sched_barrier(0);
+      mma32(dk0, frag_e0<T>(e0 ? to_f32(sqx[c0]) : 0.f), frag_e0<T>(xd));
+      __builtin_amdgcn_sched_barrier(0);
+      mma32(dk1, frag_e0<T>(e0 ? to_f32(sqx[32 + c0]) : 0.f), frag_e0<T>(xd));
     }
     // dV^T += dO^T (w P) and dK^T += Q^T dS  (contractions over the 64 queries)
 #pragma unroll

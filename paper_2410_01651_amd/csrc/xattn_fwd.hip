@@ -159,12 +159,13 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
   auto qrow_ptr = [&](int64_t w) __device__ {
     return reinterpret_cast<const T*>(p.q) + (w * SQ + qi) * kD;
   };
-  // the LMK row's queries: 16-byte piece `lane` (lanes below kD / 16-byte pieces)
+  // the LMK row's queries, copied by the first wave straight into LDS (one
+  // 16-byte piece per lane below kXPieces); visible to both waves after the
+  // next wait and barrier
   constexpr int kXPieces = kD * (int)sizeof(T) / 16;
-  u32x4 qxv{0u, 0u, 0u, 0u};
-  auto load_qx = [&](int64_t w) __device__ {
-    if (lane < kXPieces)
-      qxv = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(p.q) + (w * SQ + kS) * kD)[lane];
+  const int xh = __builtin_amdgcn_readfirstlane(half);  // the wave's half, in a scalar register
+  auto load_qx = [&](int64_t w, int xbuf) __device__ {
+    if (lane < kXPieces) dma_row16(reinterpret_cast<const T*>(p.q) + (w * SQ + kS) * kD, lane * 16u, &sX[0].q[xbuf][0]);
   };
 
   // ---- prologue: the first chunk's slot list and Q, the second chunk's metadata
@@ -183,7 +184,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     const T* qr = qrow_ptr(c_begin);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qr + 16 * kb + 8 * hh);
-    if (XR && half == 0) load_qx(c_begin);
+    if (XR && xh == 0) load_qx(c_begin, 0);
     if (half == 0) make_slots(m0, g0, 0);
     if (my_n > 1) {
       row_of(g1, ro, ex, ow);
@@ -240,7 +241,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
   auto compute = [&](int slot, int u, int64_t tok0, int buf, f32x16& o0, f32x16& o1) __device__ {
     const uint32_t co = (uint32_t)slot * 2 * kTileB;
     const int s = __builtin_amdgcn_readlane(ls, u);
-    const bool xr = XR && (u & 1) == half;  // this wave takes the LMK row of slot u
+    const bool xr = XR && (u & 1) == xh;  // this wave takes the LMK row of slot u
     const T* sK = ring + (2 * pair + slot) * (2 * TILE);
     const T* sV = sK + TILE;
     // all K fragments first, so the eight products issue back to back
@@ -322,7 +323,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
       float xsum = sum64(xe);
       if (OBO) xsum += __builtin_amdgcn_exp2f(-xm);
       if (lane == 0) sX[0].lse[s] = (xm + __builtin_amdgcn_logf(xsum)) * kLn2;
-      sX[0].p[half][lane] = (T)(xe * (__int_as_float(coef_bits) * __builtin_amdgcn_rcpf(xsum)));
+      sX[0].p[xh][lane] = (T)(xe * (__int_as_float(coef_bits) * __builtin_amdgcn_rcpf(xsum)));
     }
     Frag<T> pf[4];
     frag_from_acc(pf[0], st0, 0, coef);
@@ -349,7 +350,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
           v0 = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
           v1 = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
         }
-        const Frag<T> xf = vec_frag_t(&sX[0].p[half][0], 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh);
+        const Frag<T> xf = vec_frag_t(&sX[0].p[xh][0], 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh);
         ox0 = frag_dot(v0, xf, ox0);
         ox1 = frag_dot(v1, xf, ox1);
       }
@@ -382,18 +383,13 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
           lw = sWc[pair][buf][l32];
           kvb = kvb_n;
         }
-        // the LMK row's queries for this chunk: written by the wave that takes
-        // slot 0 (its own reads follow in program order; the partner's first
-        // read is in round 1, after a barrier)
-        if (XR && half == 0 && live && lane < kXPieces)
-          reinterpret_cast<u32x4*>(&sX[0].q[buf][0])[lane] = qxv;
         if (live_next) {
           if constexpr (!XR) {
             const T* qr = qrow_ptr(w + stride);
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) qn[kb] = load_frag(qr + 16 * kb + 8 * hh);
-          } else if (half == 0) {
-            load_qx(w + stride);
+          } else if (xh == 0) {
+            load_qx(w + stride, buf ^ 1);
           }
           if (half == 0) make_slots(meta, g1, buf ^ 1);
           if (ci + 2 < my_n) {
@@ -452,9 +448,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
         // the LMK row: add the two waves' shares (each lane first adds its key
         // half to the partner lane's), then one wave stores the row and its lse
         const float t0 = sum_xor32(ox0), t1 = sum_xor32(ox1);
-        sX[0].o[half][lane] = hh ? t1 : t0;  // lane l: d = l
+        sX[0].o[xh][lane] = hh ? t1 : t0;  // lane l: d = l
         block_barrier();
-        if (half == 0) {
+        if (xh == 0) {
           const int64_t tx = tok0 + kS;
           reinterpret_cast<T*>(p.out)[tx * kD + lane] = (T)(sX[0].o[0][lane] + sX[0].o[1][lane]);
           if (p.lse && lane < K) p.lse[tx * K + lane] = sJ[pair][buf][lane] < 0 ? -INFINITY : sX[0].lse[lane];
