@@ -186,12 +186,19 @@ def flops_per_unit():
             "bwd_dkdv_kernel": 2 * (2 * S * DH)}      # dV = P^T dO, dK = dS^T Q (its own S/dP recompute not counted)
 
 
-def mfma_roofline(kern, units, dom):
+def profile_key(kernel, tag=None):
+    """Name of a kernel's entry in the committed counter summaries: the 64K train
+    step's kernels untagged, other workloads' as kernel@tag."""
+    return kernel if tag is None else f"{kernel}@{tag}"
+
+
+def mfma_roofline(kern, units, dom, tag=None):
     fpu = flops_per_unit()
     fl = units * S * fpu[dom]
     ach = fl / (kern[dom]["avg_ms"] * 1e-3) / 1e12
+    key = profile_key(dom, tag)
     return {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": ach / BF16_PEAK_TFLOPS, "traffic": measured_traffic(dom), "counters": measured_mfma(dom),
+            "frac": ach / BF16_PEAK_TFLOPS, "traffic": measured_traffic(key), "counters": measured_mfma(key),
             "algorithmic_flops_per_launch": fl, "avg_launch_ms": kern[dom]["avg_ms"]}
 
 
@@ -324,10 +331,11 @@ def bench_forward(args, dev, gca, name):
     kern = kernel_table(per, steps)
     idx_host = fo["idx"].cpu().numpy()
     units = valid_units(idx_host, w)
-    kern["xattn_fwd_kernel"]["tflops"] = mfma_roofline(kern, units, "xattn_fwd_kernel")["achieved"]
+    tag = {"train_16k_bf16": "forward_16k", "planted_1m_bf16": "planted_1m"}[name]
+    roof = mfma_roofline(kern, units, "xattn_fwd_kernel", tag)
+    kern["xattn_fwd_kernel"]["tflops"] = roof["achieved"]
     leg = {"metric": "GCA forward tokens/s", "value": w.B * w.Lq / (ms * 1e-3), "unit": "tokens/s",
-           "ms_per_call": ms, "calls": steps, "kernels": kern,
-           "roofline": mfma_roofline(kern, units, "xattn_fwd_kernel")}
+           "ms_per_call": ms, "calls": steps, "kernels": kern, "roofline": roof}
     # the selection's matrix-core rate: 2 D flops per causal (row, earlier chunk) pair
     pairs = w.B * w.Hr * w.n_chunks * (w.n_chunks - 1) // 2
     sel_kernel = "select_part_kernel" if "select_part_kernel" in kern else \
@@ -336,8 +344,9 @@ def bench_forward(args, dev, gca, name):
     sach = sfl / (kern[sel_kernel]["avg_ms"] * 1e-3) / 1e12
     leg["selection"] = {"kernel": sel_kernel, "bound": "mfma", "achieved": sach, "peak": BF16_PEAK_TFLOPS,
                         "unit": "TFLOP/s", "frac": sach / BF16_PEAK_TFLOPS, "algorithmic_flops_per_launch": sfl,
-                        "avg_launch_ms": kern[sel_kernel]["avg_ms"], "traffic": measured_traffic(sel_kernel),
-                        "counters": measured_mfma(sel_kernel)}
+                        "avg_launch_ms": kern[sel_kernel]["avg_ms"],
+                        "traffic": measured_traffic(profile_key(sel_kernel, tag)),
+                        "counters": measured_mfma(profile_key(sel_kernel, tag))}
     if w.planted:
         pos = gi.plant_positions(w)
         leg["planted_retrieved"] = sorted(idx_host[0, 0, -1].tolist()) == sorted(pos.tolist())
