@@ -255,38 +255,40 @@ def bench_train(args, dev, gca):
     prof_ms, per = kernel_times(step, args.steps, stream, gca)
     log(f"profiled {args.steps} steps: {prof_ms / args.steps:.3f} ms/step")
     idx_host = fo["idx"].cpu().numpy()
-    # the Gumbel top-k variant of the same step (noise in the selection only)
-    pg = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, gumbel_seed=1)
-    step(pg)
-    g_ms = timed(lambda: step(pg), args.steps, stream) / args.steps
-    _, g_per = kernel_times(lambda: step(pg), args.steps, stream, gca)
-    gumbel = {"value": w.B * w.Lq / (g_ms * 1e-3), "unit": "tokens/s", "ms_per_step": g_ms,
-              "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()
-                          if k in ("chunk_scores_kernel", "topk_kernel")}}
-    log(f"gumbel top-k {args.steps} steps: {g_ms:.3f} ms/step")
-    # the same step with S+1 query rows per chunk (each chunk's LMK token as its
-    # last query row); k/v and the landmarks are shared with the step above
-    wx = get_workload("fwdbwd_64k_bf16", lmk_row=True)
-    tx = dict(t, **gi.device_tensors(wx, ("q", "dout"), dev))
-    px = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, lmk_row=True)
-    fox = forward_outputs(px, gca, dev)
-    gx = dict(grads, dq=torch.empty(gca.shapes(px).q, dtype=torch.bfloat16, device=dev))
-    wsbx, _ = gca.workspace(px, gca.OP_BACKWARD, dev)
+    gumbel = lmk_row = None
+    if not args.no_variants:
+        # the Gumbel top-k variant of the same step (noise in the selection only)
+        pg = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, gumbel_seed=1)
+        step(pg)
+        g_ms = timed(lambda: step(pg), args.steps, stream) / args.steps
+        _, g_per = kernel_times(lambda: step(pg), args.steps, stream, gca)
+        gumbel = {"value": w.B * w.Lq / (g_ms * 1e-3), "unit": "tokens/s", "ms_per_step": g_ms,
+                  "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()
+                              if k in ("chunk_scores_kernel", "topk_kernel")}}
+        log(f"gumbel top-k {args.steps} steps: {g_ms:.3f} ms/step")
+        # the same step with S+1 query rows per chunk (each chunk's LMK token as its
+        # last query row); k/v and the landmarks are shared with the step above
+        wx = get_workload("fwdbwd_64k_bf16", lmk_row=True)
+        tx = dict(t, **gi.device_tensors(wx, ("q", "dout"), dev))
+        px = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, lmk_row=True)
+        fox = forward_outputs(px, gca, dev)
+        gx = dict(grads, dq=torch.empty(gca.shapes(px).q, dtype=torch.bfloat16, device=dev))
+        wsbx, _ = gca.workspace(px, gca.OP_BACKWARD, dev)
 
-    def step_x():
-        gca.forward(px, tx["lmk_q"], tx["lmk_k"], tx["q"], tx["k"], tx["v"], ws=wsf, **fox)
-        gca.grouped_xattn_bwd(px, tx["q"], tx["k"], tx["v"], fox["idx"], fox["sel"], fox["lse"], tx["dout"],
-                              tx["lmk_q"], tx["lmk_k"], ws=wsbx, grads=gx)
+        def step_x():
+            gca.forward(px, tx["lmk_q"], tx["lmk_k"], tx["q"], tx["k"], tx["v"], ws=wsf, **fox)
+            gca.grouped_xattn_bwd(px, tx["q"], tx["k"], tx["v"], fox["idx"], fox["sel"], fox["lse"], tx["dout"],
+                                  tx["lmk_q"], tx["lmk_k"], ws=wsbx, grads=gx)
 
-    step_x()
-    x_ms = timed(step_x, args.steps, stream) / args.steps
-    _, x_per = kernel_times(step_x, args.steps, stream, gca)
-    lmk_row = {"value": wx.B * wx.Lq / (x_ms * 1e-3), "unit": "tokens/s", "ms_per_step": x_ms,
-               "query_rows_per_chunk": wx.Sq,
-               "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in x_per.items()
-                           if k in ("xattn_fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel")}}
-    log(f"S+1 query rows {args.steps} steps: {x_ms:.3f} ms/step")
-    del tx, fox, gx, wsbx
+        step_x()
+        x_ms = timed(step_x, args.steps, stream) / args.steps
+        _, x_per = kernel_times(step_x, args.steps, stream, gca)
+        lmk_row = {"value": wx.B * wx.Lq / (x_ms * 1e-3), "unit": "tokens/s", "ms_per_step": x_ms,
+                   "query_rows_per_chunk": wx.Sq,
+                   "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in x_per.items()
+                               if k in ("xattn_fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel")}}
+        log(f"S+1 query rows {args.steps} steps: {x_ms:.3f} ms/step")
+        del tx, fox, gx, wsbx
 
     units = valid_units(idx_host, w)
     kern = kernel_table(per, args.steps)
@@ -434,10 +436,14 @@ def bench_decode(args, dev, gca):
     idx_host = fo["idx"].cpu().numpy()
     found = planted in idx_host.ravel().tolist()
     # the Gumbel top-k variant of the same call
-    pg = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, gumbel_seed=1)
-    call(pg)
-    g_ms = timed(lambda: call(pg), steps, stream) / steps
-    _, g_per = kernel_times(lambda: call(pg), steps, stream, gca)
+    gumbel = None
+    if not args.no_variants:
+        pg = gca.problem(w.B, w.H, w.n_chunks, w.topk, D=w.Dl, Hr=w.Hr, dtype=w.dtype, mode=w.mode, gumbel_seed=1)
+        call(pg)
+        g_ms = timed(lambda: call(pg), steps, stream) / steps
+        _, g_per = kernel_times(lambda: call(pg), steps, stream, gca)
+        gumbel = {"value": None, "unit": "GB/s", "ms_per_call": g_ms,
+                  "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()}}
     key_bytes = w.n_chunks * w.Dl * 2
     kv_bytes = 2 * w.topk * w.H * S * DH * 2
     io_bytes = 2 * w.H * S * DH * 2 + w.Dl * 2
@@ -467,9 +473,10 @@ def bench_decode(args, dev, gca):
                      "traffic": measured_traffic("decode_scan_kernel@decode_16m"),
                      "algorithmic_bytes_per_launch": key_bytes, "avg_launch_ms": scan_ms},
         "kernels": kernel_table(per, steps),
-        "gumbel_topk": {"value": total_bytes / (g_ms * 1e-3) / 1e9, "unit": "GB/s", "ms_per_call": g_ms,
-                        "kernels": {k: {"avg_ms": sum(v) / len(v)} for k, v in g_per.items()}},
+        "gumbel_topk": gumbel,
     }
+    if gumbel is not None:
+        gumbel["value"] = total_bytes / (gumbel["ms_per_call"] * 1e-3) / 1e9
     return w, leg, host, total_bytes
 
 
@@ -660,6 +667,9 @@ def main():
     ap.add_argument("--no-host-kv", action="store_true", help="skip the decode leg with host-resident K/V")
     ap.add_argument("--no-forward-legs", action="store_true", help="skip the 16K and 1M forward legs")
     ap.add_argument("--no-peaks", action="store_true")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the Gumbel and S+1-row variants of the train step (counter runs: only the "
+                         "plain step's dispatches)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="first run one plain device copy of this many MiB (a known-size reference for "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE)")
