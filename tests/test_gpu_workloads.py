@@ -3,7 +3,8 @@
 The GPU runs the whole workload and the oracle checks it: top-k indices (exact)
 on every landmark row of every workload; fusion weights, outputs and log-sum-exp
 of every chunk of the 16K training and 64K workloads; every gradient of every
-(batch, head) slice of the 64K backward.  At 1M tokens the attention output is
+(batch, head) slice of the 64K backward; the same at the 16K and 64K shapes
+with S+1 query rows per chunk.  At 1M tokens the attention output is
 checked on sampled query chunks, and at 16M on the one new chunk.  Per-token
 tensors of the large workloads are drawn on the device by the shared seeded
 generator and copied back for the oracle.
@@ -270,3 +271,55 @@ def test_decode_long_scan_ranges(dev, n_chunks, topk, gumbel):
     assert max_abs_rel(host64(f["lse"][0]), l_ref) <= TOL[w.dtype]
     del t
     torch.cuda.empty_cache()
+
+
+def test_lmk_rows_16k_forward(dev):
+    """The 16K training shape with S+1 query rows per chunk (each chunk's LMK token as
+    its 65th row): every row's indices and weights, out / lse of every chunk and
+    head of batches 0 and 7."""
+    from paper_2410_01651_amd import gca
+    w, inp, t = _setup("train_16k_bf16", dev, lmk_row=True)
+    f = gca.forward(problem_for(w), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    ref = _check_all_rows(w, inp, f)
+    tol = TOL[w.dtype]
+    for b in (0, w.B - 1):
+        ri, rw = ref[b]
+        sl = lambda name: host64(t[name][b:b + 1])
+        o_ref, l_ref = og.xattn_fwd(sl("q"), sl("k"), sl("v"), ri[None, None], rw[None, None], w.S,
+                                    w.attn_scale, w.mode, Sq=w.Sq)
+        assert max_abs_rel(host64(f["out"][b:b + 1]), o_ref) <= tol, b
+        assert max_abs_rel(host64(f["lse"][b:b + 1]), l_ref) <= tol, b
+
+
+def test_lmk_rows_64k_fwdbwd(dev):
+    """The 64K forward + backward with S+1 query rows per chunk: every row's indices,
+    out / lse of every chunk and head of batch 0, and batch 0's backward (dq, dk, dv
+    of each of its 16 slices, dsel and both landmark gradients)."""
+    from paper_2410_01651_amd import gca
+    w, inp, t = _setup("fwdbwd_64k_bf16", dev, lmk_row=True)
+    p = problem_for(w)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                              t["lmk_q"], t["lmk_k"])
+    ref = _check_all_rows(w, inp, f)
+    tol = TOL[w.dtype]
+    b = 0
+    ri, rw = ref[b]
+    full = lambda name: host64(t[name][b:b + 1])
+    o_ref, l_ref = og.xattn_fwd(full("q"), full("k"), full("v"), ri[None, None], rw[None, None], w.S,
+                                w.attn_scale, w.mode, Sq=w.Sq)
+    assert max_abs_rel(host64(f["out"][b:b + 1]), o_ref) <= tol
+    assert max_abs_rel(host64(f["lse"][b:b + 1]), l_ref) <= tol
+    dq, dk, dv, dw = og.xattn_bwd(full("q"), full("k"), full("v"), ri[None, None], rw[None, None], full("dout"),
+                                  w.S, w.attn_scale, Sq=w.Sq)
+    for key, r in (("dq", dq), ("dk", dk), ("dv", dv)):
+        x = host64(g[key][b:b + 1])
+        for h in range(w.H):
+            e = max_abs_rel(x[:, h], r[:, h])
+            assert e <= tol, (key, h, e)
+    dsel = og.dsel_from_dw(rw[None, None], dw)
+    dlq, dlk = og.landmark_grads(dsel, ri[None, None], gi.decode(w, inp["lmk_q"][b:b + 1]),
+                                 gi.decode(w, inp["lmk_k"][b:b + 1]), w.score_scale)
+    assert max_abs_rel(host64(g["dsel"][b:b + 1]), dsel) <= tol
+    assert max_abs_rel(host64(g["dlmk_q"][b:b + 1]), dlq) <= tol
+    assert max_abs_rel(host64(g["dlmk_k"][b:b + 1]), dlk) <= tol
