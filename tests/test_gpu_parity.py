@@ -486,6 +486,30 @@ def test_lmk_rows_forward_backward(dev, name, kw, obo):
         assert e <= TOL[w.dtype], (key, e)
 
 
+def test_side_stream(dev):
+    """The forward and backward enqueued on a side stream (the binding allocates
+    their outputs and workspaces for that stream) give bit for bit what the
+    default stream gives."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w, inp = _case("fwdbwd_64k_bf16", B=1, H=4, n_chunks=96, topk=8)
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    f0 = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    g0 = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f0["idx"], f0["sel"], f0["lse"], t["dout"],
+                               t["lmk_q"], t["lmk_k"])
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    f1 = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"], stream=side)
+    g1 = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f1["idx"], f1["sel"], f1["lse"], t["dout"],
+                               t["lmk_q"], t["lmk_k"], stream=side)
+    side.synchronize()
+    for key in ("out", "idx", "sel", "lse", "w"):
+        assert torch.equal(f0[key], f1[key]), key
+    for key in g0:
+        assert torch.equal(g0[key], g1[key]), key
+
+
 def test_profile_hook(dev):
     """The per-kernel timing hook: kernels are timed in launch order up to the
     capacity, named, with positive durations, and the results do not change."""
