@@ -35,7 +35,11 @@
  *   launched and a status != GCA_OK is returned, with detail in gca_last_error().
  *   Launch failures return GCA_ERR_HIP.  Kernel faults surface at the caller's
  *   next synchronisation.
- * - All work is enqueued on `stream`; no call synchronises.  Calls are
+ * - All work is enqueued on `stream`; no call synchronises (unless the
+ *   environment variable GCA_DEBUG_SYNC is set to a value other than 0 when the
+ *   library first launches: then every kernel launch is followed by a
+ *   synchronisation of `stream` and an error check that names the kernel in
+ *   gca_last_error(), for debugging).  Calls are
  *   re-entrant (no global mutable state besides the thread-local error string
  *   and the thread-local profiling hook below).
  * - Supported in this version: d == 64, S == 64, 1 <= topk <= 32, Hr in {1, H},

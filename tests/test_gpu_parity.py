@@ -510,6 +510,47 @@ def test_side_stream(dev):
         assert torch.equal(g0[key], g1[key]), key
 
 
+_DEBUG_SYNC_CHILD = r"""
+import hashlib, sys
+sys.path.insert(0, sys.argv[1])
+sys.path.insert(0, sys.argv[1] + "/tests")
+import torch
+from _helpers import problem_for, upload
+from gen import get_workload
+from oracle import margins
+from paper_2410_01651_amd import gca
+w = get_workload("fwdbwd_64k_bf16", B=1, H=2, n_chunks=40, topk=4)
+inp, _ = margins.checked_inputs(w)
+t = upload(w, inp, torch.device("cuda:0"))
+p = problem_for(w)
+f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"], t["lmk_q"], t["lmk_k"])
+h = hashlib.sha256()
+for d in (f, g):
+    for key in sorted(d):
+        h.update(d[key].cpu().contiguous().view(torch.uint8).numpy().tobytes())
+print(h.hexdigest())
+"""
+
+
+def test_debug_sync_mode(dev):
+    """GCA_DEBUG_SYNC=1 (every launch synchronised and checked) gives bit for bit
+    the results of the ordinary mode, in a child process that reads it at load."""
+    import os
+    import subprocess
+    import sys
+    from _helpers import ROOT
+    env = dict(os.environ)
+    outs = []
+    for mode in ("0", "1"):
+        env["GCA_DEBUG_SYNC"] = mode
+        r = subprocess.run([sys.executable, "-c", _DEBUG_SYNC_CHILD, ROOT], env=env, capture_output=True,
+                           text=True, timeout=240)
+        assert r.returncode == 0, r.stderr[-2000:]
+        outs.append(r.stdout.strip().splitlines()[-1])
+    assert outs[0] == outs[1]
+
+
 def test_profile_hook(dev):
     """The per-kernel timing hook: kernels are timed in launch order up to the
     capacity, named, with positive durations, and the results do not change."""
