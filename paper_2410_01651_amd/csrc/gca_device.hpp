@@ -411,6 +411,20 @@ __device__ __forceinline__ float sum32(float x) {
   pair16(__float_as_uint(x), a, b);
   return __uint_as_float(a) + __uint_as_float(b);
 }
+// Maximum of the 32 entries of two accumulators, as a tree of three-operand
+// maxima (v_max3_f32: 16 instructions for 32 values).
+__device__ __forceinline__ float max_of(const f32x16& a, const f32x16& b) {
+  float m[11];
+#pragma unroll
+  for (int i = 0; i < 5; ++i) m[i] = fmaxf(fmaxf(a[3 * i], a[3 * i + 1]), a[3 * i + 2]);
+#pragma unroll
+  for (int i = 0; i < 5; ++i) m[5 + i] = fmaxf(fmaxf(b[3 * i], b[3 * i + 1]), b[3 * i + 2]);
+  m[10] = fmaxf(a[15], b[15]);
+  const float x0 = fmaxf(fmaxf(m[0], m[1]), m[2]), x1 = fmaxf(fmaxf(m[3], m[4]), m[5]);
+  const float x2 = fmaxf(fmaxf(m[6], m[7]), m[8]), x3 = fmaxf(m[9], m[10]);
+  return fmaxf(fmaxf(x0, x1), fmaxf(x2, x3));
+}
+
 // Sum / max over the whole wave.
 __device__ __forceinline__ float sum64(float x) {
   x = sum32(x);

@@ -232,10 +232,7 @@ __global__ __launch_bounds__(kDecThreads) void xattn_decode_kernel(DecParams p) 
       }
     }
     // per-query softmax over the chunk's 64 keys (query = accumulator column)
-    float mx = fmaxf(st0[0], st1[0]);
-#pragma unroll
-    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, fmaxf(st0[i], st1[i]));
-    mx = max_xor32(mx) * sc;
+    float mx = max_xor32(max_of(st0, st1)) * sc;
     if (OBO) mx = fmaxf(mx, 0.f);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {

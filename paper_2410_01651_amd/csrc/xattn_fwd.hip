@@ -291,10 +291,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
         va[2 * kb + 1] = lds_frag_t(sV, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
       }
     }
-    float mx = fmaxf(st0[0], st1[0]);
-#pragma unroll
-    for (int i = 1; i < 16; ++i) mx = fmaxf(mx, fmaxf(st0[i], st1[i]));
-    mx = max_xor32(mx) * sc;
+    float mx = max_xor32(max_of(st0, st1)) * sc;
     if (OBO) mx = fmaxf(mx, 0.f);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {

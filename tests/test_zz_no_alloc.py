@@ -58,6 +58,8 @@ CASES = [
     ("train_16k_bf16", dict(B=2, H=4, n_chunks=300), dict(B=1, H=2, n_chunks=90), 0),
     ("planted_1m_bf16", dict(H=2, n_chunks=2_000), dict(H=2, n_chunks=700), 1),
     ("tiny_fp32_1k", dict(B=2, H=2, n_chunks=80, topk=3), dict(B=1, H=1, n_chunks=16), 0),
+    # S+1 query rows per chunk
+    ("train_16k_bf16", dict(B=1, H=4, n_chunks=200, lmk_row=True), dict(B=1, H=2, n_chunks=70, lmk_row=True), 0),
 ]
 
 
