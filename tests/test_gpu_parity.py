@@ -458,6 +458,13 @@ LMK = [
     ("train_16k_bf16", dict(B=1, H=2, n_chunks=50, topk=12, Hr=2, D=128), False),  # k > 8, per-head retrieval
     ("train_16k_bf16", dict(B=1, H=2, n_chunks=20, topk=1), False),
     ("fwdbwd_64k_bf16", dict(B=1, H=4, n_chunks=96, topk=8), False),
+    # edges: one chunk (everything empty), k above the history, k = 32 (unstaged
+    # per-slot values), fp32 with off-by-one, uneven streams
+    ("train_16k_bf16", dict(B=1, H=2, n_chunks=1, topk=4), False),
+    ("train_16k_bf16", dict(B=2, H=2, n_chunks=3, topk=8), False),
+    ("train_16k_bf16", dict(B=1, H=2, n_chunks=65, topk=32), True),
+    ("tiny_fp32_1k", dict(B=2, H=3, n_chunks=37, topk=6, whole_reseed=False), True),
+    ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=700, topk=3), False),
 ]
 
 
@@ -476,7 +483,9 @@ def test_lmk_rows_forward_backward(dev, name, kw, obo):
     assert tuple(f["out"].shape) == (w.B, w.H, w.n_chunks * (w.S + 1), w.d)
     ref = _check_forward(w, inp, f, off_by_one=obo)
     lmk_out = host64(f["out"]).reshape(w.B, w.H, w.n_chunks, w.S + 1, w.d)[:, :, :, w.S]
-    assert np.all(lmk_out[:, :, :2] == 0.0) and np.abs(lmk_out[:, :, 2:]).min(axis=-1).max() > 0.0
+    assert np.all(lmk_out[:, :, :2] == 0.0)
+    if w.n_chunks > 2:
+        assert np.abs(lmk_out[:, :, 2:]).min(axis=-1).max() > 0.0
     g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
                               t["lmk_q"], t["lmk_k"])
     x = decode_all(w, inp)
