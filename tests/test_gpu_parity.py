@@ -495,6 +495,35 @@ def test_lmk_rows_forward_backward(dev, name, kw, obo):
         assert e <= TOL[w.dtype], (key, e)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_max_landmark_width(dev, dtype):
+    """The widest landmarks the library takes (D = 8192): the score matrix path and
+    the one-pass select of the forward, the backward's landmark gradients, and a
+    decode scan, against the oracle."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case("fwdbwd_64k_bf16", B=1, H=2, D=8192, n_chunks=60, topk=4, dtype=dtype)
+    t = upload(w, inp, dev)
+    tol = TOL[w.dtype]
+    x = decode_all(w, inp)
+    pp = oracle_params(w)
+    rf = og.forward(pp, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"])
+    rb = og.backward(pp, rf, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"], x["dout"])
+    for flags in (gca.FLAG_MATERIALIZE, gca.FLAG_FUSED_TOPK):
+        p = problem_for(w, flags=flags)
+        f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+        np.testing.assert_array_equal(f["idx"].cpu().numpy(), rf["idx"])
+        for key in ("sel", "w", "out", "lse"):
+            assert max_abs_rel(host64(f[key]), rf[key]) <= tol, (flags, key)
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                              t["lmk_q"], t["lmk_k"])
+    for key in ("dq", "dk", "dv", "dsel", "dlmk_q", "dlmk_k"):
+        assert max_abs_rel(host64(g[key]), rb[key]) <= tol, key
+    wd, ind = _case("decode_16m_bf16", H=2, D=8192, n_chunks=300, dtype=dtype, device_kv=False)
+    td = upload(wd, ind, dev)
+    fd = gca.forward(problem_for(wd), td["lmk_q"], td["lmk_k"], td["q"], td["k"], td["v"])
+    _check_forward(wd, ind, fd)
+
+
 def test_side_stream(dev):
     """The forward and backward enqueued on a side stream (the binding allocates
     their outputs and workspaces for that stream) give bit for bit what the
