@@ -92,6 +92,33 @@ def timed(run_step, steps, stream):
     return total
 
 
+def step_latency(run_step, steps, stream, isolated=False):
+    """Distribution of one step's duration: an event pair around every step.
+    Back to back (isolated=False) each duration is the step's share of the
+    stream, queue gaps included; isolated=True waits for the device after every
+    step, so a duration also holds the launch of an idle stream.  Returns
+    {"median", "p10", "p90", "min", "max"} in ms."""
+    import torch
+    evs = Events(2 * steps)
+    torch.cuda.synchronize()
+    for i in range(steps):
+        evs.record(2 * i, stream)
+        run_step()
+        evs.record(2 * i + 1, stream)
+        if isolated:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    d = sorted(evs.ms(2 * i, 2 * i + 1) for i in range(steps))
+    evs.close()
+
+    def q(f):
+        x = f * (len(d) - 1)
+        lo = int(x)
+        hi = min(lo + 1, len(d) - 1)
+        return d[lo] + (d[hi] - d[lo]) * (x - lo)
+    return {"median": q(0.5), "p10": q(0.1), "p90": q(0.9), "min": d[0], "max": d[-1], "n": len(d)}
+
+
 def kernel_times(run_step, steps, stream, gca, per_step_capacity=32):
     """Run `steps` steps with the per-kernel hook armed: every kernel's dispatch
     carries a start and a stop event, so the hook adds nothing to the stream.
@@ -254,6 +281,8 @@ def bench_train(args, dev, gca):
     # the same K steps again with every kernel's dispatch carrying start/stop events
     prof_ms, per = kernel_times(step, args.steps, stream, gca)
     log(f"profiled {args.steps} steps: {prof_ms / args.steps:.3f} ms/step")
+    lat = step_latency(step, max(args.steps, 50), stream)
+    log(f"per-step latency: median {lat['median']:.3f} p10 {lat['p10']:.3f} p90 {lat['p90']:.3f} ms")
     idx_host = fo["idx"].cpu().numpy()
     gumbel = lmk_row = None
     if not args.no_variants:
@@ -301,7 +330,7 @@ def bench_train(args, dev, gca):
     algo_fl = units * S * (flops_per_unit()["xattn_fwd_kernel"] + 5 * 2 * S * DH)
     return {
         "w": w, "t": t, "tokens": w.B * w.Lq, "ms_step": ms_step, "profiled_ms_step": prof_ms / args.steps,
-        "gumbel": gumbel, "lmk_row": lmk_row, "kernels": kern, "roofline": roof, "units": units,
+        "gumbel": gumbel, "lmk_row": lmk_row, "kernels": kern, "roofline": roof, "units": units, "latency": lat,
         "path_tflops": algo_fl / (ms_step * 1e-3) / 1e12,
     }
 
@@ -330,6 +359,7 @@ def bench_forward(args, dev, gca, name):
     steps = args.fwd_steps
     ms = timed(call, steps, stream) / steps
     _, per = kernel_times(call, steps, stream, gca)
+    lat = step_latency(call, max(steps, 50), stream)
     kern = kernel_table(per, steps)
     idx_host = fo["idx"].cpu().numpy()
     units = valid_units(idx_host, w)
@@ -337,7 +367,7 @@ def bench_forward(args, dev, gca, name):
     roof = mfma_roofline(kern, units, "xattn_fwd_kernel", tag)
     kern["xattn_fwd_kernel"]["tflops"] = roof["achieved"]
     leg = {"metric": "GCA forward tokens/s", "value": w.B * w.Lq / (ms * 1e-3), "unit": "tokens/s",
-           "ms_per_call": ms, "calls": steps, "kernels": kern, "roofline": roof}
+           "ms_per_call": ms, "calls": steps, "call_ms_distribution": lat, "kernels": kern, "roofline": roof}
     # the selection's matrix-core rate: 2 D flops per causal (row, earlier chunk) pair
     pairs = w.B * w.Hr * w.n_chunks * (w.n_chunks - 1) // 2
     sel_kernel = "select_part_kernel" if "select_part_kernel" in kern else \
@@ -432,6 +462,10 @@ def bench_decode(args, dev, gca):
     stream = torch.cuda.current_stream()
     ms_call = timed(call, steps, stream) / steps
     prof_ms, per = kernel_times(call, steps, stream, gca)
+    # per call: back to back (the steady state) and with the device idle before
+    # every call (the latency a lone decode step sees)
+    lat = {"steady_state": step_latency(call, max(steps, 50), stream),
+           "isolated": step_latency(call, max(steps, 50), stream, isolated=True)}
     planted = int(gi.plant_positions(w)[0])
     idx_host = fo["idx"].cpu().numpy()
     found = planted in idx_host.ravel().tolist()
@@ -463,7 +497,7 @@ def bench_decode(args, dev, gca):
     leg = {
         "metric": "retrieval-scan GB/s at 16M-ctx decode", "unit": "GB/s",
         "value": total_bytes / (ms_call * 1e-3) / 1e9, "ms_per_call": ms_call, "calls": steps,
-        "profiled_ms_per_call": prof_ms / steps,
+        "profiled_ms_per_call": prof_ms / steps, "call_ms_distribution": lat,
         "bytes_per_call": total_bytes, "frac_of_hbm_peak": total_bytes / (ms_call * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "planted_retrieved": found,
         "config": {"workload": "decode_16m_bf16: B=1 H=8 d=64, 16,777,216 past tokens (262,144 chunks), "
@@ -658,9 +692,9 @@ def measured_peaks(dev):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--fwd-steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--fwd-steps", type=int, default=50)
     ap.add_argument("--decode-steps", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
@@ -706,7 +740,8 @@ def main():
             line = {"decode_scan": leg}
         elif args.only == "train":
             tr = bench_train(args, dev, gca)
-            line = {"ms_per_step": tr["ms_step"], "kernels": tr["kernels"], "roofline": tr["roofline"],
+            line = {"ms_per_step": tr["ms_step"], "step_ms_distribution": tr["latency"],
+                    "kernels": tr["kernels"], "roofline": tr["roofline"],
                     "lmk_row": tr["lmk_row"]}
         else:
             name = {"forward_16k": "train_16k_bf16", "planted_1m": "planted_1m_bf16"}[args.only]
@@ -723,6 +758,7 @@ def main():
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": tr["ms_step"], "profiled_ms_per_step": tr["profiled_ms_step"],
+        "step_ms_distribution": tr["latency"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "fwdbwd_64k_bf16: B=2 H=16 d=64 L=65,536 S=64 (1,024 chunks) top-8 D=1,024, "
