@@ -224,8 +224,11 @@ def mfma_roofline(kern, units, dom, tag=None):
     fl = units * S * fpu[dom]
     ach = fl / (kern[dom]["avg_ms"] * 1e-3) / 1e12
     key = profile_key(dom, tag)
+    traffic = measured_traffic(key)
     return {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": ach / BF16_PEAK_TFLOPS, "traffic": measured_traffic(key), "counters": measured_mfma(key),
+            "frac": ach / BF16_PEAK_TFLOPS, "traffic": traffic, "counters": measured_mfma(key),
+            # the rate the traffic beyond the L2 moves at in this launch
+            "traffic_GBps": None if traffic is None else traffic / (kern[dom]["avg_ms"] * 1e-3) / 1e9,
             "algorithmic_flops_per_launch": fl, "avg_launch_ms": kern[dom]["avg_ms"]}
 
 
@@ -644,7 +647,8 @@ def cpu_baseline(w, t, heads=16):
 
 def measured_peaks(dev):
     """On-device reference rates: a streaming read of 4 GiB (the HBM rate a plain
-    coalesced read reaches) and a register-resident bf16 32x32x16 product loop (the
+    coalesced read reaches), gathers of random 16 KiB tiles (the rate the attention
+    kernels' L2 misses can reach in their access pattern) and a register-resident bf16 32x32x16 product loop (the
     matrix-core rate at the running clock)."""
     import torch
     path = os.path.join(ROOT, "peaks", "libpeaks.so")
@@ -670,6 +674,26 @@ def measured_peaks(dev):
         read()
     ms = timed(read, 10, stream) / 10
     read_gbs = nbytes / (ms * 1e-3) / 1e9
+    # random 16 KiB tiles, 4 GiB of reads per call, from a 128 MiB working set (the
+    # K/V of the eight (batch, head) slices the XCDs work on at a time at 64K: past
+    # the 4 MiB L2s, inside the 256 MiB last-level cache) and from all 4 GiB
+    L.peaks_tile_gather.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                    ctypes.c_void_p]
+    gen = torch.Generator().manual_seed(7)
+    gather = {}
+    n_reads = nbytes // 16384
+    for name, set_bytes in (("128MiB", 128 << 20), ("4GiB", nbytes)):
+        idx = torch.randint(0, set_bytes // 16384, (n_reads,), generator=gen, dtype=torch.int32).to(dev)
+
+        def gat(idx=idx):
+            assert L.peaks_tile_gather(ctypes.c_void_p(buf.data_ptr()), ctypes.c_void_p(idx.data_ptr()), n_reads,
+                                       blocks, ctypes.c_void_p(sink.data_ptr()), sp) == 0
+
+        for _ in range(3):
+            gat()
+        gms = timed(gat, 10, stream) / 10
+        gather[name] = n_reads * 16384 / (gms * 1e-3) / 1e9
+        del idx
     del buf
     iters = 20000
     mblocks = cus * 2                                  # 8 waves per CU, two per SIMD
@@ -682,6 +706,7 @@ def measured_peaks(dev):
     flops = mblocks * 4 * iters * 8 * 32768
     torch.cuda.empty_cache()
     return {"stream_read_GBps": read_gbs, "stream_read_frac_of_spec": read_gbs / HBM_PEAK_GBS,
+            "tile_gather_GBps": {"working_set_" + k: v for k, v in gather.items()},
             "mfma_bf16_TFLOPs": flops / (mms * 1e-3) / 1e12,
             "mfma_bf16_frac_of_spec": flops / (mms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
             "compute_units": cus, "read_bytes": nbytes}
@@ -802,7 +827,14 @@ def main():
             line["decode_host_kv"] = bench_decode_host_kv(args, dev, gca)
     if not args.no_peaks:
         log("on-device reference rates")
-        line["peaks_measured"] = measured_peaks(dev)
+        line["peaks_measured"] = pk = measured_peaks(dev)
+        if pk is not None:
+            # the attention kernels' traffic rate against the measured tile-gather rate
+            gat = pk["tile_gather_GBps"]["working_set_128MiB"]
+            for roof in [line["roofline"]] + [line[k]["roofline"] for k in ("forward_16k", "planted_1m")
+                                              if k in line]:
+                if roof.get("traffic_GBps") is not None:
+                    roof["traffic_frac_of_measured_gather"] = roof["traffic_GBps"] / gat
     for key, fn in baselines:
         log(f"cpu baseline ({key})")
         if key == "cpu_baseline":

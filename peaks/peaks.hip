@@ -1,5 +1,6 @@
 // On-device reference rates for the roofline peaks: a streaming read of a large
-// buffer (the HBM rate this chip delivers to a plain coalesced read) and a loop
+// buffer (the HBM rate this chip delivers to a plain coalesced read), a gather of
+// random 16 KiB tiles (the rate reads that miss the L2 reach in that pattern), and a loop
 // of dense bf16 32x32x16 matrix-core products held in registers (the matrix-core
 // rate at the clock the chip runs).  Measurement aids only; not part of libgca.
 #include <hip/hip_runtime.h>
@@ -25,6 +26,23 @@ __global__ __launch_bounds__(256) void stream_read_kernel(const u32x4* __restric
     acc ^= a ^ b ^ c ^ d;
   }
   for (; i < n; i += stride) acc ^= __builtin_nontemporal_load(p + i);
+  const uint32_t f = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+  if (f == key) sink[0] = f;
+}
+
+// Each workgroup reads whole 16 KiB tiles chosen by idx[] (tile t at p + idx[t] *
+// 16 KiB), 64 bytes per thread per tile: the access pattern of the attention
+// kernels' gathers of one retrieved chunk's K or V pair, without the compute.
+__global__ __launch_bounds__(256) void tile_gather_kernel(const u32x4* __restrict__ p,
+                                                          const int32_t* __restrict__ idx, int n, uint32_t key,
+                                                          uint32_t* __restrict__ sink) {
+  u32x4 acc = u32x4{0u, 0u, 0u, 0u};
+  for (int t = blockIdx.x; t < n; t += gridDim.x) {
+    const u32x4* tile = p + (int64_t)idx[t] * 1024;
+    const u32x4 a = tile[threadIdx.x], b = tile[threadIdx.x + 256];
+    const u32x4 c = tile[threadIdx.x + 512], d = tile[threadIdx.x + 768];
+    acc ^= a ^ b ^ c ^ d;
+  }
   const uint32_t f = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
   if (f == key) sink[0] = f;
 }
@@ -63,6 +81,14 @@ extern "C" {
 int peaks_stream_read(const void* p, int64_t n16, int blocks, void* sink, hipStream_t stream) {
   hipLaunchKernelGGL(stream_read_kernel, dim3(blocks), dim3(256), 0, stream, (const u32x4*)p, n16, 0x9E3779B9u,
                      (uint32_t*)sink);
+  return (int)hipGetLastError();
+}
+
+// Launch the gather of n 16 KiB tiles at p, tile t being p + idx[t] * 16 KiB
+// (idx: n device int32 values, each below the number of whole tiles at p).
+int peaks_tile_gather(const void* p, const void* idx, int n, int blocks, void* sink, hipStream_t stream) {
+  hipLaunchKernelGGL(tile_gather_kernel, dim3(blocks), dim3(256), 0, stream, (const u32x4*)p, (const int32_t*)idx, n,
+                     0x9E3779B9u, (uint32_t*)sink);
   return (int)hipGetLastError();
 }
 
