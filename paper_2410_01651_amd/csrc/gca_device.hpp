@@ -464,6 +464,44 @@ __device__ __forceinline__ int64_t xcd_swizzle(int64_t bid, int64_t grid) {
   return (bid & 7) * per + (bid >> 3);
 }
 
+// Work order of the persistent query-chunk streams (S = streams per XCD; the
+// item list is (b, h, c) in order).
+// * Ranges (default): XCD x owns the x-th eighth of the items and its streams
+//   sweep that range side by side (stream t takes items lo + t, lo + t + S, ...),
+//   so each XCD works on a run of consecutive query chunks of one (batch, head)
+//   slice and carries its L2 contents from one run to the next; the eight XCDs'
+//   slices together are the last-level cache's working set.
+// * Windows: the chip sweeps the items in windows of 8 S consecutive items;
+//   within window r, XCD x takes the S items of part (x + r) mod 8.  The whole
+//   chip then works on one slice at a time, for slices whose key/value chunks,
+//   eight at once, would not fit the last-level cache; the rotation deals every
+//   XCD the early (short-history) and late parts of the windows alike.
+struct StreamOrder {
+  int64_t S, st, lo, hi;  // streams per XCD; this stream within its XCD; the XCD's range
+  int64_t nwork;
+  int xcd;
+  bool windows;
+  __device__ __forceinline__ StreamOrder(int64_t S_, int64_t st_, int xcd_, int64_t nwork_, bool windows_)
+      : S(S_), st(st_), lo(nwork_ * xcd_ / 8), hi(nwork_ * (xcd_ + 1) / 8), nwork(nwork_), xcd(xcd_),
+        windows(windows_) {}
+  __device__ __forceinline__ int64_t item(int64_t r) const {
+    return windows ? (r * 8 + ((xcd + r) & 7)) * S + st : lo + st + r * S;
+  }
+  // number of items of this stream (items grow with r)
+  __device__ __forceinline__ int64_t length() const {
+    if (!windows) return lo + st < hi ? (hi - lo - st + S - 1) / S : 0;
+    const int64_t full = nwork / (8 * S);
+    return full + (item(full) < nwork ? 1 : 0);
+  }
+};
+
+// The window order pays when the key/value chunks of eight (batch, head) slices
+// (one per XCD under the range order) exceed the 256 MiB last-level cache.
+inline bool use_window_order(int64_t nKV, size_t elem_bytes) {
+  const int64_t slice_bytes = nKV * (int64_t)(2 * kS * kD) * (int64_t)elem_bytes;
+  return 8 * slice_bytes > (int64_t(256) << 20);
+}
+
 // Position (b, h, c) of work item w = (b * H + h) * nQ + c, advanced a fixed
 // number of chunks at a time so that persistent loops need no divisions.
 struct Geo {

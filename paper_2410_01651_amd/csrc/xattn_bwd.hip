@@ -54,6 +54,7 @@ struct BwdParams {
   int64_t nQ, nKV;
   int causal;
   float attn_scale;
+  bool windows;  // dQ stream order (StreamOrder), the forward's
 };
 
 // the LMK row's per-chunk exchange between the two waves of a dQ pair
@@ -191,7 +192,7 @@ __global__ __launch_bounds__(256) void csr_sort_kernel(const int* __restrict__ o
 // wave owning 32 query tokens.  Per retrieved chunk it writes D_s and the
 // shifted log-sum-exp used by the key-stationary pass, and the wave's partial
 // sum of D_s for dw; dQ stays in registers until the chunk ends.  The work order
-// is the forward's (each XCD sweeps consecutive chunks of one slice at a time).
+// is the forward's (StreamOrder, chosen the same way).
 // STAGE (k <= kDqStageK): the per-(token, slot) values are staged in LDS and
 // stored once per chunk.
 constexpr int kDqStageK = 8;
@@ -216,18 +217,17 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
-  const int64_t stride = (int64_t)(gridDim.x >> 3) * kPairs;
   const int xcd = (int)(blockIdx.x & 7);
-  const int64_t r_lo = nwork * xcd / 8, r_hi = nwork * (xcd + 1) / 8;
   const int64_t st_wg = (int64_t)(blockIdx.x >> 3) * kPairs;
-  auto stream_len = [&](int64_t st) -> int64_t {
-    return r_lo + st < r_hi ? (r_hi - r_lo - st + stride - 1) / stride : 0;
+  auto order_of = [&](int q) {
+    return StreamOrder((int64_t)(gridDim.x >> 3) * kPairs, st_wg + q, xcd, nwork, p.windows);
   };
-  const int64_t my_n = stream_len(st_wg + pair);
+  const StreamOrder ord = order_of(pair);
+  const int64_t my_n = ord.length();
   int64_t nch = 0;  // all pairs of the workgroup run nch chunks of rounds
-  for (int q = 0; q < kPairs; ++q) nch = max(nch, stream_len(st_wg + q));
+  for (int q = 0; q < kPairs; ++q) nch = max(nch, order_of(q).length());
   if (nch == 0) return;
-  const int64_t c_begin = r_lo + st_wg + pair;
+  const int64_t c_begin = ord.item(0);
   const int K = p.K;
   const int qi = 32 * half + (lane & 31);
   const int l32 = lane & 31;
@@ -278,10 +278,15 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
   Frag<T> qf[4], df[4];  // the current chunk's Q and dO rows of this lane's query
   Meta meta{-1, 0.f};
   Geo g0(c_begin, p.nQ, p.H);
-  Geo g1 = g0;
-  g1.next(p.nQ, p.H, stride);
-  Geo g2 = g1;
-  g2.next(p.nQ, p.H, stride);
+  Geo g1 = g0, g2 = g0;  // (the range order steps without divisions)
+  if (p.windows) {
+    g1 = Geo(ord.item(1), p.nQ, p.H);
+    g2 = Geo(ord.item(2), p.nQ, p.H);
+  } else {
+    g1.next(p.nQ, p.H, ord.S);
+    g2 = g1;
+    g2.next(p.nQ, p.H, ord.S);
+  }
   auto load_qdo = [&](const Geo& g, Frag<T>* qd, Frag<T>* dd, int xbuf) __device__ {
     const int64_t row = tok_of(g) + qi;
     const T* qr = reinterpret_cast<const T*>(p.q) + row * kD;
@@ -587,7 +592,10 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     g1a = zero16();
     g0 = g1;
     g1 = g2;
-    g2.next(p.nQ, p.H, stride);
+    if (p.windows)
+      g2 = Geo(ord.item(ci + 3), p.nQ, p.H);
+    else
+      g2.next(p.nQ, p.H, ord.S);
   }
 }
 
@@ -1146,6 +1154,7 @@ hipError_t launch_xattn_bwd(const Shape& s, const void* q, const void* k, const 
   p.nQ = s.nQ; p.nKV = s.nKV;
   p.causal = s.causal;
   p.attn_scale = s.attn_scale;
+  p.windows = use_window_order(s.nKV, s.bf16 ? 2 : 4);
   return s.bf16 ? launch_bwd_t<__bf16>(s, p, dsel, lmk_q, lmk_k, dlmk_q, dlmk_k, stream)
                 : launch_bwd_t<float>(s, p, dsel, lmk_q, lmk_k, dlmk_q, dlmk_k, stream);
 }

@@ -52,6 +52,7 @@ struct FwdParams {
   int64_t nQ, nKV, nwork;
   int causal;
   float attn_scale;
+  bool windows;  // stream order (StreamOrder)
 };
 
 // the LMK row's per-chunk exchange between the two waves of a pair
@@ -101,24 +102,19 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hh = lane >> 5;
   const int pair = wave >> 1, half = wave & 1;
   // Work order: workgroups are dealt to the eight XCDs round-robin (blockIdx mod
-  // 8) and each wave pair is a stream of query chunks.  XCD x owns the x-th eighth
-  // of the chunks and its streams sweep that range side by side (stream t takes
-  // chunks begin + t, + t + S, ...; S = the XCD's stream count), so at any time
-  // an XCD works on a window of consecutive query chunks of one (batch, head)
-  // slice, whose retrieved key/value chunks its L2 and the shared last-level cache
-  // keep resident across the queries that reuse them.
-  const int64_t stride = (int64_t)(gridDim.x >> 3) * kPairs;
+  // 8) and each wave pair is a stream of query chunks in StreamOrder (XCD ranges,
+  // or chip-wide windows for long slices).
   const int xcd = (int)(blockIdx.x & 7);
-  const int64_t r_lo = p.nwork * xcd / 8, r_hi = p.nwork * (xcd + 1) / 8;
   const int64_t st_wg = (int64_t)(blockIdx.x >> 3) * kPairs;
-  auto stream_len = [&](int64_t st) -> int64_t {
-    return r_lo + st < r_hi ? (r_hi - r_lo - st + stride - 1) / stride : 0;
+  auto order_of = [&](int q) {
+    return StreamOrder((int64_t)(gridDim.x >> 3) * kPairs, st_wg + q, xcd, p.nwork, p.windows);
   };
-  const int64_t my_n = stream_len(st_wg + pair);
+  const StreamOrder ord = order_of(pair);
+  const int64_t my_n = ord.length();
   int64_t nch = 0;  // all pairs of the workgroup run nch chunks of rounds
-  for (int q = 0; q < kPairs; ++q) nch = max(nch, stream_len(st_wg + q));
+  for (int q = 0; q < kPairs; ++q) nch = max(nch, order_of(q).length());
   if (nch == 0) return;
-  const int64_t c_begin = r_lo + st_wg + pair;
+  const int64_t c_begin = ord.item(0);
   const int K = p.topk;
   const int qi = 32 * half + (lane & 31);  // this lane's query token within a chunk
   const float sc = p.attn_scale * kLog2e;
@@ -172,10 +168,15 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
   Frag<T> qf[4], qn[4];
   RowMeta meta{-1, -INFINITY};
   Geo g0(c_begin, p.nQ, p.H);  // geometry of the current chunk and of the two after it
-  Geo g1 = g0;
-  g1.next(p.nQ, p.H, stride);
-  Geo g2 = g1;
-  g2.next(p.nQ, p.H, stride);
+  Geo g1 = g0, g2 = g0;  // (the range order steps without divisions)
+  if (p.windows) {
+    g1 = Geo(ord.item(1), p.nQ, p.H);
+    g2 = Geo(ord.item(2), p.nQ, p.H);
+  } else {
+    g1.next(p.nQ, p.H, ord.S);
+    g2 = g1;
+    g2.next(p.nQ, p.H, ord.S);
+  }
   if (my_n > 0) {
     int64_t ro;
     bool ex, ow;
@@ -364,7 +365,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     const bool live = ci < my_n, live_next = ci + 1 < my_n;
     const int buf = (int)(ci & 1);
     const int n = live ? sN[pair][buf] : 0;
-    const int64_t w = c_begin + ci * stride;
+    const int64_t w = ord.item(ci), w_next = ord.item(ci + 1);
     const int64_t tok0 = w * SQ;
     for (int u = 0; u < K; ++u) {
       wait_vmem<0>();
@@ -382,11 +383,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
         }
         if (live_next) {
           if constexpr (!XR) {
-            const T* qr = qrow_ptr(w + stride);
+            const T* qr = qrow_ptr(w_next);
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) qn[kb] = load_frag(qr + 16 * kb + 8 * hh);
           } else if (xh == 0) {
-            load_qx(w + stride, buf ^ 1);
+            load_qx(w_next, buf ^ 1);
           }
           if (half == 0) make_slots(meta, g1, buf ^ 1);
           if (ci + 2 < my_n) {
@@ -415,7 +416,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     // the fragments (the registers of a prefetch are what the row's own work
     // needs); the next round's wait covers them
     if (XR && live_next) {
-      const T* qr = qrow_ptr(w + stride);
+      const T* qr = qrow_ptr(w_next);
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) qf[kb] = load_frag(qr + 16 * kb + 8 * hh);
     }
@@ -473,7 +474,10 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void xattn_fwd_kernel(FwdParams
     o1 = zero16();
     g0 = g1;
     g1 = g2;
-    g2.next(p.nQ, p.H, stride);
+    if (p.windows)
+      g2 = Geo(ord.item(ci + 3), p.nQ, p.H);
+    else
+      g2.next(p.nQ, p.H, ord.S);
   }
 }
 
@@ -492,6 +496,7 @@ hipError_t launch_xattn_fwd(const Shape& s, const void* q, const void* k, const 
   p.nwork = (int64_t)s.B * s.H * s.nQ;
   p.causal = s.causal;
   p.attn_scale = s.attn_scale;
+  p.windows = use_window_order(s.nKV, s.bf16 ? 2 : 4);
   const bool xr = s.Sq != kS;
   // persistent workgroups: kWgPerCu per CU, a multiple of 8 (one share per XCD),
   // each running kPairs chunk streams

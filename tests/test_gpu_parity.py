@@ -170,6 +170,11 @@ BWD = [
     ("fwdbwd_64k_bf16", dict(B=1, H=2, Hr=2, D=128, n_chunks=33, topk=5), False),
     ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=700, topk=1), False),    # k = 1, uneven streams
     ("tiny_fp32_1k", dict(B=1, H=2, n_chunks=600, topk=1, whole_reseed=False), True),
+    # slices long enough for the chip-wide window order of the query-chunk streams
+    # (eight slices' K/V above 256 MiB), with partial windows and a slice boundary
+    # inside a window
+    ("tiny_fp32_1k", dict(B=1, H=1, n_chunks=1100, topk=2, whole_reseed=False), False),
+    ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=2100, topk=4), False),
     ("decode_16m_bf16", dict(H=2, n_chunks=300, planted=0, backward=True, device_kv=False), False),
     ("decode_16m_bf16", dict(H=2, n_chunks=100, topk=4, planted=0, dtype="fp32", backward=True,
                              device_kv=False), False),
@@ -465,6 +470,7 @@ LMK = [
     ("train_16k_bf16", dict(B=1, H=2, n_chunks=65, topk=32), True),
     ("tiny_fp32_1k", dict(B=2, H=3, n_chunks=37, topk=6, whole_reseed=False), True),
     ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=700, topk=3), False),
+    ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=2100, topk=3), False),   # window stream order
 ]
 
 
