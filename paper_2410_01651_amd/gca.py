@@ -277,20 +277,30 @@ def grouped_xattn_fwd(p: Problem, q, k, v, idx, sel, out=None, lse=None, w=None,
 
 def grouped_xattn_bwd(p: Problem, q, k, v, idx, sel, lse, dout, lmk_q=None, lmk_k=None,
                       landmark_grads=True, ws=None, grads=None, stream=None):
-    """Returns dict dq, dk, dv, dsel and (if landmark_grads) dlmk_q, dlmk_k."""
+    """Returns dict dq, dk, dv, dsel and (if landmark_grads) dlmk_q, dlmk_k.
+    landmark_grads: True (both), False (neither), or a collection of the names
+    "dlmk_q" / "dlmk_k" to request one of them."""
     torch = _torch()
     sh, dt = shapes(p), _elem_dtype(p)
     dev = q.device
     g = dict(grads or {})
+    if landmark_grads is True:
+        wanted = ("dlmk_q", "dlmk_k")
+    elif not landmark_grads:
+        wanted = ()
+    else:
+        wanted = tuple(landmark_grads)
+        if not set(wanted) <= {"dlmk_q", "dlmk_k"}:
+            raise ValueError(f"landmark_grads names must be dlmk_q / dlmk_k, got {wanted}")
+    landmark_grads = bool(wanted)
     with _alloc_on(stream):
         for name, shape, gdt in (("dq", sh.q, dt), ("dk", sh.kv, dt), ("dv", sh.kv, dt),
                                  ("dsel", sh.rows, torch.float32)):
             if name not in g:
                 g[name] = torch.empty(shape, dtype=gdt, device=dev)
-        if landmark_grads:
-            for name, shape in (("dlmk_q", sh.lmk_q), ("dlmk_k", sh.lmk_k)):
-                if name not in g:
-                    g[name] = torch.empty(shape, dtype=torch.float32, device=dev)
+        for name, shape in (("dlmk_q", sh.lmk_q), ("dlmk_k", sh.lmk_k)):
+            if name in wanted and name not in g:
+                g[name] = torch.empty(shape, dtype=torch.float32, device=dev)
         if ws is None:
             ws, nbytes = workspace(p, OP_BACKWARD, dev)
         else:
@@ -304,8 +314,8 @@ def grouped_xattn_bwd(p: Problem, q, k, v, idx, sel, lse, dout, lmk_q=None, lmk_
         _ptr(g["dsel"], "dsel", torch.float32, sh.rows),
         _ptr(lmk_q, "lmk_q", dt, sh.lmk_q) if landmark_grads else None,
         _ptr(lmk_k, "lmk_k", dt, sh.lmk_k) if landmark_grads else None,
-        _ptr(g.get("dlmk_q"), "dlmk_q", torch.float32, sh.lmk_q),
-        _ptr(g.get("dlmk_k"), "dlmk_k", torch.float32, sh.lmk_k),
+        _ptr(g.get("dlmk_q") if "dlmk_q" in wanted else None, "dlmk_q", torch.float32, sh.lmk_q),
+        _ptr(g.get("dlmk_k") if "dlmk_k" in wanted else None, "dlmk_k", torch.float32, sh.lmk_k),
         _ptr(ws, "workspace"), ctypes.c_size_t(nbytes), _stream(stream)))
     return g
 

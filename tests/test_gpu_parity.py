@@ -244,6 +244,29 @@ def test_backward_deterministic(dev):
         assert np.array_equal(host64(g1[key]), host64(g2[key])), key
 
 
+@pytest.mark.parametrize("name,kw", [("fwdbwd_64k_bf16", dict(B=2, H=4, n_chunks=40, topk=8)),
+                                     ("tiny_fp32_1k", dict(B=1, H=2, n_chunks=20, topk=3, whole_reseed=False)),
+                                     ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=12, topk=4, D=8192))])
+def test_landmark_gradients_one_at_a_time(dev, name, kw):
+    """dlmk_q alone, dlmk_k alone and both (one launch whose dlmk_k blocks form
+    dsel themselves) give the same bits for every output."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case(name, **kw)
+    if "dout" not in inp:
+        inp["dout"] = gi.draw_slices(w, "dout", (w.B, w.H, w.Lq, w.d))
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    args = (p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"], t["lmk_q"], t["lmk_k"])
+    both = gca.grouped_xattn_bwd(*args)
+    only_q = gca.grouped_xattn_bwd(*args, landmark_grads=("dlmk_q",))
+    only_k = gca.grouped_xattn_bwd(*args, landmark_grads=("dlmk_k",))
+    assert "dlmk_k" not in only_q and "dlmk_q" not in only_k
+    for part in (only_q, only_k):
+        for key in part:
+            assert np.array_equal(host64(part[key]), host64(both[key])), key
+
+
 def test_xattn_only_entry_points(dev):
     """gca_grouped_xattn_fwd / _bwd driven with an index set chosen by the caller,
     including pad slots in the middle and an out-of-range index (treated as a pad)."""
