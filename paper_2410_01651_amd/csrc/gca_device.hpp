@@ -340,6 +340,25 @@ template <> __device__ __forceinline__ f32x8 frag_e0<float>(float x) {
   f.hi = f32x4{0.f, 0.f, 0.f, 0.f};
   return f;
 }
+template <typename T> __device__ __forceinline__ Frag<T> zero_frag();
+template <> __device__ __forceinline__ bf16x8 zero_frag<__bf16>() { return frag_e0<__bf16>(0.f); }
+template <> __device__ __forceinline__ f32x8 zero_frag<float>() { return frag_e0<float>(0.f); }
+// Entries 0 .. n-1 of f kept, the rest set to 0.
+template <typename T> __device__ __forceinline__ Frag<T> frag_prefix(Frag<T> f, int n);
+template <> __device__ __forceinline__ bf16x8 frag_prefix<__bf16>(bf16x8 f, int n) {
+#pragma unroll
+  for (int m = 0; m < 8; ++m)
+    if (m >= n) f[m] = (__bf16)0.f;
+  return f;
+}
+template <> __device__ __forceinline__ f32x8 frag_prefix<float>(f32x8 f, int n) {
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    if (m >= n) f.lo[m] = 0.f;
+    if (m + 4 >= n) f.hi[m] = 0.f;
+  }
+  return f;
+}
 // Entries x[c .. c+7]: meets a row fragment (contraction along the row).
 template <typename T>
 __device__ __forceinline__ Frag<T> vec_frag(const T* x, int c) {

@@ -620,6 +620,11 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
   __shared__ __attribute__((aligned(16))) T ring[2 * ENTRY];
   constexpr int NE = 256;  // retrievers staged in LDS per batch
   __shared__ int sE[NE];
+  // LMK rows: up to kXGroup retrievers' rows staged for one padded contraction
+  // step: Q and dO rows transposed ([d][retriever]) and, per key, w P and dS
+  // ([key][retriever])
+  constexpr int kXGroup = 8;
+  __shared__ __attribute__((aligned(16))) T sXst[XR ? 4 : 1][XR ? kD : 1][kXGroup];
 
   const int64_t wid = xcd_swizzle(blockIdx.x, gridDim.x);
   if (wid >= nwork) return;
@@ -728,69 +733,125 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
     }
   };
 
-  auto run = [&](int slot) __device__ {
+  auto run = [&](int slot, int u, bool last) __device__ {
     const T* sQ = ring + slot * ENTRY;
     const T* sO = sQ + TILE;
     const uint32_t qo = (uint32_t)slot * kEntryB, oo = qo + kTileB;
     const float* sL = reinterpret_cast<const float*>(sQ + 2 * TILE);
     const float* sD = sL + kS;
-    // accumulator row i of a 32-query tile holds query 32*qt + 8*(i/4) + 4*hh + i%4,
-    // so four consecutive registers take one 16-byte column read.
-    // dP - D = dO V^T + (-D): the accumulators start from the stored -D column
-    f32x16 p0, p1;
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 d0 = *reinterpret_cast<const f32x4*>(sD + 8 * g + 4 * hh);
-      const f32x4 d1 = *reinterpret_cast<const f32x4*>(sD + 32 + 8 * g + 4 * hh);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        p0[4 * g + r] = d0[r];
-        p1[4 * g + r] = d1[r];
-      }
-    }
-    // S = Q K^T for this wave's keys (queries 0-31 in s0, 32-63 in s1), and dP
-    f32x16 s0 = zero16(), s1 = zero16();
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      mma32(s0, row_frag(sQ, qo, kb, 0), kf[kb]);
-      mma32(s1, row_frag(sQ, qo, kb, 1), kf[kb]);
-    }
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      mma32(p0, row_frag(sO, oo, kb, 0), vf[kb]);
-      mma32(p1, row_frag(sO, oo, kb, 1), vf[kb]);
-    }
-    // w P (fp32), then dS = w P o (dP - D)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4 l0 = *reinterpret_cast<const f32x4*>(sL + 8 * g + 4 * hh);
-      const f32x4 l1 = *reinterpret_cast<const f32x4*>(sL + 32 + 8 * g + 4 * hh);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        s0[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s0[4 * g + r], sc, -l0[r]));
-        s1[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s1[4 * g + r], sc, -l1[r]));
-      }
-    }
-    Frag<T> wp[4], ds[4];
-    frag_from_acc(wp[0], s0, 0, 1.f);
-    frag_from_acc(wp[1], s0, 1, 1.f);
-    frag_from_acc(wp[2], s1, 0, 1.f);
-    frag_from_acc(wp[3], s1, 1, 1.f);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      p0[i] *= s0[i];
-      p1[i] *= s1[i];
-    }
-    frag_from_acc(ds[0], p0, 0, 1.f);
-    frag_from_acc(ds[1], p0, 1, 1.f);
-    frag_from_acc(ds[2], p1, 0, 1.f);
-    frag_from_acc(ds[3], p1, 1, 1.f);
     if constexpr (XR) {
-      // the LMK row against this wave's keys: its score and dP for key kr (row
+      // with the LMK row the 64 queries go in two halves of 32, one after the
+      // other (the same products in the same order per accumulator, half the
+      // score and dP registers live at a time)
+#pragma unroll
+      for (int qh = 0; qh < 2; ++qh) {
+        f32x16 pp, ss = zero16();
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 d0 = *reinterpret_cast<const f32x4*>(sD + 32 * qh + 8 * g + 4 * hh);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) pp[4 * g + r] = d0[r];
+        }
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) mma32(ss, row_frag(sQ, qo, kb, qh), kf[kb]);
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) mma32(pp, row_frag(sO, oo, kb, qh), vf[kb]);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 l0 = *reinterpret_cast<const f32x4*>(sL + 32 * qh + 8 * g + 4 * hh);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) ss[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(ss[4 * g + r], sc, -l0[r]));
+        }
+        Frag<T> wp2[2], ds2[2];
+        frag_from_acc(wp2[0], ss, 0, 1.f);
+        frag_from_acc(wp2[1], ss, 1, 1.f);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) pp[i] *= ss[i];
+        frag_from_acc(ds2[0], pp, 0, 1.f);
+        frag_from_acc(ds2[1], pp, 1, 1.f);
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          mma32(dv0, col_frag(sO, oo, 2 * qh + kk, 0), wp2[kk]);
+          mma32(dv1, col_frag(sO, oo, 2 * qh + kk, 1), wp2[kk]);
+        }
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+          mma32(dk0, col_frag(sQ, qo, 2 * qh + kk, 0), ds2[kk]);
+          mma32(dk1, col_frag(sQ, qo, 2 * qh + kk, 1), ds2[kk]);
+        }
+      }
+    } else {
+      // accumulator row i of a 32-query tile holds query 32*qt + 8*(i/4) + 4*hh + i%4,
+      // so four consecutive registers take one 16-byte column read.
+      // dP - D = dO V^T + (-D): the accumulators start from the stored -D column
+      f32x16 p0, p1;
+  #pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 d0 = *reinterpret_cast<const f32x4*>(sD + 8 * g + 4 * hh);
+        const f32x4 d1 = *reinterpret_cast<const f32x4*>(sD + 32 + 8 * g + 4 * hh);
+  #pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          p0[4 * g + r] = d0[r];
+          p1[4 * g + r] = d1[r];
+        }
+      }
+      // S = Q K^T for this wave's keys (queries 0-31 in s0, 32-63 in s1), and dP
+      f32x16 s0 = zero16(), s1 = zero16();
+  #pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        mma32(s0, row_frag(sQ, qo, kb, 0), kf[kb]);
+        mma32(s1, row_frag(sQ, qo, kb, 1), kf[kb]);
+      }
+  #pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        mma32(p0, row_frag(sO, oo, kb, 0), vf[kb]);
+        mma32(p1, row_frag(sO, oo, kb, 1), vf[kb]);
+      }
+      // w P (fp32), then dS = w P o (dP - D)
+  #pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 l0 = *reinterpret_cast<const f32x4*>(sL + 8 * g + 4 * hh);
+        const f32x4 l1 = *reinterpret_cast<const f32x4*>(sL + 32 + 8 * g + 4 * hh);
+  #pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          s0[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s0[4 * g + r], sc, -l0[r]));
+          s1[4 * g + r] = __builtin_amdgcn_exp2f(fmaf(s1[4 * g + r], sc, -l1[r]));
+        }
+      }
+      Frag<T> wp[4], ds[4];
+      frag_from_acc(wp[0], s0, 0, 1.f);
+      frag_from_acc(wp[1], s0, 1, 1.f);
+      frag_from_acc(wp[2], s1, 0, 1.f);
+      frag_from_acc(wp[3], s1, 1, 1.f);
+  #pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        p0[i] *= s0[i];
+        p1[i] *= s1[i];
+      }
+      frag_from_acc(ds[0], p0, 0, 1.f);
+      frag_from_acc(ds[1], p0, 1, 1.f);
+      frag_from_acc(ds[2], p1, 0, 1.f);
+      frag_from_acc(ds[3], p1, 1, 1.f);
+      // dV^T += dO^T (w P) and dK^T += Q^T dS  (contractions over the 64 queries)
+  #pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        mma32(dv0, col_frag(sO, oo, kb, 0), wp[kb]);
+        mma32(dv1, col_frag(sO, oo, kb, 1), wp[kb]);
+      }
+  #pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        mma32(dk0, col_frag(sQ, qo, kb, 0), ds[kb]);
+        mma32(dk1, col_frag(sQ, qo, kb, 1), ds[kb]);
+      }
+    }
+    if constexpr (XR) {
+      // the LMK row against this wave's keys, after the tile's products (so its
+      // registers do not add to theirs): its score and dP for key kr (row
       // fragments of K and V held in registers, the dimension halves added
-      // across l ^ 32), w P and dS, then dV^T += dO_x^T (w P_x) and
-      // dK^T += q_x^T dS_x as one more contraction step whose only nonzero
-      // entry is the first
+      // across l ^ 32), w P and dS, staged with the row's Q and dO as retriever
+      // u % kXGroup; every kXGroup retrievers (and at the end of a batch) the
+      // staged rows enter dV^T += dO_X^T (w P_X) and dK^T += Q_X^T dS_X as one
+      // contraction step padded to 16 with zeros
       __builtin_amdgcn_sched_barrier(0);
       const T* sqx = sQ + XOFF;
       const T* sdx = sqx + kD;
@@ -804,28 +865,33 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
       a = sum_xor32(a);
       b = sum_xor32(b);
       const float wpx = __builtin_amdgcn_exp2f(fmaf(a, sc, -slx[0]));
-      const bool e0 = hh == 0;
-      const float xw = e0 ? wpx : 0.f, xd = e0 ? wpx * (b + slx[1]) : 0.f;
-      const int c0 = lane & 31;
-      __builtin_amdgcn_sched_barrier(0);
-      mma32(dv0, frag_e0<T>(e0 ? to_f32(sdx[c0]) : 0.f), frag_e0<T>(xw));
-      __builtin_amdgcn_sched_barrier(0);
-      mma32(dv1, frag_e0<T>(e0 ? to_f32(sdx[32 + c0]) : 0.f), frag_e0<T>(xw));
-      __builtin_amdgcn_sched_barrier(0);
-      mma32(dk0, frag_e0<T>(e0 ? to_f32(sqx[c0]) : 0.f), frag_e0<T>(xd));
-      __builtin_amdgcn_sched_barrier(0);
-      mma32(dk1, frag_e0<T>(e0 ? to_f32(sqx[32 + c0]) : 0.f), frag_e0<T>(xd));
-    }
-    // dV^T += dO^T (w P) and dK^T += Q^T dS  (contractions over the 64 queries)
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      mma32(dv0, col_frag(sO, oo, kb, 0), wp[kb]);
-      mma32(dv1, col_frag(sO, oo, kb, 1), wp[kb]);
-    }
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      mma32(dk0, col_frag(sQ, qo, kb, 0), ds[kb]);
-      mma32(dk1, col_frag(sQ, qo, kb, 1), ds[kb]);
+      const float xd = wpx * (b + slx[1]);
+      const int e = u % kXGroup;
+      if (hh == 0) {
+        sXst[2][kr][e] = (T)wpx;
+        sXst[3][kr][e] = (T)xd;
+      }
+      sXst[half][lane][e] = (half == 0 ? sqx : sdx)[lane];  // wave 0 the Q row, wave 1 the dO row
+      if (e == kXGroup - 1 || last) {
+        block_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        const int filled = e + 1, r = lane & 31;
+        Frag<T> ad0 = zero_frag<T>(), ad1 = ad0, aq0 = ad0, aq1 = ad0, bp = ad0, bs = ad0;
+        if (hh == 0) {
+          // entries past `filled` hold an earlier group's values or bits never
+          // written: both operands are cut to the filled ones (0 * NaN is NaN)
+          ad0 = frag_prefix<T>(load_frag(&sXst[1][r][0]), filled);
+          ad1 = frag_prefix<T>(load_frag(&sXst[1][32 + r][0]), filled);
+          aq0 = frag_prefix<T>(load_frag(&sXst[0][r][0]), filled);
+          aq1 = frag_prefix<T>(load_frag(&sXst[0][32 + r][0]), filled);
+          bp = frag_prefix<T>(load_frag(&sXst[2][kr][0]), filled);
+          bs = frag_prefix<T>(load_frag(&sXst[3][kr][0]), filled);
+        }
+        mma32(dv0, ad0, bp);
+        mma32(dv1, ad1, bp);
+        mma32(dk0, aq0, bs);
+        mma32(dk1, aq1, bs);
+      }
     }
   };
 
@@ -851,7 +917,7 @@ __global__ __launch_bounds__(kKvThreads, 4) void bwd_dkdv_kernel(BwdParams p, in
       wait_vmem<0>();
       block_barrier();
       if (u + 1 < nb) issue((u + 1) & 1, sE[u + 1]);
-      run(u & 1);
+      run(u & 1, u, u + 1 == nb);
     }
   }
 
