@@ -66,6 +66,20 @@ __device__ __forceinline__ f32x16 zero16() {
   return z;
 }
 
+// x, as a value the compiler cannot prove loop-invariant: an address formed
+// from it is computed where it is used instead of being hoisted and held in
+// registers across a loop (for kernels at the edge of their register budget).
+__device__ __forceinline__ int opaque(int x) {
+  __asm__ volatile("" : "+v"(x));
+  return x;
+}
+
+// Number of set bits of a wave-wide mask below this lane (v_mbcnt: no lane mask
+// is formed or kept in registers).
+__device__ __forceinline__ int lanes_below(uint64_t mask) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
 // ------------------------------------------------------- fragment loads ----
 
 // 8 consecutive elements starting at p (row-major operand, k contiguous).

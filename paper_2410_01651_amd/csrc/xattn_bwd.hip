@@ -259,7 +259,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     const uint64_t mask = __ballot(valid);
     if (lane < 32) sJ[pair][buf][lane] = valid ? m.j : -1;
     if (valid) {
-      const int rk = __popcll(mask & ((1ull << lane) - 1));
+      const int rk = lanes_below(mask);
       sSlot[pair][buf][rk] = lane;
       sJc[pair][buf][rk] = m.j;
       sWc[pair][buf][rk] = m.w;
@@ -288,7 +288,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     g2.next(p.nQ, p.H, ord.S);
   }
   auto load_qdo = [&](const Geo& g, Frag<T>* qd, Frag<T>* dd, int xbuf) __device__ {
-    const int64_t row = tok_of(g) + qi;
+    const int64_t row = tok_of(g) + (XR ? opaque(qi) : qi);
     const T* qr = reinterpret_cast<const T*>(p.q) + row * kD;
     const T* dr = reinterpret_cast<const T*>(p.dout) + row * kD;
 #pragma unroll
@@ -358,6 +358,19 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
   float ox0 = 0.f, ox1 = 0.f;  // LMK row: this lane's partial dQ for d = l%32 and 32 + l%32
   auto run = [&](int slot, int u, float lse_q, float lse_x, int64_t cbase, int64_t t, bool pre, int buf) __device__ {
     const uint32_t co = (uint32_t)slot * 2 * kTileB;
+    // With the LMK row every register counts: the other fragment offsets are
+    // derived from the first two each round by their swizzle's fixed XOR
+    // patterns (key block kb: bits 5-6; transposed halves: bit 6, and rows +8:
+    // bits 4 and 10), instead of being held across the whole loop.
+    uint32_t k0b = kofs[0], t0b = tofs[0][0];
+    if constexpr (XR && kB16) {
+      k0b = (uint32_t)opaque((int)k0b);
+      t0b = (uint32_t)opaque((int)t0b);
+    }
+    auto KO = [&](int kb) -> uint32_t { return (XR && kB16) ? (k0b ^ (uint32_t)(kb << 5)) : kofs[kb]; };
+    auto TO = [&](int dh, int r8) -> uint32_t {
+      return (XR && kB16) ? (t0b ^ (uint32_t)((dh << 6) | (r8 ? 1040 : 0))) : tofs[dh][r8];
+    };
     const int s = __builtin_amdgcn_readlane(ls, u);
     const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lw), u));
     const bool xr = XR && (u & 1) == xh;  // this wave takes the LMK row of slot u
@@ -378,7 +391,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         const Frag<T> xv = vec_frag(vt ? &sX[0].d[buf][0] : &sX[0].q[buf][0], 16 * kk + 8 * hh);
         Frag<T> r0, r1;
         if constexpr (kB16) {
-          const lds_char* kp = lds0 + (kofs[kk] + co) + (vt ? kTileB : 0u);
+          const lds_char* kp = lds0 + (KO(kk) + co) + (vt ? kTileB : 0u);
           r0 = lds_b128_at(kp);
           r1 = lds_b128_at(kp + 32 * kRowB);
         } else {
@@ -408,8 +421,8 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         __builtin_amdgcn_sched_barrier(0);  // one key block's fragments live at a time
         Frag<T> k0, k1;
         if constexpr (kB16) {
-          k0 = lds_tr2(lds0 + (tofs[0][0] + co) + 16 * kb * kRowB, lds0 + (tofs[0][1] + co) + 16 * kb * kRowB);
-          k1 = lds_tr2(lds0 + (tofs[1][0] + co) + 16 * kb * kRowB, lds0 + (tofs[1][1] + co) + 16 * kb * kRowB);
+          k0 = lds_tr2(lds0 + (TO(0, 0) + co) + 16 * kb * kRowB, lds0 + (TO(0, 1) + co) + 16 * kb * kRowB);
+          k1 = lds_tr2(lds0 + (TO(1, 0) + co) + 16 * kb * kRowB, lds0 + (TO(1, 1) + co) + 16 * kb * kRowB);
         } else {
           k0 = lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb);
           k1 = lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, 32 + cb);
@@ -428,7 +441,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       if constexpr (kB16) {
-        const lds_char* kp = lds0 + (kofs[kb] + co);
+        const lds_char* kp = lds0 + (KO(kb) + co);
         mma32(s0, lds_b128_at(kp), qf[kb]);
         mma32(s1, lds_b128_at(kp + 32 * kRowB), qf[kb]);
         mma32(p0, lds_b128_at(kp + kTileB), df[kb]);
@@ -467,9 +480,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       if constexpr (kB16) {
-        mma32(g0a, lds_tr2(lds0 + (tofs[0][0] + co) + 16 * kb * kRowB, lds0 + (tofs[0][1] + co) + 16 * kb * kRowB),
+        mma32(g0a, lds_tr2(lds0 + (TO(0, 0) + co) + 16 * kb * kRowB, lds0 + (TO(0, 1) + co) + 16 * kb * kRowB),
               f[kb]);
-        mma32(g1a, lds_tr2(lds0 + (tofs[1][0] + co) + 16 * kb * kRowB, lds0 + (tofs[1][1] + co) + 16 * kb * kRowB),
+        mma32(g1a, lds_tr2(lds0 + (TO(1, 0) + co) + 16 * kb * kRowB, lds0 + (TO(1, 1) + co) + 16 * kb * kRowB),
               f[kb]);
       } else {
         mma32(g0a, lds_frag_t(sK, 16 * kb + 4 * hh, 16 * kb + 8 + 4 * hh, cb), f[kb]);
@@ -484,8 +497,9 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         sDL[wave][0][s][l32] = dneg;
         sDL[wave][1][s][l32] = lsh;
       } else {
-        p.ws.Dbuf[cbase + s * lq_len + qi] = dneg;
-        p.ws.Lbuf[cbase + s * lq_len + qi] = lsh;
+        const int64_t o = cbase + s * lq_len + (XR ? opaque(qi) : qi);
+        p.ws.Dbuf[o] = dneg;
+        p.ws.Lbuf[o] = lsh;
       }
     }
     // this wave's 32 queries' share of dw[t, s] (and the LMK row's D)
@@ -526,11 +540,11 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
       const float lse_q = lse_next, lse_x = lsex_next;
       if (u + 1 < n) {
         issue_item(kvb, __builtin_amdgcn_readlane(lj, u + 1), is);
-        lse_next = p.lse[(tok0 + qi) * K + __builtin_amdgcn_readlane(ls, u + 1)];
+        lse_next = p.lse[(tok0 + (XR ? opaque(qi) : qi)) * K + __builtin_amdgcn_readlane(ls, u + 1)];
         if (XR) lsex_next = p.lse[(tok0 + kS) * K + __builtin_amdgcn_readlane(ls, u + 1)];
       } else if (u == K - 1 && live_next && sN[pair][buf ^ 1] > 0) {
         issue_item(kvb_n, sJc[pair][buf ^ 1][0], is);
-        lse_next = p.lse[(tok_n + qi) * K + sSlot[pair][buf ^ 1][0]];
+        lse_next = p.lse[(tok_n + (XR ? opaque(qi) : qi)) * K + sSlot[pair][buf ^ 1][0]];
         if (XR) lsex_next = p.lse[(tok_n + kS) * K + sSlot[pair][buf ^ 1][0]];
       }
       if (comp) {
@@ -544,7 +558,7 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
     // ---- finish the chunk: dQ rows of this wave; zero dw partials of empty slots
     if (live) {
       const float as = p.attn_scale;
-      T* drow = reinterpret_cast<T*>(p.dq) + (tok0 + qi) * kD;
+      T* drow = reinterpret_cast<T*>(p.dq) + (tok0 + (XR ? opaque(qi) : qi)) * kD;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         store4(drow + 8 * g + 4 * hh, as * g0a[4 * g], as * g0a[4 * g + 1], as * g0a[4 * g + 2],
@@ -560,10 +574,13 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         sX[0].o[xh][lane] = hh ? t1 : t0;  // lane l: d = l
         block_barrier();
         if (xh == 0) {
+          // (lane-dependent addresses are formed here, not kept in registers
+          // across the whole loop)
+          const int ln = opaque(lane);
           const int64_t tx = tok0 + kS;
-          reinterpret_cast<T*>(p.dq)[tx * kD + lane] = (T)(as * (sX[0].o[0][lane] + sX[0].o[1][lane]));
+          reinterpret_cast<T*>(p.dq)[tx * kD + ln] = (T)(as * (sX[0].o[0][lane] + sX[0].o[1][lane]));
           if (lane < K && sJ[pair][buf][lane] >= 0) {
-            const int64_t o = cbase + lane * lq_len + kS;
+            const int64_t o = cbase + ln * lq_len + kS;
             p.ws.Dbuf[o] = sX[0].dl[0][lane];
             p.ws.Lbuf[o] = sX[0].dl[1][lane];
           }
@@ -577,15 +594,18 @@ __global__ __launch_bounds__(kThreads, kWgPerCu) void bwd_dq_kernel(BwdParams p,
         for (int e = lane; e < 32 * K; e += 64) {
           const int sl = e >> 5, q = e & 31;
           if (sJ[pair][buf][sl] >= 0) {
-            const int64_t o = cbase + sl * lq_len + 32 * half + q;
+            const int64_t o = cbase + sl * lq_len + 32 * half + (XR ? opaque(q) : q);
             p.ws.Dbuf[o] = sDL[wave][0][sl][q];
             p.ws.Lbuf[o] = sDL[wave][1][sl][q];
           }
         }
-        if (has_row && lane < K)
-          p.ws.dwp[(tglob * K + lane) * 2 + half] = sJ[pair][buf][lane] >= 0 ? sDw[wave][lane] : 0.f;
+        if (has_row && lane < K) {
+          const int sl = opaque(lane);
+          p.ws.dwp[(tglob * K + sl) * 2 + xh] = sJ[pair][buf][lane] >= 0 ? sDw[wave][lane] : 0.f;
+        }
       } else if (has_row && n < K && lane < K && sJ[pair][buf][lane] < 0) {
-        p.ws.dwp[(tglob * K + lane) * 2 + half] = 0.f;
+        const int sl = opaque(lane);
+        p.ws.dwp[(tglob * K + sl) * 2 + xh] = 0.f;
       }
     }
     g0a = zero16();
