@@ -134,6 +134,10 @@ SWEEP = [
     ("train_16k_bf16", dict(B=1, H=4, Hr=4, D=64, n_chunks=33, topk=3), False),   # per-head retrieval
     ("train_16k_bf16", dict(B=2, H=2, n_chunks=65, topk=32), True),      # off-by-one, k = 32
     ("train_16k_bf16", dict(B=1, H=2, n_chunks=700, topk=3), False),     # 1,400 chunks: uneven streams
+    # either side of the switch to the chip-wide window order (eight slices' K/V
+    # above 256 MiB: more than 2,048 bf16 chunks per slice)
+    ("train_16k_bf16", dict(B=1, H=1, n_chunks=2048, topk=2), False),
+    ("train_16k_bf16", dict(B=1, H=1, n_chunks=2049, topk=2), False),
     ("tiny_fp32_1k", dict(B=2, H=3, n_chunks=37, topk=6, whole_reseed=False), True),
     ("tiny_fp32_1k", dict(B=1, H=2, Hr=2, D=128, n_chunks=20, topk=9, whole_reseed=False), False),
     ("decode_16m_bf16", dict(H=4, n_chunks=3000, device_kv=False), False),
