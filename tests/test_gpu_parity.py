@@ -307,14 +307,16 @@ def test_xattn_only_entry_points(dev):
         assert max_abs_rel(host64(g[key]), ref) <= 1e-4, key
 
 
-@pytest.mark.parametrize("name", ["tiny_fp32_1k", "fwdbwd_64k_bf16"])
-def test_backward_hot_key_chunk(dev, name):
+@pytest.mark.parametrize("name,lmk_row", [("tiny_fp32_1k", False), ("fwdbwd_64k_bf16", False),
+                                          ("tiny_fp32_1k", True), ("fwdbwd_64k_bf16", True)])
+def test_backward_hot_key_chunk(dev, name, lmk_row):
     """Every row retrieves chunk 0 (599 retrievers, more than one staged batch of the
     key-stationary pass's list) plus up to two other earlier chunks, from an index set
-    chosen by the caller; forward and backward against the oracle."""
+    chosen by the caller; forward and backward against the oracle.  With S+1 rows the
+    LMK rows' staged contractions also cross those batch boundaries."""
     import torch
     from paper_2410_01651_amd import gca
-    w = get_workload(name, B=1, H=2, n_chunks=600, topk=4, whole_reseed=False)
+    w = get_workload(name, B=1, H=2, n_chunks=600, topk=4, whole_reseed=False, lmk_row=lmk_row)
     inp = gi.draw_tokens(w, with_dout=True)
     t = upload(w, inp, dev)
     p = problem_for(w)
@@ -334,10 +336,11 @@ def test_backward_hot_key_chunk(dev, name):
     out, lse, wt = gca.grouped_xattn_fwd(p, t["q"], t["k"], t["v"], ti, ts)
     x = decode_all(w, inp)
     w_ref = og.fusion_weights(sel.astype(np.float64))
-    o_ref, _ = og.xattn_fwd(x["q"], x["k"], x["v"], idx, w_ref, w.S, w.attn_scale)
+    sq = w.Sq if lmk_row else None
+    o_ref, _ = og.xattn_fwd(x["q"], x["k"], x["v"], idx, w_ref, w.S, w.attn_scale, Sq=sq)
     assert max_abs_rel(host64(out), o_ref) <= TOL[w.dtype]
     g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], ti, ts, lse, t["dout"], landmark_grads=False)
-    dq, dk, dv, dw = og.xattn_bwd(x["q"], x["k"], x["v"], idx, w_ref, x["dout"], w.S, w.attn_scale)
+    dq, dk, dv, dw = og.xattn_bwd(x["q"], x["k"], x["v"], idx, w_ref, x["dout"], w.S, w.attn_scale, Sq=sq)
     for key, ref in (("dq", dq), ("dk", dk), ("dv", dv), ("dsel", og.dsel_from_dw(w_ref, dw))):
         assert max_abs_rel(host64(g[key]), ref) <= TOL[w.dtype], key
 
