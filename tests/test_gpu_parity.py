@@ -182,6 +182,8 @@ BWD = [
     ("decode_16m_bf16", dict(H=2, n_chunks=300, planted=0, backward=True, device_kv=False), False),
     ("decode_16m_bf16", dict(H=2, n_chunks=100, topk=4, planted=0, dtype="fp32", backward=True,
                              device_kv=False), False),
+    # decode backward past the window-order threshold (one query chunk per head)
+    ("decode_16m_bf16", dict(H=2, n_chunks=2500, topk=8, planted=0, backward=True, device_kv=False), False),
 ]
 
 
