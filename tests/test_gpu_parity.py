@@ -503,6 +503,7 @@ LMK = [
     ("tiny_fp32_1k", dict(B=2, H=3, n_chunks=37, topk=6, whole_reseed=False), True),
     ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=700, topk=3), False),
     ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=2100, topk=3), False),   # window stream order
+    ("fwdbwd_64k_bf16", dict(B=1, H=1, n_chunks=2100, topk=12), True),   # window order, unstaged k, off-by-one
 ]
 
 
