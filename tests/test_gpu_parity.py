@@ -273,6 +273,70 @@ def test_landmark_gradients_one_at_a_time(dev, name, kw):
             assert np.array_equal(host64(part[key]), host64(both[key])), key
 
 
+@pytest.mark.parametrize("name,kw,backward", [
+    ("train_16k_bf16", dict(B=1, H=2, n_chunks=40, topk=8), True),
+    ("train_16k_bf16", dict(B=1, H=2, n_chunks=30, topk=5, lmk_row=True), True),
+    ("decode_16m_bf16", dict(H=2, n_chunks=3000, device_kv=False), False),
+])
+def test_graph_capture_replays(dev, name, kw, backward):
+    """The path captured into a HIP graph (the library enqueues kernels only, no
+    allocation or memset) and replayed three times, with eager work and a clear of
+    every output between replays: each replay reproduces the eager call bit for bit."""
+    import torch
+    from paper_2410_01651_amd import gca
+    w, inp = _case(name, **kw)
+    if backward and "dout" not in inp:
+        inp["dout"] = gi.draw_slices(w, "dout", (w.B, w.H, w.Lq, w.d))
+    t = upload(w, inp, dev)
+    p = problem_for(w)
+    sh = gca.shapes(p)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    outs = {"out": torch.empty(sh.q, dtype=dt, device=dev), "idx": torch.empty(sh.rows, dtype=torch.int32, device=dev),
+            "sel": torch.empty(sh.rows, dtype=torch.float32, device=dev),
+            "lse": torch.empty(sh.lse, dtype=torch.float32, device=dev),
+            "w": torch.empty(sh.rows, dtype=torch.float32, device=dev)}
+    wsf, _ = gca.workspace(p, gca.OP_FORWARD, dev)
+    grads = {}
+    if backward:
+        grads = {"dq": torch.empty(sh.q, dtype=dt, device=dev), "dk": torch.empty(sh.kv, dtype=dt, device=dev),
+                 "dv": torch.empty(sh.kv, dtype=dt, device=dev),
+                 "dsel": torch.empty(sh.rows, dtype=torch.float32, device=dev),
+                 "dlmk_q": torch.empty(sh.lmk_q, dtype=torch.float32, device=dev),
+                 "dlmk_k": torch.empty(sh.lmk_k, dtype=torch.float32, device=dev)}
+        wsb, _ = gca.workspace(p, gca.OP_BACKWARD, dev)
+
+    def step():
+        gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"], ws=wsf, **outs)
+        if backward:
+            gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], outs["idx"], outs["sel"], outs["lse"], t["dout"],
+                                  t["lmk_q"], t["lmk_k"], ws=wsb, grads=grads)
+
+    every = dict(outs, **grads)
+    step()
+    torch.cuda.synchronize()
+    eager = {k: v.clone() for k, v in every.items()}
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for rep in range(3):
+        for v in every.values():
+            v.fill_(-7)
+        junk = (t["q"].float() * 3.0).sum()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k, v in every.items():
+            assert torch.equal(v, eager[k]), (rep, k)
+        assert torch.isfinite(junk)
+    del g
+
+
 def test_xattn_only_entry_points(dev):
     """gca_grouped_xattn_fwd / _bwd driven with an index set chosen by the caller,
     including pad slots in the middle and an out-of-range index (treated as a pad)."""
