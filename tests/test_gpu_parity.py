@@ -651,6 +651,41 @@ def test_side_stream(dev):
         assert torch.equal(g0[key], g1[key]), key
 
 
+def test_concurrent_streams(dev):
+    """Two different problems in flight at once on two streams (each call with its
+    own workspace: the library keeps no per-call state of its own), interleaved
+    launch by launch, give bit for bit what each gives alone."""
+    import torch
+    from paper_2410_01651_amd import gca
+    cases = [_case("fwdbwd_64k_bf16", B=1, H=4, n_chunks=96, topk=8),
+             _case("train_16k_bf16", B=2, H=3, n_chunks=70, topk=5, lmk_row=True)]
+    probs, ts, alone = [], [], []
+    for w, inp in cases:
+        if "dout" not in inp:
+            inp["dout"] = gi.draw_slices(w, "dout", (w.B, w.H, w.Lq, w.d))
+        t = upload(w, inp, dev)
+        p = problem_for(w)
+        f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+        g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                                  t["lmk_q"], t["lmk_k"])
+        probs.append(p)
+        ts.append(t)
+        alone.append(dict(f, **g))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for rep in range(3):
+        fs = [gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"], stream=s)
+              for p, t, s in zip(probs, ts, streams)]
+        gs = [gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                                    t["lmk_q"], t["lmk_k"], stream=s)
+              for p, t, f, s in zip(probs, ts, fs, streams)]
+        for s in streams:
+            s.synchronize()
+        for ref, f, g in zip(alone, fs, gs):
+            for key, v in dict(f, **g).items():
+                assert torch.equal(v, ref[key]), (rep, key)
+
+
 _DEBUG_SYNC_CHILD = r"""
 import hashlib, sys
 sys.path.insert(0, sys.argv[1])
