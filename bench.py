@@ -203,7 +203,8 @@ def measured_mfma(kernel):
     k = _profile_entry("mfma_counters.json", kernel)
     if k is None:
         return None
-    return {key: k.get(key) for key in ("mfma_busy_frac", "mfma_bf16_flops_per_launch", "l2_hit_frac")}
+    return {key: k.get(key) for key in ("mfma_busy_frac", "mfma_bf16_flops_per_launch", "l2_hit_frac",
+                                        "l2_miss_read_latency_cycles")}
 
 
 def flops_per_unit():

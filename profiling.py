@@ -133,15 +133,20 @@ def agent_counts(counter_csv: str):
     raise SystemExit(f"no GPU agent in {path}")
 
 
-def counters(mfma_csv: str, l2_csv: str, cmd: str, tag: str = "") -> dict:
+def counters(mfma_csv: str, l2_csv: str, cmd: str, tag: str = "", ea_csv: str = "") -> dict:
     """Matrix-core busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over the busy cycles of
     every SIMD, the MfmaUtil definition: GRBM_GUI_ACTIVE is reported summed over the
     XCCs, so one XCC's count is the sum divided by their number), bf16 matrix-core
     flops (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) and the L2 hit fraction (TCC_HIT /
-    (TCC_HIT + TCC_MISS)) per launch, the median over each kernel's dispatches."""
+    (TCC_HIT + TCC_MISS)) per launch, the median over each kernel's dispatches.
+    With `ea_csv` (TCC_EA0_RDREQ_LEVEL_sum, TCC_EA0_RDREQ_sum) also the average
+    latency of the reads that leave the L2 (requests in flight summed per cycle
+    over requests): this stack exposes no last-level-cache (MALL) counter, and
+    this latency is where its hits show (lower than reads served by HBM)."""
     simds, xccs = agent_counts(mfma_csv)
     m = _per_kernel_all(mfma_csv)
     l2 = _per_kernel_all(l2_csv) if l2_csv else {}
+    ea = _per_kernel_all(ea_csv) if ea_csv else {}
     med = statistics.median
     kernels = {}
     for k, c in sorted(m.items()):
@@ -162,6 +167,10 @@ def counters(mfma_csv: str, l2_csv: str, cmd: str, tag: str = "") -> dict:
             fr = [a / (a + b) for a, b in zip(h["TCC_HIT_sum"], h["TCC_MISS_sum"]) if a + b > 0]
             e["l2_hit_frac"] = med(fr) if fr else None
             e["l2_requests_per_launch"] = med([a + b for a, b in zip(h["TCC_HIT_sum"], h["TCC_MISS_sum"])])
+        x = ea.get(k, {})
+        if "TCC_EA0_RDREQ_LEVEL_sum" in x and "TCC_EA0_RDREQ_sum" in x:
+            lat = [a / b for a, b in zip(x["TCC_EA0_RDREQ_LEVEL_sum"], x["TCC_EA0_RDREQ_sum"]) if b > 0]
+            e["l2_miss_read_latency_cycles"] = med(lat) if lat else None
         kernels[k + ("@" + tag if tag else "")] = e
     return {"source_sha256": source_hash(), "simds": simds, "xccs": xccs, "command": [cmd], "kernels": kernels}
 
@@ -186,13 +195,14 @@ def main():
     c.add_argument("--mfma", required=True, help="counter CSV with SQ_VALU_MFMA_BUSY_CYCLES, "
                                                  "SQ_INSTS_VALU_MFMA_MOPS_BF16, GRBM_GUI_ACTIVE")
     c.add_argument("--l2", default="", help="counter CSV with TCC_HIT_sum, TCC_MISS_sum")
+    c.add_argument("--ea", default="", help="counter CSV with TCC_EA0_RDREQ_LEVEL_sum, TCC_EA0_RDREQ_sum")
     c.add_argument("--cmd", required=True)
     c.add_argument("--out", required=True)
     c.add_argument("--tag", default="")
     c.add_argument("--append", action="store_true")
     args = ap.parse_args()
     if args.what == "counters":
-        data = counters(args.mfma, args.l2, args.cmd, args.tag)
+        data = counters(args.mfma, args.l2, args.cmd, args.tag, args.ea)
         if args.append and os.path.exists(args.out):
             old = json.load(open(args.out))
             if old.get("source_sha256") != data["source_sha256"]:
