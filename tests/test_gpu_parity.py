@@ -187,6 +187,48 @@ BWD = [
 ]
 
 
+def _random_cases(n, seed=20241001):
+    """n seeded random small configurations across the problem options."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        base = "tiny_fp32_1k" if rng.random() < 0.3 else "fwdbwd_64k_bf16"
+        H = int(rng.integers(1, 5))
+        per_head = bool(rng.random() < 0.3)
+        kw = dict(B=int(rng.integers(1, 3)), H=H, n_chunks=int(rng.integers(1, 48)), topk=int(rng.integers(1, 17)),
+                  lmk_row=bool(rng.random() < 0.3))
+        if per_head:
+            kw.update(Hr=H, D=int(rng.choice([64, 128, 192])))
+        else:
+            kw.update(D=int(rng.choice([64, 256, 512, 768, 1024])))
+        if base == "tiny_fp32_1k":
+            kw["whole_reseed"] = False
+        out.append((f"r{i}", base, kw, bool(rng.random() < 0.4)))
+    return out
+
+
+@pytest.mark.parametrize("tag,name,kw,obo", _random_cases(40))
+def test_random_sweep(dev, tag, name, kw, obo):
+    """Seeded random small problems (batch, heads, shared or per-head retrieval,
+    landmark width, k from 1 to 16 with chunk counts around and below it, S or S+1
+    query rows, off-by-one, fp32 or bf16): forward and every gradient against the
+    oracle."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case(name, **kw)
+    if "dout" not in inp:
+        inp["dout"] = gi.draw_slices(w, "dout", (w.B, w.H, w.Lq, w.d))
+    t = upload(w, inp, dev)
+    p = problem_for(w, off_by_one=obo)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    ref = _check_forward(w, inp, f, off_by_one=obo)
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                              t["lmk_q"], t["lmk_k"])
+    x = decode_all(w, inp)
+    rb = og.backward(oracle_params(w, obo), ref, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"], x["dout"])
+    for key in ("dq", "dk", "dv", "dsel", "dlmk_q", "dlmk_k"):
+        assert max_abs_rel(host64(g[key]), rb[key]) <= TOL[w.dtype], key
+
+
 @pytest.mark.parametrize("name,kw,obo", BWD)
 def test_backward(dev, name, kw, obo):
     """dq, dk, dv, dsel and both landmark gradients against the oracle's chain rule."""
