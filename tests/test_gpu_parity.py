@@ -229,6 +229,37 @@ def test_random_sweep(dev, tag, name, kw, obo):
         assert max_abs_rel(host64(g[key]), rb[key]) <= TOL[w.dtype], key
 
 
+def _random_decode_cases(n, seed=20241002):
+    """n seeded random decode problems (past chunks from 1 to 6,000; the K/V of
+    the larger ones over fewer heads)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        nc, B = int(rng.integers(1, 6001)), int(rng.integers(1, 3))
+        # heads capped so that the drawn K/V cache stays small (B * H * nc <= 2,500)
+        H = max(1, min(int(rng.integers(1, 9)), 2500 // (B * nc)))
+        kw = dict(B=B, H=H, n_chunks=nc, topk=int(rng.integers(1, 33)),
+                  planted=0, device_kv=False, dtype="fp32" if rng.random() < 0.3 else "bf16")
+        if rng.random() < 0.3:
+            kw.update(Hr=H, D=int(rng.choice([64, 128])))
+        else:
+            kw.update(D=int(rng.choice([64, 192, 512, 1024, 2048])))
+        out.append((f"d{i}", kw, bool(rng.random() < 0.3)))
+    return out
+
+
+@pytest.mark.parametrize("tag,kw,obo", _random_decode_cases(24))
+def test_random_decode_sweep(dev, tag, kw, obo):
+    """Seeded random decode problems (batch, heads, shared or per-head retrieval,
+    landmark width, k up to 32, past lengths from 1 chunk up, off-by-one, fp32/bf16):
+    the decode scan, merge and attention against the oracle."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case("decode_16m_bf16", **kw)
+    t = upload(w, inp, dev)
+    f = gca.forward(problem_for(w, off_by_one=obo), t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    _check_forward(w, inp, f, off_by_one=obo)
+
+
 @pytest.mark.parametrize("name,kw,obo", BWD)
 def test_backward(dev, name, kw, obo):
     """dq, dk, dv, dsel and both landmark gradients against the oracle's chain rule."""
