@@ -203,6 +203,8 @@ def _random_cases(n, seed=20241001):
             kw.update(D=int(rng.choice([64, 256, 512, 768, 1024])))
         if base == "tiny_fp32_1k":
             kw["whole_reseed"] = False
+        if rng.random() < 0.3:
+            kw["gumbel_seed"] = int(rng.integers(1, 2**31))
         out.append((f"r{i}", base, kw, bool(rng.random() < 0.4)))
     return out
 
@@ -211,8 +213,8 @@ def _random_cases(n, seed=20241001):
 def test_random_sweep(dev, tag, name, kw, obo):
     """Seeded random small problems (batch, heads, shared or per-head retrieval,
     landmark width, k from 1 to 16 with chunk counts around and below it, S or S+1
-    query rows, off-by-one, fp32 or bf16): forward and every gradient against the
-    oracle."""
+    query rows, off-by-one, Gumbel top-k, fp32 or bf16): forward and every gradient
+    against the oracle."""
     from paper_2410_01651_amd import gca
     w, inp = _case(name, **kw)
     if "dout" not in inp:
@@ -244,6 +246,8 @@ def _random_decode_cases(n, seed=20241002):
             kw.update(Hr=H, D=int(rng.choice([64, 128])))
         else:
             kw.update(D=int(rng.choice([64, 192, 512, 1024, 2048])))
+        if rng.random() < 0.3:
+            kw["gumbel_seed"] = int(rng.integers(1, 2**31))
         out.append((f"d{i}", kw, bool(rng.random() < 0.3)))
     return out
 
@@ -251,8 +255,8 @@ def _random_decode_cases(n, seed=20241002):
 @pytest.mark.parametrize("tag,kw,obo", _random_decode_cases(24))
 def test_random_decode_sweep(dev, tag, kw, obo):
     """Seeded random decode problems (batch, heads, shared or per-head retrieval,
-    landmark width, k up to 32, past lengths from 1 chunk up, off-by-one, fp32/bf16):
-    the decode scan, merge and attention against the oracle."""
+    landmark width, k up to 32, past lengths from 1 chunk up, off-by-one, Gumbel
+    top-k, fp32/bf16): the decode scan, merge and attention against the oracle."""
     from paper_2410_01651_amd import gca
     w, inp = _case("decode_16m_bf16", **kw)
     t = upload(w, inp, dev)
