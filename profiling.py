@@ -6,6 +6,8 @@
         [--tag WORKLOAD --append]
     python profiling.py counters --mfma DIR3/run_counter_collection.csv --l2 DIR4/run_counter_collection.csv \
         --cmd "..." --out profiles/mfma_counters.json [--tag WORKLOAD --append]
+    python profiling.py issue --csv DIR5/run_counter_collection.csv [--csv DIR6/...] \
+        --cmd "..." --out profiles/simd_issue_breakdown.json
 
 `traffic` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
 launch for every GCA kernel, scaled by what the same counters read for a plain
@@ -175,6 +177,67 @@ def counters(mfma_csv: str, l2_csv: str, cmd: str, tag: str = "", ea_csv: str = 
     return {"source_sha256": source_hash(), "simds": simds, "xccs": xccs, "command": [cmd], "kernels": kernels}
 
 
+def issue(csvs, cmd: str) -> dict:
+    """Where each SIMD's cycles go, per launch of the attention kernels, from SQ
+    counter runs that each include GRBM_GUI_ACTIVE (medians over dispatches).
+
+    SIMD fractions (of GRBM_GUI_ACTIVE per XCC times the SIMD count): VALU issue
+    (SQ_ACTIVE_INST_VALU, quad-cycles, so x4; it counts every VALU-class
+    instruction's issue, matrix-core ones included), matrix cores busy
+    (SQ_VALU_MFMA_BUSY_CYCLES), both at once (SQ_VALU_MFMA_COEXEC_CYCLES) and
+    neither (the rest).  Wave fractions (of SQ_WAVE_CYCLES, quad-cycles like the
+    others): issuing any instruction, waiting at s_waitcnt or a barrier
+    (SQ_WAIT_ANY), and ready but not issued (SQ_WAIT_INST_ANY: a dependency or
+    another wave holding the unit).  Per wave: instruction counts by class."""
+    simds, xccs = agent_counts(csvs[0])
+    med = statistics.median
+    per = {}
+    for path in csvs:
+        for k, c in _per_kernel_all(path).items():
+            if k not in ("xattn_fwd_kernel", "bwd_dq_kernel", "bwd_dkdv_kernel"):
+                continue
+            gui = c.get("GRBM_GUI_ACTIVE")
+            for name, vals in c.items():
+                if name == "GRBM_GUI_ACTIVE":
+                    continue
+                # each run's own clock normalises its own counters
+                per.setdefault(k, {})[name] = (med(vals), med(gui))
+    kernels = {}
+    for k, c in sorted(per.items()):
+        def simd(name, quad=False):
+            v, g = c[name]
+            return v * (4.0 if quad else 1.0) / (g / xccs * simds)
+        def wave(name):
+            return c[name][0] / c["SQ_WAVE_CYCLES"][0]
+        e = {}
+        if "SQ_ACTIVE_INST_VALU" in c:
+            e["simd_valu_issue_frac"] = simd("SQ_ACTIVE_INST_VALU", quad=True)
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+            e["simd_mfma_busy_frac"] = simd("SQ_VALU_MFMA_BUSY_CYCLES")
+        if "SQ_VALU_MFMA_COEXEC_CYCLES" in c:
+            e["simd_valu_and_mfma_frac"] = simd("SQ_VALU_MFMA_COEXEC_CYCLES")
+        if all(x in e for x in ("simd_valu_issue_frac", "simd_mfma_busy_frac", "simd_valu_and_mfma_frac")):
+            e["simd_neither_frac"] = 1.0 - e["simd_valu_issue_frac"] - e["simd_mfma_busy_frac"] + \
+                e["simd_valu_and_mfma_frac"]
+        if "SQ_WAVE_CYCLES" in c:
+            for name, key in (("SQ_ACTIVE_INST_ANY", "wave_issuing_frac"), ("SQ_WAIT_ANY", "wave_waitcnt_or_barrier_frac"),
+                              ("SQ_WAIT_INST_ANY", "wave_ready_not_issued_frac"),
+                              ("SQ_WAIT_INST_LDS", "wave_lds_wait_frac")):
+                if name in c:
+                    e[key] = wave(name)
+        if "SQ_WAVES" in c:
+            n = c["SQ_WAVES"][0]
+            e["waves"] = n
+            for name, key in (("SQ_INSTS_VALU", "valu"), ("SQ_INSTS_MFMA", "mfma"), ("SQ_INSTS_LDS", "lds"),
+                              ("SQ_INSTS_SALU", "salu"), ("SQ_INSTS_VALU_TRANS_F32", "valu_trans_f32")):
+                if name in c:
+                    e.setdefault("instructions_per_wave", {})[key] = c[name][0] / n
+        if "SQ_LDS_BANK_CONFLICT" in c:
+            e["lds_bank_conflict_cycles_per_launch"] = c["SQ_LDS_BANK_CONFLICT"][0]
+        kernels[k] = e
+    return {"source_sha256": source_hash(), "simds": simds, "xccs": xccs, "command": [cmd], "kernels": kernels}
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="what", required=True)
@@ -200,7 +263,15 @@ def main():
     c.add_argument("--out", required=True)
     c.add_argument("--tag", default="")
     c.add_argument("--append", action="store_true")
+    d = sub.add_parser("issue")
+    d.add_argument("--csv", action="append", required=True, help="counter CSV of one SQ counter run")
+    d.add_argument("--cmd", required=True)
+    d.add_argument("--out", required=True)
     args = ap.parse_args()
+    if args.what == "issue":
+        json.dump(issue(args.csv, args.cmd), open(args.out, "w"), indent=1)
+        print(args.out)
+        return
     if args.what == "counters":
         data = counters(args.mfma, args.l2, args.cmd, args.tag, args.ea)
         if args.append and os.path.exists(args.out):
