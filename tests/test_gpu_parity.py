@@ -312,6 +312,38 @@ def test_backward_saturated_weights(dev):
         assert max_abs_rel(host64(g[key]), rb[key]) <= TOL[w.dtype], key
 
 
+@pytest.mark.parametrize("name,kw,obo", [("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=24, topk=4), False),
+                                         ("fwdbwd_64k_bf16", dict(B=1, H=2, n_chunks=24, topk=4), True),
+                                         ("tiny_fp32_1k", dict(B=1, H=2, n_chunks=20, topk=3), False)])
+def test_large_logits(dev, name, kw, obo):
+    """Q and K scaled by 4 (exact in both dtypes: a power of two), so the attention
+    logits reach tens of nats and each chunk's softmax is nearly one-hot: the
+    shifted exponentials, the log-sum-exp and the backward's cancellations in
+    dP - D stay finite and match the oracle."""
+    from paper_2410_01651_amd import gca
+    w, inp = _case(name, backward=True, **kw)
+    for key in ("q", "k"):
+        inp[key] = gi.encode(w, gi.decode(w, inp[key]) * 4.0)
+    t = upload(w, inp, dev)
+    p = problem_for(w, off_by_one=obo)
+    f = gca.forward(p, t["lmk_q"], t["lmk_k"], t["q"], t["k"], t["v"])
+    x = decode_all(w, inp)
+    pp = oracle_params(w, obo)
+    rf = og.forward(pp, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"])
+    np.testing.assert_array_equal(f["idx"].cpu().numpy(), rf["idx"])
+    lse = rf["lse"][np.isfinite(rf["lse"])]
+    assert lse.max() - lse.min() > 40.0  # the logits really are large
+    tol = TOL[w.dtype]
+    for key in ("out", "lse", "w"):
+        assert max_abs_rel(host64(f[key]), rf[key]) <= tol, key
+    g = gca.grouped_xattn_bwd(p, t["q"], t["k"], t["v"], f["idx"], f["sel"], f["lse"], t["dout"],
+                              t["lmk_q"], t["lmk_k"])
+    rb = og.backward(pp, rf, x["lmk_q"], x["lmk_k"], x["q"], x["k"], x["v"], x["dout"])
+    for key in ("dq", "dk", "dv", "dsel", "dlmk_q", "dlmk_k"):
+        e = max_abs_rel(host64(g[key]), rb[key])
+        assert e <= tol, (key, e)
+
+
 def test_backward_deterministic(dev):
     """No floating-point atomics: two backward passes are bit-identical."""
     from paper_2410_01651_amd import gca
