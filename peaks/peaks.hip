@@ -31,17 +31,24 @@ __global__ __launch_bounds__(256) void stream_read_kernel(const u32x4* __restric
 }
 
 // Each workgroup reads whole 16 KiB tiles chosen by idx[] (tile t at p + idx[t] *
-// 16 KiB), 64 bytes per thread per tile: the access pattern of the attention
-// kernels' gathers of one retrieved chunk's K or V pair, without the compute.
+// 16 KiB), 64 bytes per thread per tile, T tiles in flight: the access pattern of
+// the attention kernels' gathers of one retrieved chunk's K or V pair, without
+// the compute.
+template <int T>
 __global__ __launch_bounds__(256) void tile_gather_kernel(const u32x4* __restrict__ p,
                                                           const int32_t* __restrict__ idx, int n, uint32_t key,
                                                           uint32_t* __restrict__ sink) {
   u32x4 acc = u32x4{0u, 0u, 0u, 0u};
-  for (int t = blockIdx.x; t < n; t += gridDim.x) {
-    const u32x4* tile = p + (int64_t)idx[t] * 1024;
-    const u32x4 a = tile[threadIdx.x], b = tile[threadIdx.x + 256];
-    const u32x4 c = tile[threadIdx.x + 512], d = tile[threadIdx.x + 768];
-    acc ^= a ^ b ^ c ^ d;
+  for (int t = blockIdx.x * T; t < n; t += gridDim.x * T) {
+    u32x4 v[T][4];
+#pragma unroll
+    for (int u = 0; u < T; ++u) {
+      const u32x4* tile = p + (int64_t)idx[t + u < n ? t + u : t] * 1024;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) v[u][c] = tile[threadIdx.x + 256 * c];
+    }
+#pragma unroll
+    for (int u = 0; u < T; ++u) acc ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
   }
   const uint32_t f = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
   if (f == key) sink[0] = f;
@@ -85,10 +92,16 @@ int peaks_stream_read(const void* p, int64_t n16, int blocks, void* sink, hipStr
 }
 
 // Launch the gather of n 16 KiB tiles at p, tile t being p + idx[t] * 16 KiB
-// (idx: n device int32 values, each below the number of whole tiles at p).
-int peaks_tile_gather(const void* p, const void* idx, int n, int blocks, void* sink, hipStream_t stream) {
-  hipLaunchKernelGGL(tile_gather_kernel, dim3(blocks), dim3(256), 0, stream, (const u32x4*)p, (const int32_t*)idx, n,
-                     0x9E3779B9u, (uint32_t*)sink);
+// (idx: n device int32 values, each below the number of whole tiles at p), with
+// `in_flight` (1 or 2) tiles per workgroup at a time.
+int peaks_tile_gather(const void* p, const void* idx, int n, int blocks, int in_flight, void* sink,
+                      hipStream_t stream) {
+  if (in_flight == 2)
+    hipLaunchKernelGGL(tile_gather_kernel<2>, dim3(blocks), dim3(256), 0, stream, (const u32x4*)p,
+                       (const int32_t*)idx, n, 0x9E3779B9u, (uint32_t*)sink);
+  else
+    hipLaunchKernelGGL(tile_gather_kernel<1>, dim3(blocks), dim3(256), 0, stream, (const u32x4*)p,
+                       (const int32_t*)idx, n, 0x9E3779B9u, (uint32_t*)sink);
   return (int)hipGetLastError();
 }
 
